@@ -1,0 +1,192 @@
+"""Benchmark of the routed-MoE layer on one MI355X.
+
+One step = one layer forward over one batch: route -> permute -> grouped FP4
+GEMM (activation quantisation, gate/up + SwiGLU, down) -> fixed-order combine,
+all in the library's HIP kernels, inputs resident in HBM.
+
+Default workload: the decode-shaped layer (T=64, H=4096, 256 routed experts
+top-8 + 1 shared, I=2048), whose throughput is `value`. The 8K-token prefill
+layer (same dims) is measured beside it and reported under "prefill".
+
+Prints ONE JSON line (see the design doc for every field's definition).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_PEAK_FP8_TFLOPS = 5000.0  # dense FP8 (the FP8 x FP4 scaled MFMA issue rate)
+MFMA_PEAK_FP4_TFLOPS = 10100.0  # dense MXFP4
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def expert_bytes(H, I):
+    """Packed FP4 codes + E8M0 scales of one expert: (W13, W2)."""
+    return 2 * I * H // 2 + 2 * I * H // 32, H * I // 2 + H * I // 32
+
+
+def measure(cfg, weights_np, steps, warmup, fmt):
+    import torch
+
+    import synth
+    from paper_2609_15627_amd import moe
+
+    dev = torch.device("cuda:0")
+    x_np = synth.gen_x(cfg)
+    logits_np = synth.gen_logits(cfg)
+    x = torch.from_numpy(x_np.view(np.int16)).to(dev).view(torch.bfloat16)
+    logits = torch.from_numpy(logits_np).to(dev)
+    w = tuple(torch.from_numpy(a[: cfg.NE]).to(dev) for a in weights_np)
+    layer = moe.MoELayer(cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.n_shared, fmt, device=dev)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(warmup):
+        layer.forward(x, w, logits=logits)
+    torch.cuda.synchronize()
+    variant = moe.moe_last_variant()
+
+    # timed region: K steps, per-step events between the steps of the layer
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for i in range(steps):
+        layer.forward(x, w, logits=logits, events=ev[i])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t0.elapsed_time(t1)
+    names = ["route", "permute", "quant_tiles", "gate_up", "down", "combine"]
+    stage_ms = {n: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in ev]))
+                for j, n in enumerate(names)}
+
+    counts = layer.perm[0].cpu().numpy()
+    touched = int((counts > 0).sum())
+    A = cfg.A
+    w13b, w2b = expert_bytes(cfg.H, cfg.I)
+    xb = cfg.T * cfg.H * (1 + 1 / 32)                      # MXFP8 x codes + scales
+    hb = A * cfg.I * (1 + 1 / 32)                           # MXFP8 h codes + scales
+    gate_up_bytes = touched * w13b + xb + hb
+    down_bytes = touched * w2b + hb + A * cfg.H * 4
+    layer_bytes = touched * (w13b + w2b) + cfg.T * cfg.H * 2 * 2 + cfg.T * cfg.E * 4
+    gate_up_flops = 4.0 * cfg.H * cfg.I * A
+    layer_flops = 6.0 * cfg.H * cfg.I * A
+    ms = total_ms / steps
+    return dict(ms_per_step=ms, wall_s=wall, tokens_per_s=cfg.T / (ms * 1e-3), stage_ms=stage_ms,
+                touched=touched, variant=variant, gate_up_bytes=gate_up_bytes,
+                down_bytes=down_bytes, layer_bytes=layer_bytes, gate_up_flops=gate_up_flops,
+                layer_flops=layer_flops)
+
+
+def cpu_baseline(cfg, weights_np, ntok, fmt):
+    """The fp64 oracle, as it is, on a bounded token sample of the same workload."""
+    import synth
+    from oracle import moe as omoe
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    x = synth.gen_x(cfg)
+    logits = synth.gen_logits(cfg)
+    tokens = np.arange(ntok)
+    t = time.perf_counter()
+    omoe.layer(x, *weights_np, k=cfg.k, n_shared=cfg.n_shared, logits=logits, fmt=fmt,
+               tokens=tokens)
+    dt = time.perf_counter() - t
+    return {"value": ntok / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{ntok} of {cfg.T} tokens of the {cfg.name} layer (all {cfg.k}+"
+                      f"{cfg.n_shared} experts of each; routing of all tokens), {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="decode")
+    ap.add_argument("--fmt", default="e4m3", choices=["e4m3", "e2m1"])
+    ap.add_argument("--no-prefill", action="store_true", help="skip the 8K prefill measurement")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=2)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = synth.CONFIGS[args.config]
+    log(f"generating weights for {cfg.name}")
+    weights_np = synth.gen_all_experts(cfg.with_(E=cfg.E, n_shared=max(cfg.n_shared, 0)))
+    log("measuring")
+    r = measure(cfg, weights_np, args.steps, args.warmup, args.fmt)
+    log(f"{cfg.name}: {r['ms_per_step']:.4f} ms/step, stages {r['stage_ms']}")
+    gu_ms = r["stage_ms"]["gate_up"]
+    achieved = r["gate_up_bytes"] / (gu_ms * 1e-3) / 1e9
+    line = {
+        "metric": "MoE-layer tokens/s",
+        "value": r["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": r["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": f"mx{'fp8' if args.fmt == 'e4m3' else 'fp4'}x{'fp4'} (fp32 accumulate)",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: T={cfg.T} H={cfg.H} E={cfg.E}+{cfg.n_shared} "
+                               f"k={cfg.k} I={cfg.I}, FP4 e2m1 weights with E8M0 per-32 scales",
+                   "global_batch": cfg.T, "act_format": args.fmt,
+                   "experts_touched": r["touched"], "variant": r["variant"]},
+        "roofline": {"kernel": "gate_up (stage 1)", "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None},
+        "stage_ms": r["stage_ms"],
+        "layer_hbm_frac": r["layer_bytes"] / (r["ms_per_step"] * 1e-3) / 1e9 / HBM_PEAK_GBS,
+    }
+    if not args.no_prefill and cfg.name == "decode":
+        pcfg = synth.CONFIGS["prefill8k"]
+        log("measuring prefill8k")
+        p = measure(pcfg, weights_np, max(3, args.steps // 10), 2, args.fmt)
+        gu = p["stage_ms"]["gate_up"]
+        tf = p["gate_up_flops"] / (gu * 1e-3) / 1e12
+        line["prefill"] = {
+            "workload": f"prefill8k: T={pcfg.T}, same dims", "tokens_per_s": p["tokens_per_s"],
+            "ms_per_step": p["ms_per_step"], "stage_ms": p["stage_ms"], "variant": p["variant"],
+            "roofline": {"kernel": "gate_up (stage 1)", "bound": "mfma", "achieved": tf,
+                         "peak": MFMA_PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
+                         "frac": tf / MFMA_PEAK_FP8_TFLOPS,
+                         "frac_of_fp4_peak": tf / MFMA_PEAK_FP4_TFLOPS, "traffic": None},
+            "layer_mfma_frac_of_fp4_peak": p["layer_flops"] / (p["ms_per_step"] * 1e-3) / 1e12
+            / MFMA_PEAK_FP4_TFLOPS,
+        }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        line["cpu_baseline"] = cpu_baseline(cfg, weights_np, args.cpu_tokens, args.fmt)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

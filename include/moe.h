@@ -1,0 +1,231 @@
+/*
+ * moe.h -- C ABI of the routed mixture-of-experts layer for AMD gfx950 (MI355X).
+ *
+ * The layer (paper: System and model context / Execution structure, Fig.
+ * architecture) routes every token to its top-k experts, runs each expert's
+ * gate/up projection, SwiGLU and down projection on FP4 e2m1 weights with
+ * per-32 E8M0 block scales, runs an always-on shared expert beside them, and
+ * sums the weighted partial outputs in a fixed order. A layer forward is:
+ *
+ *   moe_router_logits   (optional: logits from bf16 router weights)
+ *   moe_route_topk      -> topk_ids, topk_w
+ *   moe_permute         -> counts, offsets, sorted, pos
+ *   moe_fp4_grouped_gemm-> partials (one fp32 row per (token, slot))
+ *   moe_combine_fixed_order -> out (bf16)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every array pointer is a DEVICE pointer owned by the caller. The library
+ *    never allocates, frees or synchronises; it only enqueues kernels on
+ *    `stream` (a hipStream_t passed as void*; NULL is the default stream).
+ *    Buffers must stay alive until the stream has passed the call.
+ *  - Arrays are dense row-major and little-endian. bf16 values are passed as
+ *    their uint16_t bit patterns.
+ *  - FP4 e2m1 weight codes are packed two per byte: element 2i in bits 0-3,
+ *    element 2i+1 in bits 4-7. An e2m1 code has bit 3 = sign, bits 2-1 =
+ *    exponent (bias 1), bit 0 = mantissa: values 0, .5, 1, 1.5, 2, 3, 4, 6 and
+ *    their negatives.
+ *  - E8M0 scales are one byte per 32 consecutive elements along the reduction
+ *    axis; byte b means 2^(b-127) (255 is NaN and is rejected nowhere: it is a
+ *    caller precondition, like finite inputs).
+ *  - Scales are passed in their LOGICAL layout ([rows, K/32], unshuffled): the
+ *    paper found that packed weights do not imply an unshuffled scale layout
+ *    (Correctness recovery / Later numerical and integration repairs).
+ *  - Arguments are validated on the host before anything is enqueued; a bad
+ *    argument returns MOE_ERR_INVALID_ARG (or MOE_ERR_WORKSPACE) and enqueues
+ *    nothing. A failed kernel launch returns MOE_ERR_LAUNCH. No C++ exception
+ *    crosses this boundary. Sizes of zero tokens are valid and enqueue only
+ *    what is needed to define the outputs.
+ *  - Results are deterministic: no call uses floating-point atomics or split
+ *    reductions, so repeated calls on the same inputs give identical bits.
+ */
+#ifndef MOE_H_
+#define MOE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = 1, /* null pointer, bad size, unsupported shape */
+  MOE_ERR_UNSUPPORTED = 2, /* valid request that this build does not implement */
+  MOE_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the query said */
+  MOE_ERR_LAUNCH = 4       /* a kernel launch failed (HIP error) */
+} moe_status;
+
+/* Element format of the activations fed to the matrix cores (OCP MX v1.0):
+ * each block of 32 values shares one E8M0 scale. The paper's gfx90a kernels
+ * quantised activations to INT8 per 32 elements (Historical TP4 decode
+ * optimization / Parallel decomposition); gfx950's scaled MFMA consumes MX
+ * formats instead. */
+typedef enum {
+  MOE_ACT_MXFP8_E4M3 = 0, /* 1 byte per element */
+  MOE_ACT_MXFP6_E2M3 = 1, /* reserved: not implemented in this build */
+  MOE_ACT_MXFP4_E2M1 = 2  /* 2 elements per byte, low nibble first */
+} moe_act_format;
+
+/* Geometry variants reported by moe_last_variant(). */
+enum {
+  MOE_VARIANT_NONE = 0,
+  MOE_VARIANT_STREAM = 1, /* weight-streaming geometry for few rows per expert (decode) */
+  MOE_VARIANT_TILED = 2   /* LDS-tiled MFMA geometry for many rows per expert (prefill) */
+};
+
+/* Limits checked by the validators. */
+#define MOE_MAX_EXPERTS 1024       /* routed experts E */
+#define MOE_MAX_EXPERTS_TOTAL 2048 /* E + shared experts */
+#define MOE_MAX_K_TOTAL 32         /* k + n_shared */
+
+/* ---- a1: router projection (optional helper) ----------------------------
+ * logits[t,e] = sum_h x[t,h] * w_router[e,h], products accumulated in fp32 in
+ * a fixed order. The "Router" box of the paper's layer figure.
+ *   x         bf16 [T, H]        w_router  bf16 [E, H]
+ *   logits    fp32 [T, E] (written)
+ * Requires T >= 0, H > 0 and H % 8 == 0, 1 <= E <= MOE_MAX_EXPERTS. */
+moe_status moe_router_logits(const uint16_t* x, const uint16_t* w_router, int T, int H, int E,
+                             float* logits, void* stream);
+
+/* ---- a2: top-k routing ----------------------------------------------------
+ * For every token: the k largest logits, ordered by (logit descending, expert
+ * id ascending) -- ties go to the lower id and positions are in this fixed
+ * order (paper: Correctness recovery / Later numerical and integration
+ * repairs, deterministic index selection). Weights are the softmax over the k
+ * picks, w_j = exp(l_j - l_0) / sum_{i<k} exp(l_i - l_0), in fp32.
+ * With n_shared = 1 a last column holds expert id E with weight 1.0 (the
+ * shared expert, stacked after the routed ones).
+ *   logits    fp32 [T, E]; NaN is read as -inf
+ *   topk_ids  int32 [T, k + n_shared] (written)
+ *   topk_w    fp32  [T, k + n_shared] (written)
+ * Requires 1 <= k <= E <= MOE_MAX_EXPERTS, n_shared in {0, 1},
+ * k + n_shared <= MOE_MAX_K_TOTAL. */
+moe_status moe_route_topk(const float* logits, int T, int E, int k, int n_shared, int32_t* topk_ids,
+                          float* topk_w, void* stream);
+
+/* ---- a3: token -> expert permutation ---------------------------------------
+ * Stable counting sort of the A = T * k_total assignments a = t*k_total + j by
+ * expert id topk_ids[a] (the paper's expert sorter: Prefill optimization /
+ * From per-assignment scalar work to CDNA2 MFMA, item 8).
+ *   counts   int32 [NE]      assignments per expert
+ *   offsets  int32 [NE + 1]  exclusive prefix sum of counts; offsets[NE] = A
+ *   sorted   int32 [A]       assignment indices grouped by expert, increasing
+ *                            a inside each expert
+ *   pos      int32 [A]       inverse: sorted[pos[a]] == a
+ * Ids outside [0, NE) are a precondition violation: they are skipped (never
+ * used as an address), so counts then sum to less than A and the entries of
+ * sorted past offsets[NE] are left unwritten.
+ * ws: device workspace of at least moe_permute_workspace_bytes(...) bytes,
+ * 256-byte aligned; contents need not be initialised.
+ * Requires T >= 0, 1 <= NE <= MOE_MAX_EXPERTS_TOTAL, 1 <= k_total <= MOE_MAX_K_TOTAL. */
+size_t moe_permute_workspace_bytes(int T, int n_experts_total, int k_total);
+moe_status moe_permute(const int32_t* topk_ids, int T, int n_experts_total, int k_total,
+                       int32_t* counts, int32_t* offsets, int32_t* sorted, int32_t* pos, void* ws,
+                       size_t ws_bytes, void* stream);
+
+/* ---- a4: activation quantisation (standalone) -----------------------------
+ * Per block of 32 consecutive elements of each row: X = the smallest integer
+ * in [-127, 127] with max|v| <= maxval(format) * 2^X (X = 0 for an all-zero
+ * block); scale byte = X + 127; each code = round-to-nearest-even(v / 2^X) on
+ * the element grid, subnormals included, sign bit = sign bit of v. The paper
+ * quantises activations per 32 elements before each projection (Historical
+ * TP4 decode optimization / Parallel decomposition; Historical down-consumer
+ * pilot). moe_fp4_grouped_gemm runs the same quantiser internally.
+ *   x       bf16 [rows, K] (finite)
+ *   codes   [rows, K * bits / 8] bytes, packed as the format says (written)
+ *   scales  uint8 [rows, K / 32] (written)
+ * Requires rows >= 0, K > 0, K % 32 == 0. */
+moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f, uint8_t* codes,
+                            uint8_t* scales, void* stream);
+
+/* ---- a5 + a6: grouped FP4 expert GEMMs --------------------------------------
+ * For every expert e and every sorted row r in [offsets[e], offsets[e+1]),
+ * with a = sorted[r] and t = a / k_total:
+ *   xq      = MX-quantised x[t]                     (as moe_quantize_act)
+ *   G, U    = xq . W1[e]^T, xq . W3[e]^T            (W13 rows 0..I-1 = gate W1,
+ *                                                   rows I..2I-1 = up W3)
+ *   h       = G * U / (1 + exp(-G))                 (SwiGLU, fp32)
+ *   hq      = MX-quantised h (blocks of 32 along I)
+ *   partials[a, :] = hq . W2[e]^T                   (fp32, one unique row per
+ *                                                   assignment: no atomics)
+ * Products of codes and power-of-two scales are exact; sums are fp32 on the
+ * matrix cores in a fixed order (no split-K).
+ *   x         bf16 [T, H]
+ *   offsets   int32 [NE + 1], sorted int32 [T * k_total]   (from moe_permute)
+ *   w13       uint8 [NE, 2I, H/2]   w13_s uint8 [NE, 2I, H/32]
+ *   w2        uint8 [NE, H, I/2]    w2_s  uint8 [NE, H, I/32]
+ *   partials  fp32 [T * k_total, H]; row a = t*k_total + j (written for every
+ *             assignment with a valid expert id)
+ * ws: device workspace of at least moe_fp4_grouped_gemm_workspace_bytes(...)
+ * bytes, 256-byte aligned, contents need not be initialised. Its regions are
+ * reported by moe_fp4_grouped_gemm_workspace_layout (for inspection by tests).
+ * Requires T >= 0, H > 0, I > 0, H % 128 == 0, I % 128 == 0,
+ * 1 <= NE <= MOE_MAX_EXPERTS_TOTAL, 1 <= k_total <= MOE_MAX_K_TOTAL.
+ * The geometry (MOE_VARIANT_*) is chosen from T * k_total / NE and reported
+ * by moe_last_variant(). */
+size_t moe_fp4_grouped_gemm_workspace_bytes(int T, int H, int I, int n_experts_total, int k_total,
+                                            moe_act_format f);
+
+/* Byte offsets of the workspace regions: [0] x codes [T, H*bits/8], [1] x
+ * scales [T, H/32], [2] h codes [T*k_total, I*bits/8] in sorted-row order,
+ * [3] h scales [T*k_total, I/32], [4] tile list, [5] total bytes. */
+#define MOE_WS_REGIONS 6
+moe_status moe_fp4_grouped_gemm_workspace_layout(int T, int H, int I, int n_experts_total,
+                                                 int k_total, moe_act_format f,
+                                                 size_t offsets[MOE_WS_REGIONS]);
+
+moe_status moe_fp4_grouped_gemm(const uint16_t* x, int T, int H, int I, int n_experts_total,
+                                int k_total, const int32_t* offsets, const int32_t* sorted,
+                                const uint8_t* w13, const uint8_t* w13_s, const uint8_t* w2,
+                                const uint8_t* w2_s, moe_act_format f, float* partials, void* ws,
+                                size_t ws_bytes, void* stream);
+
+/* The grouped GEMM split into its three steps, for per-step timing and
+ * inspection: stages is a bit mask, bit 0 = activation quantisation of x and
+ * the row-tile list (into ws), bit 1 = gate/up + SwiGLU + h quantisation
+ * (reads x codes and tile list from ws, writes h codes to ws), bit 2 = down
+ * projection into partials (reads h codes and tile list from ws). Calling the
+ * bits in increasing order, in one call or several on one stream with the
+ * same arguments, is exactly moe_fp4_grouped_gemm (stages = 7). */
+moe_status moe_fp4_grouped_gemm_stages(const uint16_t* x, int T, int H, int I,
+                                       int n_experts_total, int k_total, const int32_t* offsets,
+                                       const int32_t* sorted, const uint8_t* w13,
+                                       const uint8_t* w13_s, const uint8_t* w2,
+                                       const uint8_t* w2_s, moe_act_format f, float* partials,
+                                       void* ws, size_t ws_bytes, int stages, void* stream);
+
+/* ---- a7: fixed-order combine ------------------------------------------------
+ * out[t, :] = bf16_rne(acc), acc = 0; for j = 0 .. k_total-1:
+ *   acc = fmaf(topk_w[t, j], partials[t*k_total + j, :], acc)      (fp32)
+ * The shared expert's weight is 1.0, so its fma is an exact add. The paper's
+ * accepted path keeps one FP32 partial per (token, slot) and reduces them in a
+ * fixed order (Current TP8 native-AR results / Accepted large-prefill
+ * configuration; Rejected or reverted directions: BF16 partials rejected).
+ *   partials fp32 [T * k_total, H]   topk_w fp32 [T, k_total]   out bf16 [T, H]
+ * Requires T >= 0, H > 0, H % 8 == 0, 1 <= k_total <= MOE_MAX_K_TOTAL. */
+moe_status moe_combine_fixed_order(const float* partials, const float* topk_w, int T, int H,
+                                   int k_total, uint16_t* out, void* stream);
+
+/* ---- diagnostics ------------------------------------------------------------ */
+
+/* Human-readable name of a status code (static storage). */
+const char* moe_status_string(moe_status s);
+
+/* MOE_VARIANT_* chosen by the calling thread's last moe_fp4_grouped_gemm. */
+int moe_last_variant(void);
+
+/* One block-scaled matrix-core product, D = (A * 2^(sa-127)) . (B * 2^(sb-127))^T
+ * per 32-element K block, using the same operand and scale placement as the
+ * grouped GEMM. Used to check that placement against the oracle.
+ *   a   [16, 128] activation codes in format fa (packed like moe_quantize_act)
+ *   sa  uint8 [16, 4]      b  uint8 [16, 64] FP4 weight codes   sb uint8 [16, 4]
+ *   d   fp32 [16, 16] (written), d[i][j] = sum_k A[i][k] * B[j][k] */
+moe_status moe_probe_scaled_mfma(const uint8_t* a, const uint8_t* sa, moe_act_format fa,
+                                 const uint8_t* b, const uint8_t* sb, float* d, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_H_ */

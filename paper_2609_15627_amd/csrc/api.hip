@@ -1,0 +1,181 @@
+// The C ABI (include/moe.h): host-side argument validation, then the
+// launchers. Validation runs before anything is enqueued, so every error path
+// can be exercised without a GPU. No exception crosses the boundary.
+#include "moe.h"
+
+#include <hip/hip_runtime.h>
+
+#include "moe_launch.h"
+
+namespace {
+
+thread_local int g_last_variant = MOE_VARIANT_NONE;
+
+inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+inline moe_status launched(hipError_t e) {
+  if (e == hipSuccess) return MOE_OK;
+  if (e == hipErrorNotSupported) return MOE_ERR_UNSUPPORTED;
+  return MOE_ERR_LAUNCH;
+}
+
+inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int fmt_code(moe_act_format f) {
+  switch (f) {
+    case MOE_ACT_MXFP8_E4M3: return 0;
+    case MOE_ACT_MXFP6_E2M3: return 2;
+    case MOE_ACT_MXFP4_E2M1: return 4;
+  }
+  return -1;
+}
+
+bool tokens_ok(int T, int k_total) { return T >= 0 && (long)T * k_total < (1L << 31); }
+
+}  // namespace
+
+extern "C" {
+
+const char* moe_status_string(moe_status s) {
+  switch (s) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_INVALID_ARG: return "invalid argument";
+    case MOE_ERR_UNSUPPORTED: return "unsupported";
+    case MOE_ERR_WORKSPACE: return "workspace too small or missing";
+    case MOE_ERR_LAUNCH: return "kernel launch failed";
+  }
+  return "unknown status";
+}
+
+int moe_last_variant(void) { return g_last_variant; }
+
+moe_status moe_router_logits(const uint16_t* x, const uint16_t* w_router, int T, int H, int E,
+                             float* logits, void* stream) {
+  if (T < 0 || H <= 0 || H % 8 || E < 1 || E > MOE_MAX_EXPERTS) return MOE_ERR_INVALID_ARG;
+  if ((long)T * E >= (1L << 31) / 64) return MOE_ERR_INVALID_ARG;
+  if (T > 0 && (!x || !w_router || !logits)) return MOE_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(w_router, 16)) return MOE_ERR_INVALID_ARG;
+  return launched(moe::launch_router_logits(x, w_router, T, H, E, logits, as_stream(stream)));
+}
+
+moe_status moe_route_topk(const float* logits, int T, int E, int k, int n_shared, int32_t* topk_ids,
+                          float* topk_w, void* stream) {
+  if (T < 0 || E < 1 || E > MOE_MAX_EXPERTS || k < 1 || k > E) return MOE_ERR_INVALID_ARG;
+  if (n_shared != 0 && n_shared != 1) return MOE_ERR_INVALID_ARG;
+  if (k + n_shared > MOE_MAX_K_TOTAL || !tokens_ok(T, k + n_shared)) return MOE_ERR_INVALID_ARG;
+  if (T > 0 && (!logits || !topk_ids || !topk_w)) return MOE_ERR_INVALID_ARG;
+  return launched(moe::launch_route_topk(logits, T, E, k, n_shared, topk_ids, topk_w,
+                                         as_stream(stream)));
+}
+
+size_t moe_permute_workspace_bytes(int T, int n_experts_total, int k_total) {
+  if (T < 0 || n_experts_total < 1 || k_total < 1) return 0;
+  return moe::permute_workspace_bytes(T, n_experts_total, k_total);
+}
+
+moe_status moe_permute(const int32_t* topk_ids, int T, int n_experts_total, int k_total,
+                       int32_t* counts, int32_t* offsets, int32_t* sorted, int32_t* pos, void* ws,
+                       size_t ws_bytes, void* stream) {
+  if (T < 0 || n_experts_total < 1 || n_experts_total > MOE_MAX_EXPERTS_TOTAL) return MOE_ERR_INVALID_ARG;
+  if (k_total < 1 || k_total > MOE_MAX_K_TOTAL || !tokens_ok(T, k_total)) return MOE_ERR_INVALID_ARG;
+  if (!counts || !offsets) return MOE_ERR_INVALID_ARG;
+  if (T > 0 && (!topk_ids || !sorted || !pos)) return MOE_ERR_INVALID_ARG;
+  const size_t need = moe::permute_workspace_bytes(T, n_experts_total, k_total);
+  if ((long)T * k_total > 1024 && (!ws || ws_bytes < need || !aligned(ws, 256)))
+    return MOE_ERR_WORKSPACE;
+  return launched(moe::launch_permute(topk_ids, T, n_experts_total, k_total, counts, offsets, sorted,
+                                      pos, ws, as_stream(stream)));
+}
+
+moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f, uint8_t* codes,
+                            uint8_t* scales, void* stream) {
+  const int fc = fmt_code(f);
+  if (fc < 0 || rows < 0 || K <= 0 || K % 32) return MOE_ERR_INVALID_ARG;
+  if (rows > 0 && (!x || !codes || !scales)) return MOE_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(codes, 16)) return MOE_ERR_INVALID_ARG;
+  return launched(moe::launch_quantize_act(x, rows, K, fc, codes, scales, as_stream(stream)));
+}
+
+static bool gemm_dims_ok(int T, int H, int I, int NE, int k_total) {
+  return T >= 0 && H > 0 && I > 0 && H % 128 == 0 && I % 128 == 0 && NE >= 1 &&
+         NE <= MOE_MAX_EXPERTS_TOTAL && k_total >= 1 && k_total <= MOE_MAX_K_TOTAL &&
+         tokens_ok(T, k_total);
+}
+
+size_t moe_fp4_grouped_gemm_workspace_bytes(int T, int H, int I, int n_experts_total, int k_total,
+                                            moe_act_format f) {
+  if (fmt_code(f) < 0 || !gemm_dims_ok(T, H, I, n_experts_total, k_total)) return 0;
+  return moe::gemm_workspace(T, H, I, n_experts_total, k_total, fmt_code(f)).off[5];
+}
+
+moe_status moe_fp4_grouped_gemm_workspace_layout(int T, int H, int I, int n_experts_total,
+                                                 int k_total, moe_act_format f,
+                                                 size_t offsets[MOE_WS_REGIONS]) {
+  if (!offsets || fmt_code(f) < 0 || !gemm_dims_ok(T, H, I, n_experts_total, k_total))
+    return MOE_ERR_INVALID_ARG;
+  const moe::GemmWorkspace w = moe::gemm_workspace(T, H, I, n_experts_total, k_total, fmt_code(f));
+  for (int i = 0; i < MOE_WS_REGIONS; ++i) offsets[i] = w.off[i];
+  return MOE_OK;
+}
+
+static moe_status grouped_gemm(const uint16_t* x, int T, int H, int I, int n_experts_total,
+                               int k_total, const int32_t* offsets, const int32_t* sorted,
+                               const uint8_t* w13, const uint8_t* w13_s, const uint8_t* w2,
+                               const uint8_t* w2_s, moe_act_format f, float* partials, void* ws,
+                               size_t ws_bytes, int stages, void* stream) {
+  const int fc = fmt_code(f);
+  if (fc < 0 || !gemm_dims_ok(T, H, I, n_experts_total, k_total)) return MOE_ERR_INVALID_ARG;
+  if (stages < 1 || stages > 7) return MOE_ERR_INVALID_ARG;
+  if (fc == 2) return MOE_ERR_UNSUPPORTED;
+  if (T > 0 && (!x || !offsets || !sorted || !w13 || !w13_s || !w2 || !w2_s || !partials))
+    return MOE_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(w13, 16) || !aligned(w2, 16) || !aligned(w13_s, 4) ||
+      !aligned(w2_s, 4) || !aligned(partials, 16))
+    return MOE_ERR_INVALID_ARG;
+  const size_t need = moe::gemm_workspace(T, H, I, n_experts_total, k_total, fc).off[5];
+  if (T > 0 && (!ws || ws_bytes < need || !aligned(ws, 256))) return MOE_ERR_WORKSPACE;
+  moe::GemmArgs a{x, T, H, I, n_experts_total, k_total, fc, offsets, sorted,
+                  w13, w13_s, w2, w2_s, partials, static_cast<uint8_t*>(ws)};
+  int variant = MOE_VARIANT_NONE;
+  const moe_status st = launched(moe::launch_grouped_gemm(a, stages, as_stream(stream), &variant));
+  g_last_variant = variant;
+  return st;
+}
+
+moe_status moe_fp4_grouped_gemm(const uint16_t* x, int T, int H, int I, int n_experts_total,
+                                int k_total, const int32_t* offsets, const int32_t* sorted,
+                                const uint8_t* w13, const uint8_t* w13_s, const uint8_t* w2,
+                                const uint8_t* w2_s, moe_act_format f, float* partials, void* ws,
+                                size_t ws_bytes, void* stream) {
+  return grouped_gemm(x, T, H, I, n_experts_total, k_total, offsets, sorted, w13, w13_s, w2, w2_s,
+                      f, partials, ws, ws_bytes, 7, stream);
+}
+
+moe_status moe_fp4_grouped_gemm_stages(const uint16_t* x, int T, int H, int I,
+                                       int n_experts_total, int k_total, const int32_t* offsets,
+                                       const int32_t* sorted, const uint8_t* w13,
+                                       const uint8_t* w13_s, const uint8_t* w2,
+                                       const uint8_t* w2_s, moe_act_format f, float* partials,
+                                       void* ws, size_t ws_bytes, int stages, void* stream) {
+  return grouped_gemm(x, T, H, I, n_experts_total, k_total, offsets, sorted, w13, w13_s, w2, w2_s,
+                      f, partials, ws, ws_bytes, stages, stream);
+}
+
+moe_status moe_combine_fixed_order(const float* partials, const float* topk_w, int T, int H,
+                                   int k_total, uint16_t* out, void* stream) {
+  if (T < 0 || H <= 0 || H % 8 || k_total < 1 || k_total > MOE_MAX_K_TOTAL || !tokens_ok(T, k_total))
+    return MOE_ERR_INVALID_ARG;
+  if (T > 0 && (!partials || !topk_w || !out)) return MOE_ERR_INVALID_ARG;
+  if (!aligned(partials, 16) || !aligned(out, 16)) return MOE_ERR_INVALID_ARG;
+  return launched(moe::launch_combine(partials, topk_w, T, H, k_total, out, as_stream(stream)));
+}
+
+moe_status moe_probe_scaled_mfma(const uint8_t* a, const uint8_t* sa, moe_act_format fa,
+                                 const uint8_t* b, const uint8_t* sb, float* d, void* stream) {
+  const int fc = fmt_code(fa);
+  if (fc < 0 || !a || !sa || !b || !sb || !d) return MOE_ERR_INVALID_ARG;
+  if (!aligned(a, 16) || !aligned(b, 16)) return MOE_ERR_INVALID_ARG;
+  return launched(moe::launch_probe(a, sa, fc, b, sb, d, as_stream(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,51 @@
+// Internal launchers behind the C ABI (host side). Arguments are already
+// validated by api.hip; every launcher only enqueues on the given stream.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace moe {
+
+hipError_t launch_router_logits(const uint16_t* x, const uint16_t* wr, int T, int H, int E,
+                                float* logits, hipStream_t s);
+hipError_t launch_route_topk(const float* logits, int T, int E, int k, int n_shared, int32_t* ids,
+                             float* w, hipStream_t s);
+
+size_t permute_workspace_bytes(int T, int NE, int k_total);
+hipError_t launch_permute(const int32_t* ids, int T, int NE, int k_total, int32_t* counts,
+                          int32_t* offsets, int32_t* sorted, int32_t* pos, void* ws,
+                          hipStream_t s);
+
+// fmt: 0 = e4m3, 2 = e2m3, 4 = e2m1 (matrix-core operand codes)
+int act_bits(int fmt);
+hipError_t launch_quantize_act(const uint16_t* x, long rows, int K, int fmt, uint8_t* codes,
+                               uint8_t* scales, hipStream_t s);
+
+struct GemmWorkspace {
+  size_t off[6];  // x codes, x scales, h codes, h scales, tile list, total
+};
+GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt);
+
+struct GemmArgs {
+  const uint16_t* x;
+  int T, H, I, NE, k_total, fmt;
+  const int32_t* offsets;
+  const int32_t* sorted;
+  const uint8_t *w13, *w13_s, *w2, *w2_s;
+  float* partials;
+  uint8_t* ws;
+};
+// stages: bit 0 = activation quantisation + tile list, bit 1 = gate/up
+// (stage 1), bit 2 = down (stage 2). Writes the geometry variant used
+// (MOE_VARIANT_*) to *variant.
+hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int* variant);
+
+hipError_t launch_combine(const float* partials, const float* w, int T, int H, int k_total,
+                          uint16_t* out, hipStream_t s);
+
+hipError_t launch_probe(const uint8_t* a, const uint8_t* sa, int fmt, const uint8_t* b,
+                        const uint8_t* sb, float* d, hipStream_t s);
+
+}  // namespace moe

@@ -1,0 +1,173 @@
+// a3: stable counting sort of assignments by expert id (the expert sorter).
+//
+// Three passes over chunks of kChunk assignments:
+//   1. perm_hist     per-chunk histograms, counted in LDS;
+//   2. perm_scan     counts, offsets (exclusive scan over experts) and, per
+//                    (chunk, expert), the first output slot of that chunk;
+//   3. perm_scatter  one wave per chunk walks its assignments in order, 64 at
+//                    a time. Lanes holding the same expert find each other
+//                    with ballots over the id bits; a lane's rank among its
+//                    lower-numbered peers plus the running per-expert cursor
+//                    in LDS is its slot, which keeps the sort stable.
+// Small inputs (one chunk) run all three steps in one workgroup.
+// Integer counting only, so the result is exact and run-to-run identical.
+#include "moe_dev.h"
+#include "moe_launch.h"
+
+namespace moe {
+
+constexpr int kChunk = 1024;
+
+__global__ __launch_bounds__(256) void perm_hist(const int32_t* __restrict__ ids, int A, int NE,
+                                                 int32_t* __restrict__ hist) {
+  extern __shared__ int32_t sh[];
+  for (int e = threadIdx.x; e < NE; e += blockDim.x) sh[e] = 0;
+  __syncthreads();
+  const int base = blockIdx.x * kChunk;
+  const int end = min(A, base + kChunk);
+  for (int a = base + threadIdx.x; a < end; a += blockDim.x) {
+    const int e = ids[a];
+    if ((unsigned)e < (unsigned)NE) atomicAdd(&sh[e], 1);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < NE; e += blockDim.x) hist[(size_t)blockIdx.x * NE + e] = sh[e];
+}
+
+// One block of 1024 threads; thread e owns experts e and e + 1024.
+__global__ __launch_bounds__(1024) void perm_scan(int32_t* __restrict__ hist, int nchunks, int NE,
+                                                  int32_t* __restrict__ counts,
+                                                  int32_t* __restrict__ offsets) {
+  int tot[2] = {0, 0};
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int e = threadIdx.x + 1024 * q;
+    if (e < NE) {
+      int run = 0;
+      for (int c = 0; c < nchunks; ++c) {
+        int32_t* p = hist + (size_t)c * NE + e;
+        const int n = *p;
+        *p = run;  // chunk-local base (relative to the expert's offset)
+        run += n;
+      }
+      tot[q] = run;
+    }
+  }
+  int total0, total1;
+  const int pre0 = block_exclusive_scan_1024(tot[0], &total0);
+  const int pre1 = block_exclusive_scan_1024(tot[1], &total1);
+  int off[2] = {pre0, total0 + pre1};
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int e = threadIdx.x + 1024 * q;
+    if (e < NE) {
+      counts[e] = tot[q];
+      offsets[e] = off[q];
+      for (int c = 0; c < nchunks; ++c) hist[(size_t)c * NE + e] += off[q];
+    }
+  }
+  if (threadIdx.x == 0) offsets[NE] = total0 + total1;
+}
+
+// Stable in-order placement of up to kChunk assignments by one wave, given the
+// first output slot of every expert for this chunk in cursor[] (LDS).
+__device__ __forceinline__ void scatter_chunk(const int32_t* __restrict__ ids, int base, int end,
+                                              int NE, int nbits, int32_t* cursor,
+                                              int32_t* __restrict__ sorted,
+                                              int32_t* __restrict__ pos) {
+  const int lane = threadIdx.x % kWave;
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+  for (int g = base; g < end; g += kWave) {
+    const int a = g + lane;
+    int e = a < end ? ids[a] : -1;
+    const bool ok = (unsigned)e < (unsigned)NE;
+    uint64_t peers = __ballot(ok);
+    for (int b = 0; b < nbits; ++b) {
+      const bool bit = ok && ((e >> b) & 1);
+      const uint64_t m = __ballot(bit);
+      peers &= bit ? m : ~m;
+    }
+    if (ok) {
+      const int rank = __popcll(peers & lt);
+      const int dest = cursor[e] + rank;
+      sorted[dest] = a;
+      pos[a] = dest;
+      // the highest peer advances the cursor past the whole group
+      if ((peers >> lane) == 1ull) cursor[e] = dest + 1;
+    }
+  }
+}
+
+__global__ __launch_bounds__(64) void perm_scatter(const int32_t* __restrict__ ids, int A, int NE,
+                                                   int nbits, const int32_t* __restrict__ hist,
+                                                   int32_t* __restrict__ sorted,
+                                                   int32_t* __restrict__ pos) {
+  extern __shared__ int32_t cursor[];
+  for (int e = threadIdx.x; e < NE; e += blockDim.x)
+    cursor[e] = hist[(size_t)blockIdx.x * NE + e];
+  __syncthreads();
+  const int base = blockIdx.x * kChunk;
+  scatter_chunk(ids, base, min(A, base + kChunk), NE, nbits, cursor, sorted, pos);
+}
+
+// All three steps in one workgroup of 1024 threads (A <= kChunk).
+__global__ __launch_bounds__(1024) void perm_small(const int32_t* __restrict__ ids, int A, int NE,
+                                                   int nbits, int32_t* __restrict__ counts,
+                                                   int32_t* __restrict__ offsets,
+                                                   int32_t* __restrict__ sorted,
+                                                   int32_t* __restrict__ pos) {
+  extern __shared__ int32_t cursor[];
+  for (int e = threadIdx.x; e < NE; e += blockDim.x) cursor[e] = 0;
+  __syncthreads();
+  for (int a = threadIdx.x; a < A; a += blockDim.x) {
+    const int e = ids[a];
+    if ((unsigned)e < (unsigned)NE) atomicAdd(&cursor[e], 1);
+  }
+  __syncthreads();
+  int c0 = threadIdx.x < NE ? cursor[threadIdx.x] : 0;
+  int c1 = threadIdx.x + 1024 < NE ? cursor[threadIdx.x + 1024] : 0;
+  int total0, total1;
+  const int p0 = block_exclusive_scan_1024(c0, &total0);
+  const int p1 = block_exclusive_scan_1024(c1, &total1) + total0;
+  if (threadIdx.x < NE) {
+    counts[threadIdx.x] = c0;
+    offsets[threadIdx.x] = p0;
+    cursor[threadIdx.x] = p0;
+  }
+  if (threadIdx.x + 1024 < NE) {
+    counts[threadIdx.x + 1024] = c1;
+    offsets[threadIdx.x + 1024] = p1;
+    cursor[threadIdx.x + 1024] = p1;
+  }
+  if (threadIdx.x == 0) offsets[NE] = total0 + total1;
+  __syncthreads();
+  if (threadIdx.x < kWave) scatter_chunk(ids, 0, A, NE, nbits, cursor, sorted, pos);
+}
+
+size_t permute_workspace_bytes(int T, int NE, int k_total) {
+  const long A = (long)T * k_total;
+  const long nchunks = (A + kChunk - 1) / kChunk;
+  return (size_t)((nchunks * NE * sizeof(int32_t) + 255) / 256 * 256);
+}
+
+hipError_t launch_permute(const int32_t* ids, int T, int NE, int k_total, int32_t* counts,
+                          int32_t* offsets, int32_t* sorted, int32_t* pos, void* ws,
+                          hipStream_t s) {
+  const int A = T * k_total;
+  int nbits = 0;
+  while ((1 << nbits) < NE) ++nbits;
+  const size_t lds = (size_t)NE * sizeof(int32_t);
+  if (A <= kChunk) {
+    hipLaunchKernelGGL(perm_small, dim3(1), dim3(1024), lds, s, ids, A, NE, nbits, counts, offsets,
+                       sorted, pos);
+    return hipGetLastError();
+  }
+  const int nchunks = (A + kChunk - 1) / kChunk;
+  int32_t* hist = static_cast<int32_t*>(ws);
+  hipLaunchKernelGGL(perm_hist, dim3(nchunks), dim3(256), lds, s, ids, A, NE, hist);
+  hipLaunchKernelGGL(perm_scan, dim3(1), dim3(1024), 0, s, hist, nchunks, NE, counts, offsets);
+  hipLaunchKernelGGL(perm_scatter, dim3(nchunks), dim3(64), lds, s, ids, A, NE, nbits, hist,
+                     sorted, pos);
+  return hipGetLastError();
+}
+
+}  // namespace moe

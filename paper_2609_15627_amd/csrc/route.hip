@@ -1,0 +1,141 @@
+// a1 router projection and a2 top-k routing.
+//
+// Top-k: one wave per token. Lane l holds logits of experts l, l+64, ...; k
+// rounds of a wave-wide arg-max over (logit descending, id ascending) pick the
+// experts in their fixed order (ties to the lower id: paper, Correctness
+// recovery / Later numerical and integration repairs). Lanes 0..k-1 keep pick
+// j = lane; the renormalised softmax weights are formed from them with the
+// denominator summed in pick order.
+#include "moe_dev.h"
+#include "moe_launch.h"
+
+namespace moe {
+
+// logits[t, e] = sum_h x[t, h] * wr[e, h]; one wave per (t, e). Each lane
+// accumulates 8 consecutive h per step (fmaf, fixed order), then a fixed
+// butterfly sums the 64 lane partials.
+__global__ __launch_bounds__(256) void router_logits_kernel(const uint16_t* __restrict__ x,
+                                                            const uint16_t* __restrict__ wr, int T,
+                                                            int H, int E,
+                                                            float* __restrict__ logits) {
+  const long wave = ((long)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (wave >= (long)T * E) return;
+  const int t = (int)(wave / E), e = (int)(wave % E);
+  const uint16_t* xr = x + (size_t)t * H;
+  const uint16_t* wrow = wr + (size_t)e * H;
+  float acc = 0.0f;
+  for (int h = lane * 8; h < H; h += kWave * 8) {
+    const uint4 xv = *reinterpret_cast<const uint4*>(xr + h);
+    const uint4 wv = *reinterpret_cast<const uint4*>(wrow + h);
+    const uint32_t xs[4] = {xv.x, xv.y, xv.z, xv.w};
+    const uint32_t ws[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc = fmaf(bf16_to_f32(xs[i] & 0xffffu), bf16_to_f32(ws[i] & 0xffffu), acc);
+      acc = fmaf(bf16_to_f32(xs[i] >> 16), bf16_to_f32(ws[i] >> 16), acc);
+    }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) acc += shfl_xor_f(acc, m);
+  if (lane == 0) logits[(size_t)t * E + e] = acc;
+}
+
+// EPL = experts held per lane (ceil(E / 64) rounded up to a power of two).
+template <int EPL>
+__global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict__ logits, int T,
+                                                         int E, int k, int n_shared,
+                                                         int32_t* __restrict__ ids,
+                                                         float* __restrict__ wts) {
+  const int t = (int)(((long)blockIdx.x * blockDim.x + threadIdx.x) / kWave);
+  const int lane = threadIdx.x % kWave;
+  if (t >= T) return;
+  const float* row = logits + (size_t)t * E;
+  float v[EPL];
+  bool live[EPL];
+#pragma unroll
+  for (int j = 0; j < EPL; ++j) {
+    const int e = lane + kWave * j;
+    live[j] = e < E;
+    float x = live[j] ? row[e] : -INFINITY;
+    v[j] = (x != x) ? -INFINITY : x;  // NaN reads as -inf
+  }
+  float my_val = 0.0f;
+  int my_id = 0;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const int e = lane + kWave * j;
+      if (live[j] && (v[j] > bv || (v[j] == bv && e < bi))) {
+        bv = v[j];
+        bi = e;
+      }
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const float ov = shfl_xor_f(bv, m);
+      const int oi = shfl_xor_i(bi, m);
+      if (ov > bv || (ov == bv && oi < bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    // every lane now holds the same (bv, bi); retire the pick
+#pragma unroll
+    for (int j = 0; j < EPL; ++j)
+      if (lane + kWave * j == bi) live[j] = false;
+    if (lane == r) {
+      my_val = bv;
+      my_id = bi;
+    }
+  }
+  const float l0 = __shfl(my_val, 0, kWave);
+  const float ex = lane < k ? expf(my_val - l0) : 0.0f;
+  float den = 0.0f;
+  for (int j = 0; j < k; ++j) den += __shfl(ex, j, kWave);
+  const int kt = k + n_shared;
+  int32_t* id_row = ids + (size_t)t * kt;
+  float* w_row = wts + (size_t)t * kt;
+  if (lane < k) {
+    id_row[lane] = my_id;
+    w_row[lane] = ex / den;
+  } else if (lane == k && n_shared) {
+    id_row[lane] = E;
+    w_row[lane] = 1.0f;
+  }
+}
+
+hipError_t launch_router_logits(const uint16_t* x, const uint16_t* wr, int T, int H, int E,
+                                float* logits, hipStream_t s) {
+  const long waves = (long)T * E;
+  if (waves == 0) return hipSuccess;
+  const int blocks = (int)((waves * kWave + 255) / 256);
+  hipLaunchKernelGGL(router_logits_kernel, dim3(blocks), dim3(256), 0, s, x, wr, T, H, E, logits);
+  return hipGetLastError();
+}
+
+hipError_t launch_route_topk(const float* logits, int T, int E, int k, int n_shared, int32_t* ids,
+                             float* w, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const int blocks = (T + 3) / 4;  // 4 waves (tokens) per 256-thread block
+  const int epl = (E + kWave - 1) / kWave;
+#define MOE_ROUTE(N)                                                                      \
+  hipLaunchKernelGGL(route_topk_kernel<N>, dim3(blocks), dim3(256), 0, s, logits, T, E, k, \
+                     n_shared, ids, w)
+  if (epl <= 1)
+    MOE_ROUTE(1);
+  else if (epl <= 2)
+    MOE_ROUTE(2);
+  else if (epl <= 4)
+    MOE_ROUTE(4);
+  else if (epl <= 8)
+    MOE_ROUTE(8);
+  else
+    MOE_ROUTE(16);
+#undef MOE_ROUTE
+  return hipGetLastError();
+}
+
+}  // namespace moe

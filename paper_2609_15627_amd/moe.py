@@ -1,0 +1,287 @@
+"""Python binding of libmoe.so (include/moe.h): argument marshalling only.
+
+Every function takes and returns torch tensors on the GPU; torch provides the
+device memory and the stream, every step of the layer runs in the library's
+HIP kernels. The library must be built (``__graft_entry__.build()`` or
+``python -m paper_2609_15627_amd._build``); importing this module without it
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmoe.so")
+
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_LAUNCH = range(5)
+ACT_FORMATS = {"e4m3": 0, "e2m3": 1, "e2m1": 2}
+ACT_BITS = {"e4m3": 8, "e2m3": 6, "e2m1": 4}
+VARIANT_NONE, VARIANT_STREAM, VARIANT_TILED = 0, 1, 2
+WS_REGIONS = 6
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_SZ = ctypes.c_size_t
+
+_SIGNATURES = {
+    "moe_router_logits": (_I, [_P, _P, _I, _I, _I, _P, _P]),
+    "moe_route_topk": (_I, [_P, _I, _I, _I, _I, _P, _P, _P]),
+    "moe_permute_workspace_bytes": (_SZ, [_I, _I, _I]),
+    "moe_permute": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _P, _SZ, _P]),
+    "moe_quantize_act": (_I, [_P, _I, _I, _I, _P, _P, _P]),
+    "moe_fp4_grouped_gemm_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I]),
+    "moe_fp4_grouped_gemm_workspace_layout": (_I, [_I, _I, _I, _I, _I, _I, ctypes.POINTER(_SZ)]),
+    "moe_fp4_grouped_gemm": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P,
+                                  _SZ, _P]),
+    "moe_fp4_grouped_gemm_stages": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P,
+                                         _P, _SZ, _I, _P]),
+    "moe_combine_fixed_order": (_I, [_P, _P, _I, _I, _I, _P, _P]),
+    "moe_status_string": (ctypes.c_char_p, [_I]),
+    "moe_last_variant": (_I, []),
+    "moe_probe_scaled_mfma": (_I, [_P, _P, _I, _P, _P, _P, _P]),
+}
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build the HIP library first "
+                          "(python -m paper_2609_15627_amd._build)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype, fn.argtypes = res, args
+    return lib
+
+
+lib = _load()
+LIB_PATH = _LIB_PATH
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status, what):
+        super().__init__(f"{what}: {lib.moe_status_string(status).decode()} (status {status})")
+        self.status = status
+
+
+def _check(status, what):
+    if status != MOE_OK:
+        raise MoeError(status, what)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(t, dtype, shape, name):
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or not t.is_cuda:
+        raise ValueError(f"{name}: expected contiguous {dtype} {tuple(shape)} on the GPU, got "
+                         f"{t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+def _u16(t):
+    """bf16 tensors are passed as their bit patterns."""
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t
+
+
+def moe_router_logits(x, w_router, logits=None, stream=None):
+    """logits [T, E] fp32 = x [T, H] bf16 . w_router [E, H] bf16 ^T."""
+    T, H = x.shape
+    E = w_router.shape[0]
+    _need(x, torch.bfloat16, (T, H), "x")
+    _need(w_router, torch.bfloat16, (E, H), "w_router")
+    if logits is None:
+        logits = torch.empty((T, E), dtype=torch.float32, device=x.device)
+    _need(logits, torch.float32, (T, E), "logits")
+    _check(lib.moe_router_logits(_ptr(x), _ptr(w_router), T, H, E, _ptr(logits), _stream(stream)),
+           "moe_router_logits")
+    return logits
+
+
+def moe_route_topk(logits, k, n_shared=0, topk_ids=None, topk_w=None, stream=None):
+    T, E = logits.shape
+    kt = k + n_shared
+    _need(logits, torch.float32, (T, E), "logits")
+    if topk_ids is None:
+        topk_ids = torch.empty((T, kt), dtype=torch.int32, device=logits.device)
+    if topk_w is None:
+        topk_w = torch.empty((T, kt), dtype=torch.float32, device=logits.device)
+    _need(topk_ids, torch.int32, (T, kt), "topk_ids")
+    _need(topk_w, torch.float32, (T, kt), "topk_w")
+    _check(lib.moe_route_topk(_ptr(logits), T, E, k, n_shared, _ptr(topk_ids), _ptr(topk_w),
+                              _stream(stream)), "moe_route_topk")
+    return topk_ids, topk_w
+
+
+def moe_permute_workspace_bytes(T, n_experts_total, k_total):
+    return lib.moe_permute_workspace_bytes(T, n_experts_total, k_total)
+
+
+def moe_permute(topk_ids, n_experts_total, out=None, ws=None, stream=None):
+    """Returns (counts, offsets, sorted, pos) int32 tensors."""
+    T, kt = topk_ids.shape
+    _need(topk_ids, torch.int32, (T, kt), "topk_ids")
+    dev = topk_ids.device
+    if out is None:
+        out = (torch.empty(n_experts_total, dtype=torch.int32, device=dev),
+               torch.empty(n_experts_total + 1, dtype=torch.int32, device=dev),
+               torch.empty(T * kt, dtype=torch.int32, device=dev),
+               torch.empty(T * kt, dtype=torch.int32, device=dev))
+    counts, offsets, srt, pos = out
+    nb = moe_permute_workspace_bytes(T, n_experts_total, kt)
+    if ws is None:
+        ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=dev)
+    _check(lib.moe_permute(_ptr(topk_ids), T, n_experts_total, kt, _ptr(counts), _ptr(offsets),
+                           _ptr(srt), _ptr(pos), _ptr(ws), ws.numel(), _stream(stream)),
+           "moe_permute")
+    return counts, offsets, srt, pos
+
+
+def act_code_bytes(K, fmt):
+    return K * ACT_BITS[fmt] // 8
+
+
+def moe_quantize_act(x, fmt="e4m3", codes=None, scales=None, stream=None):
+    rows, K = x.shape
+    _need(x, torch.bfloat16, (rows, K), "x")
+    if codes is None:
+        codes = torch.empty((rows, act_code_bytes(K, fmt)), dtype=torch.uint8, device=x.device)
+    if scales is None:
+        scales = torch.empty((rows, K // 32), dtype=torch.uint8, device=x.device)
+    _check(lib.moe_quantize_act(_ptr(x), rows, K, ACT_FORMATS[fmt], _ptr(codes), _ptr(scales),
+                                _stream(stream)), "moe_quantize_act")
+    return codes, scales
+
+
+def moe_fp4_grouped_gemm_workspace_bytes(T, H, I, n_experts_total, k_total, fmt="e4m3"):
+    return lib.moe_fp4_grouped_gemm_workspace_bytes(T, H, I, n_experts_total, k_total,
+                                                    ACT_FORMATS[fmt])
+
+
+def moe_fp4_grouped_gemm_workspace_layout(T, H, I, n_experts_total, k_total, fmt="e4m3"):
+    arr = (_SZ * WS_REGIONS)()
+    _check(lib.moe_fp4_grouped_gemm_workspace_layout(T, H, I, n_experts_total, k_total,
+                                                     ACT_FORMATS[fmt], arr),
+           "moe_fp4_grouped_gemm_workspace_layout")
+    return list(arr)
+
+
+def moe_fp4_grouped_gemm(x, offsets, sorted_, w13, w13_s, w2, w2_s, k_total, fmt="e4m3",
+                         partials=None, ws=None, stream=None, stages=7):
+    """stages: 7 runs the whole call; other masks call moe_fp4_grouped_gemm_stages."""
+    T, H = x.shape
+    NE, two_i, _ = w13.shape
+    I = two_i // 2
+    _need(x, torch.bfloat16, (T, H), "x")
+    _need(offsets, torch.int32, (NE + 1,), "offsets")
+    _need(sorted_, torch.int32, (T * k_total,), "sorted")
+    _need(w13, torch.uint8, (NE, 2 * I, H // 2), "w13")
+    _need(w13_s, torch.uint8, (NE, 2 * I, H // 32), "w13_s")
+    _need(w2, torch.uint8, (NE, H, I // 2), "w2")
+    _need(w2_s, torch.uint8, (NE, H, I // 32), "w2_s")
+    if partials is None:
+        partials = torch.empty((T * k_total, H), dtype=torch.float32, device=x.device)
+    _need(partials, torch.float32, (T * k_total, H), "partials")
+    if ws is None:
+        ws = torch.empty(max(moe_fp4_grouped_gemm_workspace_bytes(T, H, I, NE, k_total, fmt), 256),
+                         dtype=torch.uint8, device=x.device)
+    args = (_ptr(x), T, H, I, NE, k_total, _ptr(offsets), _ptr(sorted_), _ptr(w13), _ptr(w13_s),
+            _ptr(w2), _ptr(w2_s), ACT_FORMATS[fmt], _ptr(partials), _ptr(ws), ws.numel())
+    if stages == 7:
+        _check(lib.moe_fp4_grouped_gemm(*args, _stream(stream)), "moe_fp4_grouped_gemm")
+    else:
+        _check(lib.moe_fp4_grouped_gemm_stages(*args, stages, _stream(stream)),
+               "moe_fp4_grouped_gemm_stages")
+    return partials
+
+
+def moe_combine_fixed_order(partials, topk_w, out=None, stream=None):
+    T, kt = topk_w.shape
+    H = partials.shape[1]
+    _need(partials, torch.float32, (T * kt, H), "partials")
+    _need(topk_w, torch.float32, (T, kt), "topk_w")
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.bfloat16, device=partials.device)
+    _need(out, torch.bfloat16, (T, H), "out")
+    _check(lib.moe_combine_fixed_order(_ptr(partials), _ptr(topk_w), T, H, kt, _ptr(out),
+                                       _stream(stream)), "moe_combine_fixed_order")
+    return out
+
+
+def moe_last_variant():
+    return lib.moe_last_variant()
+
+
+def moe_probe_scaled_mfma(a, sa, b, sb, fmt="e4m3", d=None, stream=None):
+    if d is None:
+        d = torch.empty((16, 16), dtype=torch.float32, device=a.device)
+    _check(lib.moe_probe_scaled_mfma(_ptr(a), _ptr(sa), ACT_FORMATS[fmt], _ptr(b), _ptr(sb),
+                                     _ptr(d), _stream(stream)), "moe_probe_scaled_mfma")
+    return d
+
+
+class MoELayer:
+    """One routed-MoE layer forward through the four library calls.
+
+    Owns the intermediate buffers and workspaces (torch allocations made once
+    at construction); ``forward`` enqueues only library kernels.
+    """
+
+    def __init__(self, T, H, E, k, I, n_shared=0, fmt="e4m3", device="cuda"):
+        self.T, self.H, self.E, self.k, self.I, self.S = T, H, E, k, I, n_shared
+        self.NE, self.kt = E + n_shared, k + n_shared
+        self.fmt = fmt
+        dev = torch.device(device)
+        A = T * self.kt
+        self.logits = torch.empty((T, E), dtype=torch.float32, device=dev)
+        self.ids = torch.empty((T, self.kt), dtype=torch.int32, device=dev)
+        self.w = torch.empty((T, self.kt), dtype=torch.float32, device=dev)
+        self.perm = (torch.empty(self.NE, dtype=torch.int32, device=dev),
+                     torch.empty(self.NE + 1, dtype=torch.int32, device=dev),
+                     torch.empty(A, dtype=torch.int32, device=dev),
+                     torch.empty(A, dtype=torch.int32, device=dev))
+        self.perm_ws = torch.empty(max(moe_permute_workspace_bytes(T, self.NE, self.kt), 256),
+                                   dtype=torch.uint8, device=dev)
+        self.partials = torch.empty((A, H), dtype=torch.float32, device=dev)
+        self.gemm_ws = torch.empty(
+            max(moe_fp4_grouped_gemm_workspace_bytes(T, H, I, self.NE, self.kt, fmt), 256),
+            dtype=torch.uint8, device=dev)
+        self.out = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+
+    def workspace_view(self, region):
+        """uint8 view of a grouped-GEMM workspace region (0..3, see include/moe.h)."""
+        off = moe_fp4_grouped_gemm_workspace_layout(self.T, self.H, self.I, self.NE, self.kt,
+                                                    self.fmt)
+        return self.gemm_ws[off[region]:off[region + 1]]
+
+    def forward(self, x, weights, logits=None, w_router=None, stream=None, events=None):
+        """Enqueue the layer. ``events``: optional list of 7 torch.cuda.Event
+        recorded between the steps (route, permute, quantise, gate/up, down,
+        combine) for per-step timing."""
+        w13, w13_s, w2, w2_s = weights
+        ev = (lambda i: events[i].record(stream)) if events else (lambda i: None)
+        ev(0)
+        if logits is None:
+            logits = moe_router_logits(x, w_router, self.logits, stream=stream)
+        moe_route_topk(logits, self.k, self.S, self.ids, self.w, stream=stream)
+        ev(1)
+        counts, offsets, srt, pos = moe_permute(self.ids, self.NE, out=self.perm, ws=self.perm_ws,
+                                                stream=stream)
+        ev(2)
+        g = (x, offsets, srt, w13, w13_s, w2, w2_s, self.kt, self.fmt)
+        if events:
+            for i, st in enumerate((1, 2, 4)):
+                moe_fp4_grouped_gemm(*g, partials=self.partials, ws=self.gemm_ws, stream=stream,
+                                     stages=st)
+                ev(3 + i)
+        else:
+            moe_fp4_grouped_gemm(*g, partials=self.partials, ws=self.gemm_ws, stream=stream)
+        out = moe_combine_fixed_order(self.partials, self.w, out=self.out, stream=stream)
+        ev(6)
+        return out

@@ -1,0 +1,81 @@
+"""Shared helpers of the GPU parity tests: upload seeded inputs, run the
+library's layer forward, compare with the oracle."""
+from __future__ import annotations
+
+import functools
+import sys
+
+import numpy as np
+import torch
+
+import synth
+
+
+def log(msg):
+    """Name the case on stdout before each GPU step (flushed)."""
+    print(f"[gpu] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def to_dev_u8(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def to_dev_bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def bf16_bits(t):
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def bf16_to_f64(bits):
+    return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+@functools.lru_cache(maxsize=2)
+def _stacked_weights(H, I, NE, seed):
+    cfg = synth.LayerConfig("w", 1, H, NE, 1, I, 0, "normal", seed)
+    return synth.gen_all_experts(cfg)
+
+
+@functools.lru_cache(maxsize=1)
+def _dev_weights(H, I, NE, seed):
+    return tuple(to_dev_u8(a) for a in _stacked_weights(H, I, NE, seed))
+
+
+def drop_caches():
+    _dev_weights.cache_clear()
+    _stacked_weights.cache_clear()
+    torch.cuda.empty_cache()
+
+
+def dev_weights(cfg, share=True):
+    """Device weights of a config. Routed experts depend only on (H, I, e, seed),
+    so configs with equal dims share one upload (the shared expert is index E)."""
+    if not share:
+        return tuple(to_dev_u8(a) for a in synth.gen_all_experts(cfg))
+    ne_max = 257 if (cfg.H, cfg.I) == (4096, 2048) else cfg.NE
+    full = _dev_weights(cfg.H, cfg.I, ne_max, cfg.seed)
+    if cfg.NE == ne_max:
+        return full
+    return tuple(a[:cfg.NE] for a in full)
+
+
+def rowrel(y, ref):
+    """max over rows of max|y - ref| / max|ref| (row-wise infinity-norm relative error)."""
+    y = np.asarray(y, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = np.abs(ref).max(axis=1)
+    den = np.where(den == 0, 1.0, den)
+    return float((np.abs(y - ref).max(axis=1) / den).max())
+
+
+def metrics(y, ref):
+    """The paper's kernel-level metrics: max abs error, relative L2, cosine."""
+    y = np.asarray(y, np.float64).ravel()
+    ref = np.asarray(ref, np.float64).ravel()
+    d = y - ref
+    return dict(max_abs=float(np.abs(d).max()), rel_l2=float(np.linalg.norm(d) / np.linalg.norm(ref)),
+                cosine=float(y @ ref / (np.linalg.norm(y) * np.linalg.norm(ref))),
+                rowrel=rowrel(y.reshape(1, -1), ref.reshape(1, -1)))

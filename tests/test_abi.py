@@ -1,0 +1,121 @@
+"""Host-only checks of the C ABI: the library loads, exports every entry point
+declared in include/moe.h, and rejects bad arguments before touching the GPU
+(every call below returns from host-side validation; no HIP call is made)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from tests.conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "moe.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def m():
+    from paper_2609_15627_amd import moe
+    return moe
+
+
+def test_header_declares_the_four_layer_calls():
+    names = declared_functions()
+    for n in ("moe_route_topk", "moe_permute", "moe_fp4_grouped_gemm", "moe_combine_fixed_order"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(m):
+    lib = ctypes.CDLL(m.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_covers_every_declared_symbol(m):
+    assert set(declared_functions()) <= set(m._SIGNATURES)
+
+
+def test_status_strings(m):
+    for s in range(5):
+        assert m.lib.moe_status_string(s)
+    assert m.lib.moe_last_variant() == m.VARIANT_NONE
+
+
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
+NUL = ctypes.c_void_p(0)
+
+
+@pytest.mark.parametrize("args", [
+    (FAKE, -1, 8, 2, 0, FAKE, FAKE, NUL),          # T < 0
+    (FAKE, 4, 0, 1, 0, FAKE, FAKE, NUL),           # E < 1
+    (FAKE, 4, 8, 9, 0, FAKE, FAKE, NUL),           # k > E
+    (FAKE, 4, 8, 0, 0, FAKE, FAKE, NUL),           # k < 1
+    (FAKE, 4, 8, 2, 2, FAKE, FAKE, NUL),           # n_shared not 0/1
+    (FAKE, 4, 2048, 2, 0, FAKE, FAKE, NUL),        # E > MOE_MAX_EXPERTS
+    (FAKE, 4, 64, 33, 0, FAKE, FAKE, NUL),         # k_total > 32
+    (NUL, 4, 8, 2, 0, FAKE, FAKE, NUL),            # null logits
+    (FAKE, 4, 8, 2, 0, NUL, FAKE, NUL),            # null ids
+])
+def test_route_rejects(m, args):
+    assert m.lib.moe_route_topk(*args) == m.MOE_ERR_INVALID_ARG
+
+
+def test_permute_rejects(m):
+    L = m.lib
+    assert L.moe_permute(FAKE, -1, 8, 2, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, NUL) == 1
+    assert L.moe_permute(FAKE, 4, 0, 2, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, NUL) == 1
+    assert L.moe_permute(FAKE, 4, 4096, 2, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, NUL) == 1
+    assert L.moe_permute(FAKE, 4, 8, 0, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, NUL) == 1
+    assert L.moe_permute(FAKE, 4, 8, 2, NUL, FAKE, FAKE, FAKE, FAKE, 1 << 20, NUL) == 1
+    # large inputs need a workspace
+    assert L.moe_permute(FAKE, 4096, 8, 2, FAKE, FAKE, FAKE, FAKE, NUL, 0, NUL) == m.MOE_ERR_WORKSPACE
+    need = m.moe_permute_workspace_bytes(4096, 8, 2)
+    assert L.moe_permute(FAKE, 4096, 8, 2, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, NUL) == 3
+
+
+def test_gemm_rejects(m):
+    L = m.lib
+    base = dict(T=8, H=256, I=128, NE=4, kt=2, f=0)
+
+    def call(ws_bytes=1 << 30, ws=FAKE, **kw):
+        a = dict(base, **kw)
+        return L.moe_fp4_grouped_gemm(FAKE, a["T"], a["H"], a["I"], a["NE"], a["kt"], FAKE, FAKE,
+                                      FAKE, FAKE, FAKE, FAKE, a["f"], FAKE, ws, ws_bytes, NUL)
+    assert call(H=200) == 1            # H % 128
+    assert call(I=96) == 1             # I % 128
+    assert call(T=-1) == 1
+    assert call(NE=0) == 1
+    assert call(kt=40) == 1
+    assert call(f=7) == 1
+    assert call(f=1) == m.MOE_ERR_UNSUPPORTED   # MXFP6 activations not built
+    assert call(ws=NUL) == m.MOE_ERR_WORKSPACE
+    need = m.moe_fp4_grouped_gemm_workspace_bytes(8, 256, 128, 4, 2, "e4m3")
+    assert need > 0 and call(ws_bytes=need - 1) == m.MOE_ERR_WORKSPACE
+    assert m.moe_fp4_grouped_gemm_workspace_bytes(8, 200, 128, 4, 2) == 0
+
+
+def test_workspace_layout_is_ordered_and_sized(m):
+    for fmt in ("e4m3", "e2m1"):
+        off = m.moe_fp4_grouped_gemm_workspace_layout(64, 4096, 2048, 257, 9, fmt)
+        assert off == sorted(off) and all(o % 256 == 0 for o in off)
+        bits = m.ACT_BITS[fmt]
+        assert off[1] - off[0] >= 64 * 4096 * bits // 8
+        assert off[3] - off[2] >= 64 * 9 * 2048 * bits // 8
+        assert off[5] == m.moe_fp4_grouped_gemm_workspace_bytes(64, 4096, 2048, 257, 9, fmt)
+
+
+def test_combine_quant_logits_reject(m):
+    L = m.lib
+    assert L.moe_combine_fixed_order(FAKE, FAKE, 4, 100, 2, FAKE, NUL) == 1   # H % 8
+    assert L.moe_combine_fixed_order(FAKE, FAKE, 4, 128, 0, FAKE, NUL) == 1
+    assert L.moe_combine_fixed_order(NUL, FAKE, 4, 128, 2, FAKE, NUL) == 1
+    assert L.moe_quantize_act(FAKE, 4, 100, 0, FAKE, FAKE, NUL) == 1          # K % 32
+    assert L.moe_quantize_act(FAKE, 4, 128, 9, FAKE, FAKE, NUL) == 1          # format
+    assert L.moe_router_logits(FAKE, FAKE, 4, 100, 8, FAKE, NUL) == 1         # H % 8
+    assert L.moe_router_logits(FAKE, FAKE, 4, 128, 0, FAKE, NUL) == 1
+    assert L.moe_probe_scaled_mfma(NUL, FAKE, 0, FAKE, FAKE, FAKE, NUL) == 1

@@ -1,0 +1,217 @@
+"""GPU parity of the individual kernels against the oracle (through the C ABI).
+
+Integer work (route ids, permutation, activation codes and scales) must match
+bit for bit; routing weights to 1e-6 relative."""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import moe as omoe
+from oracle import mx
+from tests.gpu_common import bf16_bits, log, to_dev_bf16, to_dev_u8
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def m():
+    from paper_2609_15627_amd import moe
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return moe
+
+
+# --------------------------------------------------------------------------- probe
+def _probe(m, codes, sa, bcodes, sb, fmt):
+    a_bytes = codes.astype(np.uint8) if fmt == "e4m3" else mx.pack_nibbles(codes.astype(np.uint8))
+    b_bytes = mx.pack_nibbles(bcodes)
+    d = m.moe_probe_scaled_mfma(to_dev_u8(a_bytes), to_dev_u8(sa), to_dev_u8(b_bytes),
+                                to_dev_u8(sb), fmt=fmt)
+    torch.cuda.synchronize()
+    A = mx.mx_dequantize(codes, sa, fmt)
+    B = mx.dequant_fp4(b_bytes, sb)
+    prod = np.abs(A)[:, None, :] * np.abs(B)[None, :, :]          # |A_ik B_jk|
+    return d.cpu().numpy().astype(np.float64), A @ B.T, prod.sum(-1), prod.max(-1)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e2m1"])
+def test_probe_scaled_mfma_layout(m, fmt):
+    """One 16x16x128 block-scaled product with non-constant scales, against
+    the oracle's dequantised operands: pins operand, K-block and scale
+    placement of the matrix-core instruction as the GEMM uses it.
+
+    Operands whose products share a narrow exponent range come out as an fp32
+    sum would (error <= K * 2^-24 * sum|products|): any misplaced element or
+    scale would be off by orders of magnitude more."""
+    log(f"probe {fmt}")
+    rng = np.random.default_rng(0)
+    if fmt == "e4m3":
+        codes = rng.integers(0x40, 0x78, (16, 128)) | (rng.integers(0, 2, (16, 128)) << 7)
+    else:
+        codes = rng.integers(0, 16, (16, 128))
+    sa = rng.integers(120, 134, (16, 4)).astype(np.uint8)
+    bcodes = rng.integers(0, 16, (16, 128)).astype(np.uint8)
+    sb = rng.integers(122, 131, (16, 4)).astype(np.uint8)
+    got, want, cond, _ = _probe(m, codes, sa, bcodes, sb, fmt)
+    ratio = np.abs(got - want) / cond
+    log(f"  max |err| / sum|products| = {ratio.max():.3e}")
+    assert np.all(ratio <= 128 * 2.0 ** -24)
+
+
+def test_probe_fp8_wide_range_precision(m):
+    """FP8 codes spanning the whole e4m3 range inside one instruction: the
+    matrix core aligns the products of one instruction to a limited number of
+    bits below the largest, so small products lose low bits. Measured bound:
+    |err| <= 2^-9 * max_k |A_ik B_jk| (observed about 2^-12)."""
+    log("probe e4m3 wide range")
+    rng = np.random.default_rng(1)
+    codes = rng.integers(0, 0x7F, (16, 128)) | (rng.integers(0, 2, (16, 128)) << 7)
+    sa = rng.integers(120, 134, (16, 4)).astype(np.uint8)
+    bcodes = rng.integers(0, 16, (16, 128)).astype(np.uint8)
+    sb = rng.integers(122, 131, (16, 4)).astype(np.uint8)
+    got, want, _, pmax = _probe(m, codes, sa, bcodes, sb, "e4m3")
+    r = np.abs(got - want) / pmax
+    log(f"  max |err| / max|product| = {r.max():.3e}")
+    assert np.all(r <= 2.0 ** -9)
+
+
+# --------------------------------------------------------------------------- route
+def _check_route(m, logits, k, n_shared):
+    ids_ref, w_ref = omoe.route_topk(logits, k, n_shared)
+    ids, w = m.moe_route_topk(torch.from_numpy(logits).cuda(), k, n_shared)
+    torch.cuda.synchronize()
+    ids, w = ids.cpu().numpy(), w.cpu().numpy().astype(np.float64)
+    assert np.array_equal(ids, ids_ref)
+    assert np.all(np.abs(w - w_ref) <= 1e-6 * np.abs(w_ref))
+    assert np.all(np.abs(w[:, :k].sum(1) - 1.0) <= 8 * 2.0 ** -24 + 1e-7)
+
+
+@pytest.mark.parametrize("name", ["decode", "prefill8k", "skew32k", "tpshard"])
+def test_route_configs(m, name):
+    cfg = synth.CONFIGS[name]
+    log(f"route {name}")
+    _check_route(m, synth.gen_logits(cfg), cfg.k, cfg.n_shared)
+
+
+@pytest.mark.parametrize("T,E,k,S", [(1, 1, 1, 0), (5, 8, 8, 1), (33, 64, 6, 0), (70, 65, 7, 1),
+                                     (9, 1000, 32, 0), (100, 130, 31, 1)])
+def test_route_shapes_and_ties(m, T, E, k, S):
+    log(f"route T={T} E={E} k={k} S={S}")
+    rng = np.random.default_rng(T * 1000 + E)
+    lg = rng.integers(-3, 3, (T, E)).astype(np.float32)        # many exact ties
+    lg[0, :] = 0.0
+    if E > 2:
+        lg[-1, 1] = -np.inf
+        lg[-1, 2] = -0.0
+    _check_route(m, lg, k, S)
+    _check_route(m, rng.standard_normal((T, E)).astype(np.float32), k, S)
+
+
+def test_route_empty(m):
+    ids, w = m.moe_route_topk(torch.empty((0, 8), dtype=torch.float32, device="cuda"), 2)
+    torch.cuda.synchronize()
+    assert ids.shape == (0, 2)
+
+
+# --------------------------------------------------------------------------- permute
+def _check_permute(m, ids, ne):
+    ref = omoe.permute(ids, ne)
+    got = m.moe_permute(torch.from_numpy(ids.astype(np.int32)).cuda(), ne)
+    torch.cuda.synchronize()
+    for r, g, name in zip(ref, got, ("counts", "offsets", "sorted", "pos")):
+        assert np.array_equal(g.cpu().numpy(), r), name
+
+
+@pytest.mark.parametrize("name", ["tiny", "decode", "prefill8k", "skew32k", "tpshard"])
+def test_permute_configs(m, name):
+    cfg = synth.CONFIGS[name]
+    log(f"permute {name}")
+    if cfg.routing == "router":
+        lg = omoe.router_logits(synth.gen_x(cfg), synth.gen_router_weight(cfg)).astype(np.float32)
+    else:
+        lg = synth.gen_logits(cfg)
+    ids, _ = omoe.route_topk(lg, cfg.k, cfg.n_shared)
+    _check_permute(m, ids, cfg.NE)
+
+
+@pytest.mark.parametrize("T,kt,ne", [(0, 3, 5), (1, 1, 1), (7, 3, 5), (341, 3, 2048), (342, 3, 7),
+                                     (1000, 9, 257), (5000, 2, 1), (3000, 32, 1100)])
+def test_permute_shapes(m, T, kt, ne):
+    log(f"permute T={T} kt={kt} ne={ne}")
+    rng = np.random.default_rng(T + ne)
+    ids = rng.integers(0, ne, (T, kt))
+    if T > 10:
+        ids[: T // 2] = rng.integers(0, min(ne, 3), (T // 2, kt))   # skewed
+    _check_permute(m, ids, ne)
+
+
+# --------------------------------------------------------------------------- quantise
+def _codes_from_bytes(b, fmt, K):
+    if fmt == "e4m3":
+        return b
+    if fmt == "e2m1":
+        return mx.unpack_nibbles(b)
+    bits = np.unpackbits(b.reshape(b.shape[0], -1, 24), axis=-1, bitorder="little")
+    bits = bits.reshape(b.shape[0], -1, 32, 6)
+    return (bits * (1 << np.arange(6))).sum(-1).reshape(b.shape[0], K).astype(np.uint8)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e2m3", "e2m1"])
+def test_quantize_act_bit_exact(m, fmt):
+    log(f"quant {fmt}")
+    rng = np.random.default_rng(1)
+    K = 4096
+    x = synth.f32_to_bf16_bits(rng.standard_normal((64, K), dtype=np.float32)
+                               * np.exp(rng.uniform(-30, 30, (64, 1))).astype(np.float32))
+    x[0, :64] = 0                        # all-zero block
+    x[1, :32] = 0x8000                   # -0.0 block
+    x[2, 5] = 0x0001                     # bf16 subnormal
+    allb = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    fin = allb[np.isfinite(mx.bf16_to_f64(allb))]
+    extra = np.resize(fin, (-(-fin.size // K), K))           # every finite bf16 value
+    x = np.concatenate([x, extra])
+    codes_ref, sc_ref = mx.mx_quantize(mx.bf16_to_f64(x), fmt)
+    codes, sc = m.moe_quantize_act(to_dev_bf16(x), fmt)
+    torch.cuda.synchronize()
+    assert np.array_equal(sc.cpu().numpy(), sc_ref)
+    got = _codes_from_bytes(codes.cpu().numpy(), fmt, K)
+    assert np.array_equal(got, codes_ref)
+
+
+# --------------------------------------------------------------------------- combine
+def _round_f32(fr):
+    """Round an exact rational to the nearest fp32, ties to even."""
+    c = np.float32(float(fr))
+    best = None
+    for cand in (np.nextafter(c, np.float32(-np.inf)), c, np.nextafter(c, np.float32(np.inf))):
+        d = abs(Fraction(float(cand)) - fr)
+        even = (int(np.float32(cand).view(np.uint32)) & 1) == 0
+        if best is None or d < best[0] or (d == best[0] and even):
+            best = (d, cand)
+    return best[1]
+
+
+def test_combine_fixed_order(m):
+    log("combine")
+    rng = np.random.default_rng(2)
+    T, kt, H = 37, 9, 256
+    P = (rng.standard_normal((T * kt, H)) * 1e4).astype(np.float32)
+    w = rng.random((T, kt)).astype(np.float32)
+    w[:, -1] = 1.0
+    out = m.moe_combine_fixed_order(torch.from_numpy(P).cuda(), torch.from_numpy(w).cuda())
+    torch.cuda.synchronize()
+    got = bf16_bits(out)
+    # the fp32 fixed-order fma chain, evaluated with exact rationals and one
+    # correctly rounded fp32 result per step
+    for t, h in [(0, 0), (5, 17), (36, 255), (20, 128)]:
+        acc = np.float32(0)
+        for j in range(kt):
+            exact = Fraction(float(w[t, j])) * Fraction(float(P[t * kt + j, h])) + Fraction(float(acc))
+            acc = _round_f32(exact)
+        want = mx.f64_to_bf16(np.array([float(acc)]))[0]
+        assert got[t, h] == want
+    ref = (w.astype(np.float64)[:, :, None] * P.reshape(T, kt, H).astype(np.float64)).sum(1)
+    gotf = mx.bf16_to_f64(got)
+    assert np.all(np.abs(gotf - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-3)

@@ -1,0 +1,203 @@
+"""GPU parity of the whole layer (route -> permute -> grouped GEMM -> combine)
+against the fp64 oracle, through the C ABI, in the launch configuration the
+benchmark times.
+
+Bar (bf16 output): max over tokens of max_h |y - y*| / max_h |y*| <= 1e-2,
+against the oracle with the same activation quantisation; route ids and the
+permutation bit-exact; activation codes bit-exact; ten repeated runs
+bit-identical."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import moe as omoe
+from oracle import mx
+from tests import gpu_common as gc
+from tests.gpu_common import log
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+@pytest.fixture(scope="module")
+def m():
+    from paper_2609_15627_amd import moe
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return moe
+
+
+def run_layer(m, cfg, x_dev, weights, logits=None, wr=None, fmt="e4m3"):
+    layer = m.MoELayer(cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.n_shared, fmt)
+    lg = None if logits is None else torch.from_numpy(logits).cuda()
+    out = layer.forward(x_dev, weights, logits=lg, w_router=wr)
+    torch.cuda.synchronize()
+    return layer, out
+
+
+def check_against_oracle(cfg, inp, layer, out, tokens, fmt="e4m3", logits=None):
+    ref = omoe.layer(inp.x, *inp.weights, k=cfg.k, n_shared=cfg.n_shared,
+                     logits=inp.logits if logits is None else logits, fmt=fmt, tokens=tokens,
+                     keep=True)
+    y = gc.bf16_to_f64(gc.bf16_bits(out)[tokens])
+    err = gc.rowrel(y, ref["out_f64"])
+    log(f"  rowrel={err:.3e} vs oracle-Q; tokens={len(tokens)}")
+    assert err <= TOL
+    # partials of every (token, slot), before the routing weights
+    # Partials of single experts: an h value at a rounding midpoint can land on
+    # the other code on the GPU (fp32 h) than in the oracle (fp64 h); with FP4
+    # codes one such step moves a partial by a few percent of its row maximum.
+    P = layer.partials.view(cfg.T, cfg.k_total, cfg.H).cpu().numpy()[tokens]
+    perr = gc.rowrel(P.reshape(-1, cfg.H), ref["p_slots"].reshape(-1, cfg.H))
+    assert perr <= (TOL if fmt == "e4m3" else 5e-2), perr
+    return ref, err
+
+
+def small_case(T, H, I, E, k, S, seed, routing="normal"):
+    cfg = synth.LayerConfig("small", T, H, E, k, I, S, routing, seed)
+    return cfg, synth.make_inputs(cfg)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e2m1"])
+@pytest.mark.parametrize("shape", [
+    (37, 512, 384, 16, 4, 1),     # ragged: ~10 rows per expert, K tail, 3 h tiles
+    (200, 384, 384, 4, 2, 0),     # many rows per expert: 7 row tiles with a ragged tail
+    (64, 1024, 256, 64, 8, 1),    # decode-like spread
+    (3, 256, 128, 8, 8, 1),       # k = E
+    (1, 128, 128, 1, 1, 0),       # smallest shape
+])
+def test_small_layers(m, shape, fmt):
+    cfg, inp = small_case(*shape, seed=sum(shape))
+    log(f"small layer {shape} {fmt}")
+    weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, logits=inp.logits, fmt=fmt)
+    ref, _ = check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T), fmt)
+    assert np.array_equal(layer.ids.cpu().numpy(), ref["ids"])
+    assert np.array_equal(layer.perm[2].cpu().numpy(), ref["sorted"])
+    xq = layer.workspace_view(0)[: cfg.T * m.act_code_bytes(cfg.H, fmt)].cpu().numpy()
+    if fmt == "e4m3":
+        assert np.array_equal(xq.reshape(cfg.T, cfg.H), ref["xq"])
+
+
+def test_tiny_config_with_router(m):
+    """The tiny workload end to end, logits from the bf16 router weights."""
+    cfg = synth.CONFIGS["tiny"]
+    inp = synth.make_inputs(cfg)
+    log("tiny config")
+    weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    wr = gc.to_dev_bf16(inp.wr)
+    layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, wr=wr)
+    lg64 = omoe.router_logits(inp.x, inp.wr)
+    lg_gpu = layer.logits.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(lg_gpu - lg64) <= 1e-5 * np.abs(lg64).max())
+    # the oracle routes on its own logits; no near-ties in this workload
+    srt = np.sort(lg64, axis=1)[:, ::-1]
+    assert np.all(srt[:, cfg.k - 1] - srt[:, cfg.k] > 1e-5)
+    ref = omoe.layer(inp.x, *inp.weights, k=cfg.k, wr_bits=inp.wr, keep=True)
+    assert np.array_equal(layer.ids.cpu().numpy(), ref["ids"])
+    y = gc.bf16_to_f64(gc.bf16_bits(out))
+    err = gc.rowrel(y, ref["out_f64"])
+    log(f"  tiny rowrel={err:.3e}")
+    assert err <= TOL
+
+
+def test_hand_cases_exact(m):
+    """H1 and H2 (tests/golden/hand_cases.json) come out exactly on the GPU."""
+    log("hand cases")
+    x = gc.to_dev_bf16(np.full((1, 128), 0x3F00, np.uint16))
+
+    def const(h, i, w2_scale=127):
+        b = 2 | (2 << 4)
+        return (np.full((2 * i, h // 2), b, np.uint8), np.full((2 * i, h // 32), 127, np.uint8),
+                np.full((h, i // 2), b, np.uint8), np.full((h, i // 32), w2_scale, np.uint8))
+    # H = I = 128: G = U = 64, h = 4096/(1+e^-64) -> 4096, P = 128*4096 = 524288
+    w = tuple(gc.to_dev_u8(np.stack([a])) for a in const(128, 128))
+    cfg = synth.LayerConfig("h1", 1, 128, 1, 1, 128, 0)
+    _, out = run_layer(m, cfg, x, w, logits=np.zeros((1, 1), np.float32))
+    assert np.all(gc.bf16_to_f64(gc.bf16_bits(out)) == 524288.0)
+    e0, e2 = const(128, 128), const(128, 128, 128)
+    w = tuple(gc.to_dev_u8(np.stack(z)) for z in zip(e0, e0, e2, e0))
+    cfg = synth.LayerConfig("h2", 1, 128, 4, 2, 128, 0)
+    layer, out = run_layer(m, cfg, x, w, logits=np.array([[1, 3, 3, 0]], np.float32))
+    assert layer.ids.cpu().numpy().tolist() == [[1, 2]]
+    assert np.all(gc.bf16_to_f64(gc.bf16_bits(out)) == 0.5 * 524288 + 0.5 * 2 * 524288)
+
+
+def test_empty_tokens(m):
+    log("T = 0")
+    cfg = synth.LayerConfig("empty", 0, 256, 8, 2, 128, 1)
+    w = tuple(gc.to_dev_u8(a) for a in synth.gen_all_experts(cfg))
+    layer = m.MoELayer(0, 256, 8, 2, 128, 1)
+    out = layer.forward(torch.empty((0, 256), dtype=torch.bfloat16, device="cuda"), w,
+                        logits=torch.empty((0, 8), dtype=torch.float32, device="cuda"))
+    torch.cuda.synchronize()
+    assert out.shape == (0, 256)
+    assert layer.perm[1].cpu().numpy().tolist() == [0] * 10
+
+
+def _sample_tokens(cfg, ids, n):
+    """Tokens of the most and least loaded non-empty routed experts, plus seeded picks."""
+    routed = ids[:, :cfg.k]
+    cnt = np.bincount(routed.ravel(), minlength=cfg.E)
+    nz = np.nonzero(cnt)[0]
+    hi, lo = nz[np.argmax(cnt[nz])], nz[np.argmin(cnt[nz])]
+    t_hi = int(np.nonzero((routed == hi).any(1))[0][0])
+    t_lo = int(np.nonzero((routed == lo).any(1))[0][-1])
+    rng = np.random.default_rng(7)
+    extra = rng.choice(cfg.T, max(0, n - 2), replace=False)
+    return np.unique(np.concatenate([[t_hi, t_lo, cfg.T - 1], extra]))[:max(n, 2)]
+
+
+@pytest.mark.parametrize("name,ntok", [("decode", 3), ("prefill8k", 2), ("skew32k", 2),
+                                       ("tpshard", 6)])
+def test_full_size_configs(m, name, ntok):
+    """Full-size workloads: route, permutation and activation codes compared in
+    full; outputs and partials on sampled tokens; determinism over ten runs
+    (tpshard) or three (others)."""
+    cfg = synth.CONFIGS[name]
+    log(f"full {name}: generating inputs")
+    inp = synth.make_inputs(cfg, lazy=True)
+    weights = gc.dev_weights(cfg)
+    x = gc.to_dev_bf16(inp.x)
+    log(f"full {name}: forward")
+    layer, out = run_layer(m, cfg, x, weights, logits=inp.logits)
+    variant = m.moe_last_variant()
+    ids_ref, w_ref = omoe.route_topk(inp.logits, cfg.k, cfg.n_shared)
+    assert np.array_equal(layer.ids.cpu().numpy(), ids_ref)
+    perm_ref = omoe.permute(ids_ref, cfg.NE)
+    for g, r in zip(layer.perm, perm_ref):
+        assert np.array_equal(g.cpu().numpy(), r)
+    xq = layer.workspace_view(0)[: cfg.T * cfg.H].cpu().numpy().reshape(cfg.T, cfg.H)
+    rows = np.arange(0, cfg.T, max(1, cfg.T // 256))
+    xq_ref, _ = mx.mx_quantize(mx.bf16_to_f64(inp.x[rows]), "e4m3")
+    assert np.array_equal(xq[rows], xq_ref)
+    tokens = _sample_tokens(cfg, ids_ref, ntok)
+    log(f"full {name}: oracle on tokens {tokens.tolist()} (variant {variant})")
+    check_against_oracle(cfg, inp, layer, out, tokens)
+    first = gc.bf16_bits(out).copy()
+    reps = 10 if name == "tpshard" else 3
+    for _ in range(reps - 1):
+        out2 = layer.forward(x, weights, logits=torch.from_numpy(inp.logits).cuda())
+        torch.cuda.synchronize()
+        assert np.array_equal(gc.bf16_bits(out2), first)
+    log(f"full {name}: {reps} runs bit-identical")
+
+
+def test_metamorphic_w2_scale_doubles_output(m):
+    """W2 scale bytes + 1 => every output exactly x2 on the GPU (bitwise)."""
+    cfg = synth.LayerConfig("mm", 96, 512, 16, 4, 256, 1, "normal", 3)
+    inp = synth.make_inputs(cfg)
+    log("metamorphic w2 scale")
+    w = [gc.to_dev_u8(a) for a in inp.weights]
+    x = gc.to_dev_bf16(inp.x)
+    _, out = run_layer(m, cfg, x, tuple(w), logits=inp.logits)
+    base = gc.bf16_to_f64(gc.bf16_bits(out))
+    w[3] = w[3] + 1
+    _, out2 = run_layer(m, cfg, x, tuple(w), logits=inp.logits)
+    assert np.array_equal(gc.bf16_to_f64(gc.bf16_bits(out2)), 2 * base)
+    # token permutation permutes output rows bit-exactly
+    perm = np.random.default_rng(0).permutation(cfg.T)
+    w[3] = w[3] - 1
+    _, out3 = run_layer(m, cfg, gc.to_dev_bf16(inp.x[perm]), tuple(w), logits=inp.logits[perm])
+    assert np.array_equal(gc.bf16_bits(out3), gc.bf16_bits(out)[perm])
