@@ -124,6 +124,9 @@ def main():
     ap.add_argument("--no-prefill", action="store_true", help="skip the 8K prefill measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=2)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB five times (the "
+                         "reference for scaling HBM byte counters) and exit")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -135,6 +138,20 @@ def main():
 
     import synth
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        for i in range(5):
+            ev[i].record()
+            dst.copy_(src)
+        ev[5].record()
+        torch.cuda.synchronize()
+        ms = min(ev[i].elapsed_time(ev[i + 1]) for i in range(1, 5))
+        print(json.dumps({"calibrate_copy_bytes": n, "copies": 5, "best_ms": ms,
+                          "copy_GBps_read_plus_write": 2 * n / ms / 1e6}), flush=True)
+        return
     cfg = synth.CONFIGS[args.config]
     log(f"generating weights for {cfg.name}")
     weights_np = synth.gen_all_experts(cfg.with_(E=cfg.E, n_shared=max(cfg.n_shared, 0)))

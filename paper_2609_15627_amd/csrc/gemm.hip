@@ -1,0 +1,119 @@
+// a5 / a6: the grouped FP4 expert GEMM behind moe_fp4_grouped_gemm --
+// activation quantisation, row-tile list, geometry choice, stage launches.
+#include "gemm_common.h"
+#include "gemm_launch.h"
+#include "moe_launch.h"
+
+namespace moe {
+
+// ---------------------------------------------------------------------------
+// Tile list: expert e with c rows gets ceil(c / BM) row tiles. One block of
+// 1024 threads: tile counts, exclusive scan, then every thread fills tiles
+// i = tid, tid + 1024, ... by binary search over the per-expert tile starts.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void build_tiles_kernel(const int32_t* __restrict__ offsets,
+                                                           int NE, int BM, int4* __restrict__ tiles,
+                                                           int* __restrict__ ntiles) {
+  extern __shared__ int start[];  // [NE + 1]
+  int m[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int e = threadIdx.x + 1024 * q;
+    m[q] = e < NE ? (offsets[e + 1] - offsets[e] + BM - 1) / BM : 0;
+  }
+  int t0, t1;
+  const int p0 = block_exclusive_scan_1024(m[0], &t0);
+  const int p1 = block_exclusive_scan_1024(m[1], &t1) + t0;
+  if (threadIdx.x < NE) start[threadIdx.x] = p0;
+  if (threadIdx.x + 1024 < NE) start[threadIdx.x + 1024] = p1;
+  const int total = t0 + t1;
+  if (threadIdx.x == 0) {
+    start[NE] = total;
+    *ntiles = total;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < total; i += 1024) {
+    int lo = 0, hi = NE;  // find e with start[e] <= i < start[e + 1]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (start[mid] <= i) lo = mid; else hi = mid;
+    }
+    const int j = i - start[lo];
+    const int r0 = offsets[lo] + j * BM;
+    tiles[i] = make_int4(lo, r0, min(BM, offsets[lo + 1] - r0), 0);
+  }
+}
+
+static int tile_bound(long A, int NE, int BM) {
+  const long nonempty = A < NE ? A : NE;
+  return (int)((A + nonempty * (BM - 1)) / BM);
+}
+
+GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt) {
+  auto al = [](size_t v) { return (v + 255) / 256 * 256; };
+  const size_t A = (size_t)T * k_total;
+  const size_t bits = act_bits(fmt);
+  GemmWorkspace w;
+  size_t o = 0;
+  w.off[0] = o;  o += al((size_t)T * H * bits / 8);
+  w.off[1] = o;  o += al((size_t)T * (H / 32));
+  w.off[2] = o;  o += al(A * I * bits / 8);
+  w.off[3] = o;  o += al(A * (I / 32));
+  w.off[4] = o;  o += al(sizeof(int4) * ((size_t)tile_bound((long)A, NE, 16) + 1) + 16);
+  w.off[5] = o;
+  return w;
+}
+
+static hipError_t launch_streaming(const GemmArgs& a, const GemmWorkspace& w, int stages,
+                                   hipStream_t s) {
+  constexpr int BM = 16;
+  const long A = (long)a.T * a.k_total;
+  const int mt = tile_bound(A, a.NE, BM);
+  int4* tiles = reinterpret_cast<int4*>(a.ws + w.off[4]);
+  int* ntiles = reinterpret_cast<int*>(tiles + mt + 1);
+  if (stages & 1) {
+    hipError_t err = launch_quantize_act(a.x, a.T, a.H, a.fmt, a.ws + w.off[0], a.ws + w.off[1], s);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(build_tiles_kernel, dim3(1), dim3(1024), (a.NE + 1) * sizeof(int), s,
+                       a.offsets, a.NE, BM, tiles, ntiles);
+  }
+  if (stages & 2) {
+    S1Args p1;
+    p1.xq = a.ws + w.off[0];
+    p1.xs = a.ws + w.off[1];
+    p1.sorted = a.sorted;
+    p1.w13 = a.w13;
+    p1.w13s = a.w13_s;
+    p1.hq = a.ws + w.off[2];
+    p1.hs = a.ws + w.off[3];
+    p1.H = a.H;
+    p1.I = a.I;
+    p1.k_total = a.k_total;
+    p1.t = TileArgs{tiles, ntiles, mt, 0, 1};
+    launch_s1_stream(p1, mt, a.fmt, s);
+  }
+  if (stages & 4) {
+    S2Args p2;
+    p2.hq = a.ws + w.off[2];
+    p2.hs = a.ws + w.off[3];
+    p2.sorted = a.sorted;
+    p2.w2 = a.w2;
+    p2.w2s = a.w2_s;
+    p2.partials = a.partials;
+    p2.H = a.H;
+    p2.I = a.I;
+    p2.t = TileArgs{tiles, ntiles, mt, 0, 1};
+    launch_s2_stream(p2, mt, a.fmt, s);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int* variant) {
+  const GemmWorkspace w = gemm_workspace(a.T, a.H, a.I, a.NE, a.k_total, a.fmt);
+  *variant = 1;
+  if (a.T == 0) return hipSuccess;
+  if (a.fmt != 0 && a.fmt != 4) return hipErrorNotSupported;
+  return launch_streaming(a, w, stages, s);
+}
+
+}  // namespace moe

@@ -1,0 +1,15 @@
+// Launchers of the grouped-GEMM kernels of each geometry (host side).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "gemm_common.h"
+
+namespace moe {
+
+// Weight-streaming geometry. mt: row tiles the grid is sized for; fa:
+// activation operand format code.
+void launch_s1_stream(const S1Args& p, long mt, int fa, hipStream_t s);
+void launch_s2_stream(const S2Args& p, long mt, int fa, hipStream_t s);
+
+}  // namespace moe
