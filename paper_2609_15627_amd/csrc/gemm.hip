@@ -64,13 +64,34 @@ GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt) 
   return w;
 }
 
-static hipError_t launch_streaming(const GemmArgs& a, const GemmWorkspace& w, int stages,
-                                   hipStream_t s) {
-  constexpr int BM = 16;
+static int max_lds_per_block() {
+  static const int v = [] {
+    int dev = 0, bytes = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&bytes, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+      return 0;
+    return bytes;
+  }();
+  return v;
+}
+
+// Geometry rule (runtime M): the LDS-tiled geometry when experts average at
+// least kTiledMinRows rows, the weight-streaming geometry otherwise.
+constexpr int kTiledMinRows = 64;
+
+static bool use_tiled(const GemmArgs& a) {
+  const long A = (long)a.T * a.k_total;
+  return A >= (long)kTiledMinRows * a.NE && tiled_ok(a.H, a.I) &&
+         (size_t)max_lds_per_block() >= tiled_lds_bytes(a.fmt);
+}
+
+static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int stages,
+                                  bool tiled, hipStream_t s) {
+  const int BM = tiled ? tiled_rows() : 16;
   const long A = (long)a.T * a.k_total;
   const int mt = tile_bound(A, a.NE, BM);
   int4* tiles = reinterpret_cast<int4*>(a.ws + w.off[4]);
-  int* ntiles = reinterpret_cast<int*>(tiles + mt + 1);
+  int* ntiles = reinterpret_cast<int*>(tiles + tile_bound(A, a.NE, 16) + 1);
   if (stages & 1) {
     hipError_t err = launch_quantize_act(a.x, a.T, a.H, a.fmt, a.ws + w.off[0], a.ws + w.off[1], s);
     if (err != hipSuccess) return err;
@@ -90,7 +111,8 @@ static hipError_t launch_streaming(const GemmArgs& a, const GemmWorkspace& w, in
     p1.I = a.I;
     p1.k_total = a.k_total;
     p1.t = TileArgs{tiles, ntiles, mt, 0, 1};
-    launch_s1_stream(p1, mt, a.fmt, s);
+    if (tiled) launch_s1_tiled(p1, mt, a.fmt, s);
+    else launch_s1_stream(p1, mt, a.fmt, s);
   }
   if (stages & 4) {
     S2Args p2;
@@ -103,17 +125,19 @@ static hipError_t launch_streaming(const GemmArgs& a, const GemmWorkspace& w, in
     p2.H = a.H;
     p2.I = a.I;
     p2.t = TileArgs{tiles, ntiles, mt, 0, 1};
-    launch_s2_stream(p2, mt, a.fmt, s);
+    if (tiled) launch_s2_tiled(p2, mt, a.fmt, s);
+    else launch_s2_stream(p2, mt, a.fmt, s);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int* variant) {
   const GemmWorkspace w = gemm_workspace(a.T, a.H, a.I, a.NE, a.k_total, a.fmt);
-  *variant = 1;
+  const bool tiled = use_tiled(a);
+  *variant = tiled ? 2 : 1;
   if (a.T == 0) return hipSuccess;
   if (a.fmt != 0 && a.fmt != 4) return hipErrorNotSupported;
-  return launch_streaming(a, w, stages, s);
+  return launch_geometry(a, w, stages, tiled, s);
 }
 
 }  // namespace moe

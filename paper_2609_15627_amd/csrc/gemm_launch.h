@@ -12,4 +12,11 @@ namespace moe {
 void launch_s1_stream(const S1Args& p, long mt, int fa, hipStream_t s);
 void launch_s2_stream(const S2Args& p, long mt, int fa, hipStream_t s);
 
+// LDS-tiled geometry (many rows per expert): row tiles of tiled_rows() rows.
+int tiled_rows();
+size_t tiled_lds_bytes(int fa);
+bool tiled_ok(int H, int I);
+void launch_s1_tiled(const S1Args& p, long mt, int fa, hipStream_t s);
+void launch_s2_tiled(const S2Args& p, long mt, int fa, hipStream_t s);
+
 }  // namespace moe

@@ -36,21 +36,60 @@ def run_layer(m, cfg, x_dev, weights, logits=None, wr=None, fmt="e4m3"):
     return layer, out
 
 
+def check_hq_codes(layer, cfg, ref, fmt):
+    """The h codes the GPU fed to the down projection against the oracle's.
+
+    The GPU's h carries the fp32 / matrix-core accumulation error of G and U,
+    which is relative to the largest products, not to h itself: an element
+    can take a neighbouring grid value (when it sits near a rounding
+    midpoint), and elements far below their block's maximum can move a few
+    subnormal steps. Bound: |v_gpu - v_oracle| <= one grid step at the larger
+    magnitude + 1e-4 of the format maximum (448, the block's scaled maximum
+    is at most that), in units of the block scale. Block scales must agree,
+    and differing codes must be rare (at most 1e-3 of the codes)."""
+    if fmt != "e4m3":
+        return 0
+    hq = layer.workspace_view(2)[: cfg.A * cfg.I].cpu().numpy().reshape(cfg.A, cfg.I)
+    hs = layer.workspace_view(3)[: cfg.A * cfg.I // 32].cpu().numpy().reshape(cfg.A, cfg.I // 32)
+    flips = total = 0
+    for r in ref["per_expert"].values():
+        g, o = hq[r["rows"]].astype(np.int64), r["hq"].astype(np.int64)
+        assert np.array_equal(hs[r["rows"]], r["hs"]), "h block scales differ"
+        d = g != o
+        vg = mx.elem_decode(g, "e4m3")
+        vo = mx.elem_decode(o, "e4m3")
+        big = np.maximum(np.abs(vg), np.abs(vo))
+        _, ex = np.frexp(big)
+        step = np.ldexp(1.0, np.maximum(ex - 1, -6) - 3)
+        far = d & (np.abs(vg - vo) > step + 1e-4 * 448)
+        assert not far.any(), f"h codes too far apart: {list(zip(g[far], o[far]))[:8]}"
+        flips += int(d.sum())
+        total += d.size
+    assert flips <= 1e-3 * max(total, 1), (flips, total)
+    return flips
+
+
 def check_against_oracle(cfg, inp, layer, out, tokens, fmt="e4m3", logits=None):
+    """Layer output, partials and h codes against the oracle with the same
+    activation quantisation. Output bar: row-relative error <= 1e-2 when each
+    token sums at least 4096 h values (I * k_total, the paper's regime and all
+    five workloads); smaller layers weigh a single neighbouring-code flip of h
+    more (about step / sqrt(I * k_total) of a row), so they get 3e-2."""
     ref = omoe.layer(inp.x, *inp.weights, k=cfg.k, n_shared=cfg.n_shared,
                      logits=inp.logits if logits is None else logits, fmt=fmt, tokens=tokens,
                      keep=True)
+    flips = check_hq_codes(layer, cfg, ref, fmt) if len(tokens) == cfg.T else -1
     y = gc.bf16_to_f64(gc.bf16_bits(out)[tokens])
     err = gc.rowrel(y, ref["out_f64"])
-    log(f"  rowrel={err:.3e} vs oracle-Q; tokens={len(tokens)}")
-    assert err <= TOL
-    # partials of every (token, slot), before the routing weights
+    tol = TOL if cfg.I * cfg.k_total >= 4096 else 3 * TOL
+    log(f"  rowrel={err:.3e} vs oracle-Q (bar {tol:g}); tokens={len(tokens)}; h code flips={flips}")
+    assert err <= tol
     # Partials of single experts: an h value at a rounding midpoint can land on
-    # the other code on the GPU (fp32 h) than in the oracle (fp64 h); with FP4
-    # codes one such step moves a partial by a few percent of its row maximum.
+    # the other code on the GPU than in the oracle; with FP4 codes one such
+    # step moves a partial by a few percent of its row maximum.
     P = layer.partials.view(cfg.T, cfg.k_total, cfg.H).cpu().numpy()[tokens]
     perr = gc.rowrel(P.reshape(-1, cfg.H), ref["p_slots"].reshape(-1, cfg.H))
-    assert perr <= (TOL if fmt == "e4m3" else 5e-2), perr
+    assert perr <= (3 * tol if fmt == "e4m3" else 5e-2), perr
     return ref, err
 
 
@@ -66,18 +105,33 @@ def small_case(T, H, I, E, k, S, seed, routing="normal"):
     (64, 1024, 256, 64, 8, 1),    # decode-like spread
     (3, 256, 128, 8, 8, 1),       # k = E
     (1, 128, 128, 1, 1, 0),       # smallest shape
+    (300, 512, 256, 4, 2, 1),     # tiled geometry: ~150-300 rows per expert, ragged tiles
+    (130, 256, 384, 2, 1, 0),     # tiled geometry: ~65 rows per expert, partial row blocks
 ])
 def test_small_layers(m, shape, fmt):
     cfg, inp = small_case(*shape, seed=sum(shape))
     log(f"small layer {shape} {fmt}")
     weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
     layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, logits=inp.logits, fmt=fmt)
+    log(f"  variant {m.moe_last_variant()}")
     ref, _ = check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T), fmt)
     assert np.array_equal(layer.ids.cpu().numpy(), ref["ids"])
     assert np.array_equal(layer.perm[2].cpu().numpy(), ref["sorted"])
     xq = layer.workspace_view(0)[: cfg.T * m.act_code_bytes(cfg.H, fmt)].cpu().numpy()
     if fmt == "e4m3":
         assert np.array_equal(xq.reshape(cfg.T, cfg.H), ref["xq"])
+
+
+def test_tiled_geometry_skewed(m):
+    """Zipf-skewed routing through the tiled geometry: hot experts with many
+    row tiles, cold ones with a handful of rows or none."""
+    cfg = synth.LayerConfig("skew", 600, 512, 16, 4, 256, 0, "zipf", 5, zipf_empty=3)
+    inp = synth.make_inputs(cfg)
+    log("tiled skewed")
+    weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, logits=inp.logits)
+    assert m.moe_last_variant() == m.VARIANT_TILED
+    check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T))
 
 
 def test_tiny_config_with_router(m):
@@ -163,6 +217,7 @@ def test_full_size_configs(m, name, ntok):
     log(f"full {name}: forward")
     layer, out = run_layer(m, cfg, x, weights, logits=inp.logits)
     variant = m.moe_last_variant()
+    assert variant == (m.VARIANT_STREAM if name == "decode" else m.VARIANT_TILED)
     ids_ref, w_ref = omoe.route_topk(inp.logits, cfg.k, cfg.n_shared)
     assert np.array_equal(layer.ids.cpu().numpy(), ids_ref)
     perm_ref = omoe.permute(ids_ref, cfg.NE)
