@@ -3,14 +3,13 @@
 //
 // Workgroup tile: 128 sorted rows of one expert x 256 weight rows (stage 1:
 // 128 gate rows and the 128 matching up rows; stage 2: 256 output columns),
-// K in steps of 128. Four waves in a 2 x 2 arrangement, each owning 64 rows x
-// 128 weight rows = 4 x 8 products of 16x16 per step (16x16x128 block-scaled
-// matrix-core instructions), so every activation fragment read from LDS is
-// used 8 times and every weight fragment 4 times.
+// K in steps of 128. NW waves (4 or 8) in a 2 x NW/2 arrangement, each owning
+// 64 rows x 512/NW weight rows = 4 x 32/NW products of 16x16 per step
+// (16x16x128 block-scaled matrix-core instructions).
 //
 // Global -> LDS: direct loads (global_load_lds_dwordx4 writes lane l's 16
-// bytes at LDS offset 16*l of the instruction's destination), two stages in
-// flight. Each lane picks the global address that lands in the right
+// bytes at LDS offset 16*l of the instruction's destination), several stages in
+// flight (kStages-deep ring). Each lane picks the global address that lands in the right
 // swizzled LDS slot:
 //   activation rows (FP8, 128 bytes per row and step): 16-byte chunk c of row
 //     r is stored at chunk c ^ ((r >> 1) & 7);
@@ -31,6 +30,10 @@
 #include "gemm_common.h"
 #include "gemm_launch.h"
 
+#ifndef TILED_WAVES
+#define TILED_WAVES 8
+#endif
+
 namespace moe {
 
 constexpr int TBM = 128, TBN = 256;
@@ -46,8 +49,18 @@ struct TStage {
   static constexpr int kAS = kB + TBN * 64;          // 128 activation scale dwords
   static constexpr int kBS = kAS + TBM * 4;          // 256 weight scale dwords
   static constexpr int kBytes = kBS + TBN * 4;
-  static constexpr int kAInstr = TBM * kARow / 4096;  // activation DMA instructions per wave
-  static constexpr int kLoads = kAInstr + 4 + 2;      // DMA instructions per wave per step
+  static constexpr int kAKB = TBM * kARow / 1024;    // activation KiB per step
+};
+
+// Work split of the workgroup's NW waves.
+template <int FA, int NW>
+struct TWaves {
+  static constexpr int kAInstr = TStage<FA>::kAKB / NW;   // activation DMA instructions per wave
+  static constexpr int kBInstr = 16 / NW;                 // weight DMA instructions per wave
+  static constexpr int kASRows = TBM / NW;                // activation scale rows per wave
+  static constexpr int kBSRows = TBN / NW;                // weight scale rows per wave
+  static constexpr int kLoads = kAInstr + kBInstr + 2;    // DMA instructions per wave per step
+  static constexpr int kNCB = 32 / NW;                    // 16-column blocks per wave
 };
 
 __device__ __forceinline__ void tdma16(const void* g, uint8_t* l) {
@@ -64,64 +77,102 @@ __device__ __forceinline__ void twait_vmcnt() {
 }
 
 // Per-lane source rows of the DMA instructions of one wave.
-template <int FA>
+template <int FA, int NW>
 struct TLoad {
-  const uint8_t* a[TStage<FA>::kAInstr];  // activation row of each instruction
-  const uint8_t* b[4];                    // weight row of each instruction
-  const uint8_t* as;                      // activation scale row (lanes < 32)
-  const uint8_t* bs;                      // weight scale row
-  uint32_t a_chunk[TStage<FA>::kAInstr];  // logical 16-byte chunk this lane fetches
-  uint32_t b_chunk[4];
+  using W = TWaves<FA, NW>;
+  const uint8_t* a[W::kAInstr];  // activation row of each instruction
+  const uint8_t* b[W::kBInstr];  // weight row of each instruction
+  const uint8_t* as;             // activation scale row (lanes < kASRows)
+  const uint8_t* bs;             // weight scale row (lanes < kBSRows)
+  uint32_t a_chunk[W::kAInstr];  // logical 16-byte chunk this lane fetches
+  uint32_t b_chunk[W::kBInstr];
 };
 
-template <int FA>
-__device__ __forceinline__ void tissue(uint8_t* st, const TLoad<FA>& L, int w, int lane, int k0) {
-  using S = TStage<FA>;
-#pragma unroll
-  for (int i = 0; i < S::kAInstr; ++i)
-    tdma16(L.a[i] + (size_t)k0 * S::kARow / 128 + 16 * L.a_chunk[i],
-           st + S::kA + 1024 * (S::kAInstr * w + i));
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    tdma16(L.b[i] + (size_t)k0 / 2 + 16 * L.b_chunk[i], st + S::kB + 1024 * (4 * w + i));
-  if (lane < 32) tdma4(L.as + k0 / 32, st + S::kAS + 128 * w);  // 32 rows per wave
-  tdma4(L.bs + k0 / 32, st + S::kBS + 256 * w);
+// Row of the tile and swizzled chunk for activation DMA instruction i of wave
+// w: one instruction fills 1 KiB of the row-major, chunk-swizzled layout.
+template <int FA, int NW>
+__device__ __forceinline__ void a_slot(int w, int i, int lane, int* row, uint32_t* chunk) {
+  const int ci = TWaves<FA, NW>::kAInstr * w + i;
+  if constexpr (FA == 0) {
+    *row = 8 * ci + lane / 8;
+    *chunk = (lane % 8) ^ ((*row >> 1) & 7);
+  } else {
+    *row = 16 * ci + lane / 4;
+    *chunk = (lane % 4) ^ ((*row >> 2) & 3);
+  }
 }
 
-// One K step for one wave: rows [64 wm, +64), weight rows given by brow0[cb].
-template <int FA>
-__device__ __forceinline__ void tcompute(const uint8_t* st, int wm, const int* brow, int nrb,
-                                         int g, int c16, v4f (*acc)[8]) {
+template <int NW>
+__device__ __forceinline__ void b_slot(int w, int i, int lane, int* row, uint32_t* chunk) {
+  const int ci = (16 / NW) * w + i;
+  *row = 16 * ci + lane / 4;
+  *chunk = (lane % 4) ^ ((*row >> 2) & 3);
+}
+
+template <int FA, int NW>
+__device__ __forceinline__ void tissue(uint8_t* st, const TLoad<FA, NW>& L, int w, int lane,
+                                       int k0) {
   using S = TStage<FA>;
-  v4u bop[8];
-  int sb[8];
+  using W = TWaves<FA, NW>;
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb) {
+  for (int i = 0; i < W::kAInstr; ++i)
+    tdma16(L.a[i] + (size_t)k0 * S::kARow / 128 + 16 * L.a_chunk[i],
+           st + S::kA + 1024 * (W::kAInstr * w + i));
+#pragma unroll
+  for (int i = 0; i < W::kBInstr; ++i)
+    tdma16(L.b[i] + (size_t)k0 / 2 + 16 * L.b_chunk[i], st + S::kB + 1024 * (W::kBInstr * w + i));
+  if (lane < W::kASRows) tdma4(L.as + k0 / 32, st + S::kAS + 4 * W::kASRows * w);
+  if (lane < W::kBSRows) tdma4(L.bs + k0 / 32, st + S::kBS + 4 * W::kBSRows * w);
+}
+
+template <int FA>
+__device__ __forceinline__ v8i read_a(const uint8_t* st, int r, int g) {
+  using S = TStage<FA>;
+  if constexpr (FA == 0) {
+    const int sw = (r >> 1) & 7;
+    const v4u lo = *reinterpret_cast<const v4u*>(st + S::kA + r * 128 + 16 * (g ^ sw));
+    const v4u hi = *reinterpret_cast<const v4u*>(st + S::kA + r * 128 + 16 * ((4 + g) ^ sw));
+    return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z,
+               (int)hi.w};
+  } else {
+    const v4u lo = *reinterpret_cast<const v4u*>(st + S::kA + r * 64 + 16 * (g ^ ((r >> 2) & 3)));
+    return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, 0, 0, 0, 0};
+  }
+}
+
+// One K step for one wave: rows [64 wm, +64) (the first nrb 16-row blocks
+// hold valid rows), weight rows brow[cb] + [0, 16). All fragments of the
+// step are read from LDS first, then the 4 x NCB products issue.
+template <int FA, int NCB, bool FULL>
+__device__ __forceinline__ void tcompute(const uint8_t* st, int wm, const int* brow, int nrb,
+                                         int g, int c16, v4f (*acc)[NCB]) {
+  using S = TStage<FA>;
+  v4u bop[NCB];
+  int sb[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
     const int r = brow[cb] + c16;
-    const int ch = g ^ ((r >> 2) & 3);
-    bop[cb] = *reinterpret_cast<const v4u*>(st + S::kB + r * 64 + 16 * ch);
+    bop[cb] = *reinterpret_cast<const v4u*>(st + S::kB + r * 64 + 16 * (g ^ ((r >> 2) & 3)));
     sb[cb] = (int)(*reinterpret_cast<const uint32_t*>(st + S::kBS + 4 * r) >> (8 * g));
+  }
+  v8i aop[4];
+  int sa[4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+    const int r = 64 * wm + 16 * rb + c16;
+    if (FULL || rb < nrb) {
+      aop[rb] = read_a<FA>(st, r, g);
+      sa[rb] = (int)(*reinterpret_cast<const uint32_t*>(st + S::kAS + 4 * r) >> (8 * g));
+    }
   }
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb) {
-    if (rb < nrb) {
-      const int r = 64 * wm + 16 * rb + c16;
-      v8i aop;
-      if constexpr (FA == 0) {
-        const int sw = (r >> 1) & 7;
-        const v4u lo = *reinterpret_cast<const v4u*>(st + S::kA + r * 128 + 16 * (g ^ sw));
-        const v4u hi = *reinterpret_cast<const v4u*>(st + S::kA + r * 128 + 16 * ((4 + g) ^ sw));
-        aop = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z,
-                  (int)hi.w};
-      } else {
-        const v4u lo = *reinterpret_cast<const v4u*>(st + S::kA + r * 64 + 16 * (g ^ ((r >> 2) & 3)));
-        aop = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, 0, 0, 0, 0};
-      }
-      const int sa = (int)(*reinterpret_cast<const uint32_t*>(st + S::kAS + 4 * r) >> (8 * g));
+    if (FULL || rb < nrb) {
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb) {
-        const v8i b = v8i{(int)bop[cb].x, (int)bop[cb].y, (int)bop[cb].z, (int)bop[cb].w, 0, 0, 0, 0};
-        acc[rb][cb] = mfma_scaled_16x16x128<FA, 0, 0>(aop, b, acc[rb][cb], sa, sb[cb]);
+      for (int cb = 0; cb < NCB; ++cb) {
+        const v8i b =
+            v8i{(int)bop[cb].x, (int)bop[cb].y, (int)bop[cb].z, (int)bop[cb].w, 0, 0, 0, 0};
+        acc[rb][cb] = mfma_scaled_16x16x128<FA, 0, 0>(aop[rb], b, acc[rb][cb], sa[rb], sb[cb]);
       }
     }
   }
@@ -139,31 +190,43 @@ __device__ __forceinline__ bool ttile(const TileArgs& t, int4* tile, int* nt) {
   return true;
 }
 
-// The K loop shared by both stages (two-stage DMA ring, barriers around the
-// consumption of each stage).
-template <int FA>
-__device__ __forceinline__ void tk_loop(uint8_t* lds, const TLoad<FA>& L, int nk, int w, int lane,
-                                        int wm, const int* brow, int nrb, int g, int c16,
-                                        v4f (*acc)[8]) {
+// The K loop shared by both stages: a ring of kStages LDS stages, kStages-1
+// of them in flight. Iteration k waits for its own stage-k loads, then one
+// barrier makes every wave's stage k visible and guarantees every wave has
+// finished reading stage k-1, whose slot is refilled with stage k+kStages-1.
+constexpr int kStages = 4;
+
+template <int FA, int NW>
+__device__ __forceinline__ void tk_loop(uint8_t* lds, const TLoad<FA, NW>& L, int nk, int w,
+                                        int lane, int wm, const int* brow, int nrb, int g, int c16,
+                                        v4f (*acc)[TWaves<FA, NW>::kNCB]) {
   using S = TStage<FA>;
-  tissue<FA>(lds, L, w, lane, 0);
+  using W = TWaves<FA, NW>;
+#pragma unroll
+  for (int s = 0; s < kStages - 1; ++s)
+    if (s < nk) tissue<FA, NW>(lds + s * S::kBytes, L, w, lane, s * 128);
   for (int k = 0; k < nk; ++k) {
-    uint8_t* cur = lds + (k & 1) * S::kBytes;
-    if (k + 1 < nk) {
-      tissue<FA>(lds + ((k + 1) & 1) * S::kBytes, L, w, lane, (k + 1) * 128);
-      twait_vmcnt<S::kLoads>();
-    } else {
-      twait_vmcnt<0>();
-    }
-    __syncthreads();
-    tcompute<FA>(cur, wm, brow, nrb, g, c16, acc);
-    __syncthreads();
+    if (k + kStages - 2 < nk) twait_vmcnt<(kStages - 2) * W::kLoads>();
+    else twait_vmcnt<0>();
+    // Workgroup barrier without a memory fence: __syncthreads() would make the
+    // compiler wait for every outstanding load (the younger stages too). The
+    // explicit vmcnt wait above already covers this wave's stage-k loads, and
+    // the asm memory clobber keeps LDS accesses on their side of the barrier.
+    asm volatile("s_barrier" ::: "memory");
+    if (k + kStages - 1 < nk)
+      tissue<FA, NW>(lds + ((k + kStages - 1) % kStages) * S::kBytes, L, w, lane,
+                     (k + kStages - 1) * 128);
+    if (nrb == 4)
+      tcompute<FA, W::kNCB, true>(lds + (k % kStages) * S::kBytes, wm, brow, nrb, g, c16, acc);
+    else
+      tcompute<FA, W::kNCB, false>(lds + (k % kStages) * S::kBytes, wm, brow, nrb, g, c16, acc);
   }
 }
 
-template <int FA>
-__global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
-  using S = TStage<FA>;
+template <int FA, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void s1_tiled_kernel(S1Args p) {
+  using W = TWaves<FA, NW>;
+  constexpr int NCB = W::kNCB, NBW = NCB / 2;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   int4 tile;
   int nt;
@@ -174,64 +237,56 @@ __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
   const int wm = w & 1, wn = w >> 1;
   const int hc0 = nt * (TBN / 2);  // first h column of the workgroup
 
-  TLoad<FA> L;
+  TLoad<FA, NW> L;
 #pragma unroll
-  for (int i = 0; i < S::kAInstr; ++i) {
-    int r, phys, sw;
-    if constexpr (FA == 0) {
-      r = 8 * (S::kAInstr * w + i) + lane / 8;
-      phys = lane % 8;
-      sw = (r >> 1) & 7;
-    } else {
-      r = 16 * (S::kAInstr * w + i) + lane / 4;
-      phys = lane % 4;
-      sw = (r >> 2) & 3;
-    }
-    const int rr = r < nrows ? r : 0;
-    const int tok = p.sorted[row0 + rr] / p.k_total;
+  for (int i = 0; i < W::kAInstr; ++i) {
+    int r;
+    a_slot<FA, NW>(w, i, lane, &r, &L.a_chunk[i]);
+    const int tok = p.sorted[row0 + (r < nrows ? r : 0)] / p.k_total;
     L.a[i] = p.xq + (size_t)tok * (p.H / 32) * ActBytes<FA>::kBlock;
-    L.a_chunk[i] = phys ^ sw;
   }
   const size_t ebase = (size_t)e * 2 * p.I;
+  auto wrow = [&](int r) {  // weight row of tile row r: 128 gate rows then 128 up rows
+    return ebase + (r < TBN / 2 ? hc0 + r : p.I + hc0 + (r - TBN / 2));
+  };
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = 16 * (4 * w + i) + lane / 4;  // weight row of the tile, 0..255
-    const size_t wr = ebase + (r < 128 ? hc0 + r : p.I + hc0 + (r - 128));
-    L.b[i] = p.w13 + wr * (p.H / 2);
-    L.b_chunk[i] = (lane % 4) ^ ((r >> 2) & 3);
+  for (int i = 0; i < W::kBInstr; ++i) {
+    int r;
+    b_slot<NW>(w, i, lane, &r, &L.b_chunk[i]);
+    L.b[i] = p.w13 + wrow(r) * (p.H / 2);
   }
   {
-    const int ra = 32 * w + (lane & 31);
+    const int ra = W::kASRows * w + lane % W::kASRows;
     const int tok = p.sorted[row0 + (ra < nrows ? ra : 0)] / p.k_total;
     L.as = p.xs + (size_t)tok * (p.H / 32);
-    const int rb = 64 * w + lane;
-    const size_t wr = ebase + (rb < 128 ? hc0 + rb : p.I + hc0 + (rb - 128));
-    L.bs = p.w13s + wr * (p.H / 32);
+    L.bs = p.w13s + wrow(W::kBSRows * w + lane % W::kBSRows) * (p.H / 32);
   }
-  // this wave's 8 weight column blocks: 4 gate then 4 up
-  int brow[8];
+  // this wave's column blocks: NBW gate blocks then the matching NBW up blocks
+  int brow[NCB];
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb) {
-    brow[cb] = 64 * wn + 16 * cb;
-    brow[4 + cb] = 128 + 64 * wn + 16 * cb;
+  for (int cb = 0; cb < NBW; ++cb) {
+    brow[cb] = 16 * (NBW * wn + cb);
+    brow[NBW + cb] = TBN / 2 + 16 * (NBW * wn + cb);
   }
   const int nrb = min(4, max(0, (nrows - 64 * wm + 15) / 16));
-  v4f acc[4][8];
+  v4f acc[4][NCB];
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb) acc[rb][cb] = v4f{0.f, 0.f, 0.f, 0.f};
-  tk_loop<FA>(lds, L, p.H / 128, w, lane, wm, brow, nrb, g, c16, acc);
+    for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = v4f{0.f, 0.f, 0.f, 0.f};
+  tk_loop<FA, NW>(lds, L, p.H / 128, w, lane, wm, brow, nrb, g, c16, acc);
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb) {
     const int off = 64 * wm + 16 * rb;
-    if (off < nrows) s1_epilogue<FA, 4>(acc[rb], p, row0 + off, nrows - off, hc0 + 64 * wn, g, c16);
+    if (off < nrows)
+      s1_epilogue<FA, NBW>(acc[rb], p, row0 + off, nrows - off, hc0 + 16 * NBW * wn, g, c16);
   }
 }
 
-template <int FA>
-__global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
-  using S = TStage<FA>;
+template <int FA, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void s2_tiled_kernel(S2Args p) {
+  using W = TWaves<FA, NW>;
+  constexpr int NCB = W::kNCB;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   int4 tile;
   int nt;
@@ -242,59 +297,54 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
   const int wm = w & 1, wn = w >> 1;
   const int nc0 = nt * TBN;
 
-  TLoad<FA> L;
+  TLoad<FA, NW> L;
 #pragma unroll
-  for (int i = 0; i < S::kAInstr; ++i) {
-    int r, phys, sw;
-    if constexpr (FA == 0) {
-      r = 8 * (S::kAInstr * w + i) + lane / 8;
-      phys = lane % 8;
-      sw = (r >> 1) & 7;
-    } else {
-      r = 16 * (S::kAInstr * w + i) + lane / 4;
-      phys = lane % 4;
-      sw = (r >> 2) & 3;
-    }
+  for (int i = 0; i < W::kAInstr; ++i) {
+    int r;
+    a_slot<FA, NW>(w, i, lane, &r, &L.a_chunk[i]);
     const size_t ar = (size_t)row0 + (r < nrows ? r : 0);
     L.a[i] = p.hq + ar * (p.I / 32) * ActBytes<FA>::kBlock;
-    L.a_chunk[i] = phys ^ sw;
   }
   const size_t ebase = (size_t)e * p.H + nc0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = 16 * (4 * w + i) + lane / 4;
+  for (int i = 0; i < W::kBInstr; ++i) {
+    int r;
+    b_slot<NW>(w, i, lane, &r, &L.b_chunk[i]);
     L.b[i] = p.w2 + (ebase + r) * (p.I / 2);
-    L.b_chunk[i] = (lane % 4) ^ ((r >> 2) & 3);
   }
   {
-    const int ra = 32 * w + (lane & 31);
+    const int ra = W::kASRows * w + lane % W::kASRows;
     L.as = p.hs + ((size_t)row0 + (ra < nrows ? ra : 0)) * (p.I / 32);
-    L.bs = p.w2s + (ebase + 64 * w + lane) * (p.I / 32);
+    L.bs = p.w2s + (ebase + W::kBSRows * w + lane % W::kBSRows) * (p.I / 32);
   }
-  int brow[8];
+  int brow[NCB];
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb) brow[cb] = 128 * wn + 16 * cb;
+  for (int cb = 0; cb < NCB; ++cb) brow[cb] = 16 * (NCB * wn + cb);
   const int nrb = min(4, max(0, (nrows - 64 * wm + 15) / 16));
-  v4f acc[4][8];
+  v4f acc[4][NCB];
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb) acc[rb][cb] = v4f{0.f, 0.f, 0.f, 0.f};
-  tk_loop<FA>(lds, L, p.I / 128, w, lane, wm, brow, nrb, g, c16, acc);
+    for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = v4f{0.f, 0.f, 0.f, 0.f};
+  tk_loop<FA, NW>(lds, L, p.I / 128, w, lane, wm, brow, nrb, g, c16, acc);
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb) {
     const int off = 64 * wm + 16 * rb;
-    if (off < nrows) s2_epilogue<8>(acc[rb], p, row0 + off, nrows - off, nc0 + 128 * wn, g, c16);
+    if (off < nrows)
+      s2_epilogue<NCB>(acc[rb], p, row0 + off, nrows - off, nc0 + 16 * NCB * wn, g, c16);
   }
 }
 
 int tiled_rows() { return TBM; }
 
 size_t tiled_lds_bytes(int fa) {
-  return 2 * (size_t)(fa == 0 ? TStage<0>::kBytes : TStage<4>::kBytes);
+  return kStages * (size_t)(fa == 0 ? TStage<0>::kBytes : TStage<4>::kBytes);
 }
 
 bool tiled_ok(int H, int I) { return I % (TBN / 2) == 0 && H % TBN == 0; }
+
+// Waves per workgroup of the tiled kernels (4 or 8).
+constexpr int kTiledWaves = TILED_WAVES;
 
 template <int FA>
 static void launch_t1(const S1Args& p, long mt, hipStream_t s) {
@@ -302,8 +352,8 @@ static void launch_t1(const S1Args& p, long mt, hipStream_t s) {
   q.t.n_ntiles = p.I / (TBN / 2);
   const long chunks = (mt + kChunkM - 1) / kChunkM;
   const long n = chunks * kChunkM * q.t.n_ntiles;
-  hipLaunchKernelGGL((s1_tiled_kernel<FA>), dim3((int)((n + 7) / 8 * 8)), dim3(256),
-                     2 * TStage<FA>::kBytes, s, q);
+  hipLaunchKernelGGL((s1_tiled_kernel<FA, kTiledWaves>), dim3((int)((n + 7) / 8 * 8)),
+                     dim3(64 * kTiledWaves), kStages * TStage<FA>::kBytes, s, q);
 }
 
 template <int FA>
@@ -312,8 +362,8 @@ static void launch_t2(const S2Args& p, long mt, hipStream_t s) {
   q.t.n_ntiles = p.H / TBN;
   const long chunks = (mt + kChunkM - 1) / kChunkM;
   const long n = chunks * kChunkM * q.t.n_ntiles;
-  hipLaunchKernelGGL((s2_tiled_kernel<FA>), dim3((int)((n + 7) / 8 * 8)), dim3(256),
-                     2 * TStage<FA>::kBytes, s, q);
+  hipLaunchKernelGGL((s2_tiled_kernel<FA, kTiledWaves>), dim3((int)((n + 7) / 8 * 8)),
+                     dim3(64 * kTiledWaves), kStages * TStage<FA>::kBytes, s, q);
 }
 
 void launch_s1_tiled(const S1Args& p, long mt, int fa, hipStream_t s) {
