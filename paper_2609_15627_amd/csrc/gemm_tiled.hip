@@ -1,98 +1,107 @@
-// a5 / a6: grouped FP4 expert GEMMs, LDS-tiled matrix-core geometry for many
-// rows per expert (prefill-sized batches).
+// a5 / a6: grouped FP4 expert GEMMs, LDS-tiled geometry for prefill-sized
+// batches (many rows per expert), on the 32x32x64 block-scaled matrix cores.
 //
-// Workgroup tile: 128 sorted rows of one expert x 256 weight rows (stage 1:
+// Workgroup tile: 256 sorted rows of one expert x 256 weight rows (stage 1:
 // 128 gate rows and the 128 matching up rows; stage 2: 256 output columns),
-// K in steps of 128. NW waves (4 or 8) in a 2 x NW/2 arrangement, each owning
-// 64 rows x 512/NW weight rows = 4 x 32/NW products of 16x16 per step
-// (16x16x128 block-scaled matrix-core instructions).
+// K in steps of 128 = two 64-element sub-steps. Four waves in a 2 x 2
+// arrangement, one per SIMD; each owns 128 rows x 128 weight rows = 4 x 4
+// products of 32x32 per sub-step, accumulated in fp32.
 //
-// Global -> LDS: direct loads (global_load_lds_dwordx4 writes lane l's 16
-// bytes at LDS offset 16*l of the instruction's destination), several stages in
-// flight (kStages-deep ring). Each lane picks the global address that lands in the right
-// swizzled LDS slot:
-//   activation rows (FP8, 128 bytes per row and step): 16-byte chunk c of row
-//     r is stored at chunk c ^ ((r >> 1) & 7);
-//   weight rows (FP4, 64 bytes per row and step) and FP4 activation rows:
-//     chunk c of row r at chunk c ^ ((r >> 2) & 3);
-// so the matrix-core operand reads (16 lanes = 16 consecutive rows, one
-// chunk each) hit 16 distinct bank groups. Scales: one dword per row and
-// step (the 4 block scales of the step), lane group g uses byte g.
+// Data movement, chosen from measurements on gfx950:
+//  - operands travel global -> LDS by DMA (global_load_lds, 16 bytes a lane,
+//    1 KiB of contiguous LDS per instruction) through a ring of three K-step
+//    stages; a load instruction costs about the same per distinct cache line
+//    it touches, so every instruction reads whole 64- or 128-byte row
+//    segments;
+//  - E8M0 scales move in 16-byte row pieces covering four K steps (a
+//    separate ring of two scale groups), not one word per row per step: a
+//    4-byte gather costs a cache line per lane;
+//  - LDS rows are chunk-swizzled (16-byte chunk c of row r stored at
+//    c ^ f(r)) so the operand reads of the 32x32x64 layout run at full LDS
+//    rate;
+//  - each wave reads the next sub-step's operands from LDS while the matrix
+//    cores work on the current one (two register sets), with one workgroup
+//    barrier per K step.
 //
-// Rows past the tile's end load a valid row instead (a product row depends
-// only on its own activation row, and those rows are never stored), and
-// 16-row blocks that are entirely past the end skip their products.
+// K order inside a step: the products only need A and B to agree on which
+// physical K elements a lane's bytes stand for. Sub-step s, lane half h takes
+// the physical 32-element block 2h + s of the step's four, so a lane's two
+// scale bytes of a step (blocks 2h and 2h + 1) are adjacent: one aligned
+// 16-bit LDS read per row and step, op_sel s picks the byte.
 //
-// Work order: chunks of kChunkM consecutive row tiles x all N tiles, N tile
-// fastest across chunks of row tiles: the workgroups that run together on an
-// XCD share activation rows (across N tiles) and weight tiles (across the row
-// tiles of one expert) through that XCD's L2.
+// Matrix-core operand layout (32x32x64, measured): lane l supplies row l % 32
+// of A and column l % 32 of B. An FP4 lane holds K elements [32 h, 32 h + 32)
+// of the 64 (h = l / 32), two per byte, low nibble first; an FP8 lane holds
+// K [16 h, 16 h + 16) in bytes 0-15 and K [32 + 16 h, +16) in bytes 16-31.
+// The lane's scale register carries the scale of 32-element K block h in the
+// byte selected by the instruction's op_sel. D: lane l, element i holds row
+// 8 (i / 4) + 4 h + i % 4, column l % 32.
 #include "gemm_common.h"
 #include "gemm_launch.h"
 
-#ifndef TILED_WAVES
-#define TILED_WAVES 8
-#endif
-
 namespace moe {
 
-constexpr int TBM = 128, TBN = 256;
-constexpr int kChunkM = 4;
-
+typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_ptr_t;
 
+constexpr int TBM = 256;       // sorted rows per tile
+constexpr int TBN = 256;       // weight rows per tile
+constexpr int kNStage = 3;     // K-step stages in the LDS ring
+constexpr int kSG = 4;         // K steps per scale group (16 scale bytes per row)
+constexpr int kTChunk = 2;     // row tiles per chunk of the launch order
+constexpr int kHStride = 136;  // fp32 row stride of the stage-1 epilogue buffer
+
 template <int FA>
-struct TStage {
-  static constexpr int kARow = FA == 0 ? 128 : 64;  // activation bytes per row per step
-  static constexpr int kA = 0;
-  static constexpr int kB = kA + TBM * kARow;        // 256 weight rows x 64 bytes
-  static constexpr int kAS = kB + TBN * 64;          // 128 activation scale dwords
-  static constexpr int kBS = kAS + TBM * 4;          // 256 weight scale dwords
-  static constexpr int kBytes = kBS + TBN * 4;
-  static constexpr int kAKB = TBM * kARow / 1024;    // activation KiB per step
+struct TL {
+  static constexpr int kARow = FA == 0 ? 128 : 64;  // activation bytes per row per K step
+  static constexpr int kB = TBM * kARow;             // weight rows follow the activation rows
+  static constexpr int kStage = kB + TBN * 64;
+  static constexpr int kS = kNStage * kStage;        // two scale buffers follow the stages
+  static constexpr int kSBuf = (TBM + TBN) * 16;
+  static constexpr int kLoop = kS + 2 * kSBuf;
+  static constexpr int kAInstr = TBM * kARow / 4096;  // DMA instructions per wave per step
+  static constexpr int kBInstr = TBN * 64 / 4096;
+  static constexpr int kStageLoads = kAInstr + kBInstr;
+  static constexpr int kScaleLoads = 2;
 };
 
-// Work split of the workgroup's NW waves.
-template <int FA, int NW>
-struct TWaves {
-  static constexpr int kAInstr = TStage<FA>::kAKB / NW;   // activation DMA instructions per wave
-  static constexpr int kBInstr = 16 / NW;                 // weight DMA instructions per wave
-  static constexpr int kASRows = TBM / NW;                // activation scale rows per wave
-  static constexpr int kBSRows = TBN / NW;                // weight scale rows per wave
-  static constexpr int kLoads = kAInstr + kBInstr + 2;    // DMA instructions per wave per step
-  static constexpr int kNCB = 32 / NW;                    // 16-column blocks per wave
-};
+template <int FA>
+constexpr int t_lds_s1() {
+  return TL<FA>::kLoop > TBM * kHStride * 4 ? TL<FA>::kLoop : TBM * kHStride * 4;
+}
 
 __device__ __forceinline__ void tdma16(const void* g, uint8_t* l) {
   __builtin_amdgcn_global_load_lds(g, (lds_ptr_t*)l, 16, 0, 0);
 }
-__device__ __forceinline__ void tdma4(const void* g, uint8_t* l) {
-  __builtin_amdgcn_global_load_lds(g, (lds_ptr_t*)l, 4, 0, 0);
-}
 
 template <int N>
-__device__ __forceinline__ void twait_vmcnt() {
+__device__ __forceinline__ void tvmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xf00);
 }
+__device__ __forceinline__ void tlgkm0() { __builtin_amdgcn_s_waitcnt(0xc07f); }
 
-// Per-lane source rows of the DMA instructions of one wave.
-template <int FA, int NW>
-struct TLoad {
-  using W = TWaves<FA, NW>;
-  const uint8_t* a[W::kAInstr];  // activation row of each instruction
-  const uint8_t* b[W::kBInstr];  // weight row of each instruction
-  const uint8_t* as;             // activation scale row (lanes < kASRows)
-  const uint8_t* bs;             // weight scale row (lanes < kBSRows)
-  uint32_t a_chunk[W::kAInstr];  // logical 16-byte chunk this lane fetches
-  uint32_t b_chunk[W::kBInstr];
+// Workgroup barrier without a memory fence: __syncthreads() would also wait
+// for every outstanding DMA (the younger stages too). The explicit waits
+// before it cover this wave's own loads; the asm memory clobber keeps LDS
+// accesses on their side of it.
+__device__ __forceinline__ void tbarrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// DMA sources of one wave at K step 0: workgroup-uniform bases plus 32-bit
+// per-lane byte offsets (so the loads use the scalar-base addressing form).
+template <int FA>
+struct TSrc {
+  const uint8_t *abase, *bbase, *asbase, *bsbase;
+  uint32_t a[TL<FA>::kAInstr];  // activation row + chunk of each instruction
+  uint32_t b[TL<FA>::kBInstr];  // weight row + chunk of each instruction
+  uint32_t as;                  // activation scale row 64 w + lane
+  uint32_t bs;                  // weight scale row 64 w + lane
 };
 
-// Row of the tile and swizzled chunk for activation DMA instruction i of wave
-// w: one instruction fills 1 KiB of the row-major, chunk-swizzled layout.
-template <int FA, int NW>
-__device__ __forceinline__ void a_slot(int w, int i, int lane, int* row, uint32_t* chunk) {
-  const int ci = TWaves<FA, NW>::kAInstr * w + i;
+// Tile row and logical 16-byte chunk fetched by lane `lane` of activation
+// DMA instruction ci (1 KiB of the chunk-swizzled activation rows).
+template <int FA>
+__device__ __forceinline__ void t_aslot(int ci, int lane, int* row, int* chunk) {
   if constexpr (FA == 0) {
     *row = 8 * ci + lane / 8;
     *chunk = (lane % 8) ^ ((*row >> 1) & 7);
@@ -101,269 +110,462 @@ __device__ __forceinline__ void a_slot(int w, int i, int lane, int* row, uint32_
     *chunk = (lane % 4) ^ ((*row >> 2) & 3);
   }
 }
-
-template <int NW>
-__device__ __forceinline__ void b_slot(int w, int i, int lane, int* row, uint32_t* chunk) {
-  const int ci = (16 / NW) * w + i;
+__device__ __forceinline__ void t_bslot(int ci, int lane, int* row, int* chunk) {
   *row = 16 * ci + lane / 4;
   *chunk = (lane % 4) ^ ((*row >> 2) & 3);
 }
 
-template <int FA, int NW>
-__device__ __forceinline__ void tissue(uint8_t* st, const TLoad<FA, NW>& L, int w, int lane,
-                                       int k0) {
-  using S = TStage<FA>;
-  using W = TWaves<FA, NW>;
+template <int FA>
+__device__ __forceinline__ void t_issue_stage(uint8_t* lds, const TSrc<FA>& S, int w, int k) {
+  using L = TL<FA>;
+  uint8_t* st = lds + (k % kNStage) * L::kStage;
+  const size_t ka = (size_t)k * L::kARow, kb = (size_t)k * 64;
 #pragma unroll
-  for (int i = 0; i < W::kAInstr; ++i)
-    tdma16(L.a[i] + (size_t)k0 * S::kARow / 128 + 16 * L.a_chunk[i],
-           st + S::kA + 1024 * (W::kAInstr * w + i));
+  for (int i = 0; i < L::kAInstr; ++i)
+    tdma16(S.abase + ka + S.a[i], st + 1024 * (L::kAInstr * w + i));
 #pragma unroll
-  for (int i = 0; i < W::kBInstr; ++i)
-    tdma16(L.b[i] + (size_t)k0 / 2 + 16 * L.b_chunk[i], st + S::kB + 1024 * (W::kBInstr * w + i));
-  if (lane < W::kASRows) tdma4(L.as + k0 / 32, st + S::kAS + 4 * W::kASRows * w);
-  if (lane < W::kBSRows) tdma4(L.bs + k0 / 32, st + S::kBS + 4 * W::kBSRows * w);
+  for (int i = 0; i < L::kBInstr; ++i)
+    tdma16(S.bbase + kb + S.b[i], st + L::kB + 1024 * (L::kBInstr * w + i));
 }
 
 template <int FA>
-__device__ __forceinline__ v8i read_a(const uint8_t* st, int r, int g) {
-  using S = TStage<FA>;
-  if constexpr (FA == 0) {
-    const int sw = (r >> 1) & 7;
-    const v4u lo = *reinterpret_cast<const v4u*>(st + S::kA + r * 128 + 16 * (g ^ sw));
-    const v4u hi = *reinterpret_cast<const v4u*>(st + S::kA + r * 128 + 16 * ((4 + g) ^ sw));
-    return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z,
-               (int)hi.w};
-  } else {
-    const v4u lo = *reinterpret_cast<const v4u*>(st + S::kA + r * 64 + 16 * (g ^ ((r >> 2) & 3)));
-    return v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, 0, 0, 0, 0};
-  }
+__device__ __forceinline__ void t_issue_scales(uint8_t* lds, const TSrc<FA>& S, int w, int q) {
+  using L = TL<FA>;
+  uint8_t* sb = lds + L::kS + (q & 1) * L::kSBuf;
+  tdma16(S.asbase + 16 * q + S.as, sb + 1024 * w);
+  tdma16(S.bsbase + 16 * q + S.bs, sb + TBM * 16 + 1024 * w);
 }
 
-// One K step for one wave: rows [64 wm, +64) (the first nrb 16-row blocks
-// hold valid rows), weight rows brow[cb] + [0, 16). All fragments of the
-// step are read from LDS first, then the 4 x NCB products issue.
-template <int FA, int NCB, bool FULL>
-__device__ __forceinline__ void tcompute(const uint8_t* st, int wm, const int* brow, int nrb,
-                                         int g, int c16, v4f (*acc)[NCB]) {
-  using S = TStage<FA>;
-  v4u bop[NCB];
-  int sb[NCB];
+// Per-lane LDS byte offsets of the operand reads (block 0; block b adds a
+// compile-time offset).
+struct TLane {
+  uint32_t a0[2], a1[2];  // activation piece(s) of sub-step s (FP8: bytes 0-15, 16-31)
+  uint32_t b[2];          // weight piece of sub-step s
+  uint32_t as, bs;        // this lane's scale byte pair of block 0 in a scale buffer
+};
+
+// Weight tile row of block nb relative to the wave's first weight row:
+// stage 1 pairs gate blocks (rows 64 wn + 32 nb) with the up blocks of the
+// same h columns (rows 128 + 64 wn + 32 nb); stage 2 takes 4 consecutive.
+template <int ST>
+__device__ __forceinline__ constexpr int t_nrow(int nb) {
+  return ST == 1 ? (nb < 2 ? 32 * nb : 128 + 32 * (nb - 2)) : 32 * nb;
+}
+
+struct TOps {
+  v8i a[4];
+  v8i b[4];
+};
+
+template <int FA, int ST, int S, bool FULL>
+__device__ __forceinline__ void t_read_ops(const uint8_t* st, const TLane& L, int nmb, TOps& o) {
+  using Lo = TL<FA>;
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
-    const int r = brow[cb] + c16;
-    bop[cb] = *reinterpret_cast<const v4u*>(st + S::kB + r * 64 + 16 * (g ^ ((r >> 2) & 3)));
-    sb[cb] = (int)(*reinterpret_cast<const uint32_t*>(st + S::kBS + 4 * r) >> (8 * g));
+  for (int nb = 0; nb < 4; ++nb) {
+    const v4u v = *reinterpret_cast<const v4u*>(st + L.b[S] + t_nrow<ST>(nb) * 64);
+    o.b[nb] = v8i{(int)v.x, (int)v.y, (int)v.z, (int)v.w, 0, 0, 0, 0};
   }
-  v8i aop[4];
-  int sa[4];
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    const int r = 64 * wm + 16 * rb + c16;
-    if (FULL || rb < nrb) {
-      aop[rb] = read_a<FA>(st, r, g);
-      sa[rb] = (int)(*reinterpret_cast<const uint32_t*>(st + S::kAS + 4 * r) >> (8 * g));
-    }
-  }
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    if (FULL || rb < nrb) {
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) {
-        const v8i b =
-            v8i{(int)bop[cb].x, (int)bop[cb].y, (int)bop[cb].z, (int)bop[cb].w, 0, 0, 0, 0};
-        acc[rb][cb] = mfma_scaled_16x16x128<FA, 0, 0>(aop[rb], b, acc[rb][cb], sa[rb], sb[cb]);
+  for (int mb = 0; mb < 4; ++mb) {
+    if (FULL || mb < nmb) {
+      const v4u lo = *reinterpret_cast<const v4u*>(st + L.a0[S] + mb * 32 * Lo::kARow);
+      if constexpr (FA == 0) {
+        const v4u hi = *reinterpret_cast<const v4u*>(st + L.a1[S] + mb * 32 * Lo::kARow);
+        o.a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w,
+                      (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+      } else {
+        o.a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, 0, 0, 0, 0};
       }
     }
   }
 }
 
-// Work item of this workgroup: row tile mt, N tile nt.
-__device__ __forceinline__ bool ttile(const TileArgs& t, int4* tile, int* nt) {
-  const int lin = xcd_remap(blockIdx.x, gridDim.x);
-  const int per = kChunkM * t.n_ntiles;
-  const int chunk = lin / per, r = lin % per;
-  *nt = r / kChunkM;
-  const int mt = chunk * kChunkM + r % kChunkM;
+// Scale byte pairs of step j of a group: byte s of the result is the scale
+// of sub-step s for this lane.
+template <int ST>
+__device__ __forceinline__ void t_read_scales(const uint8_t* sbuf, const TLane& L, int j,
+                                              uint32_t* sa, uint32_t* sb) {
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+    sa[mb] = *reinterpret_cast<const uint16_t*>(sbuf + L.as + mb * 32 * 16 + 4 * j);
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb)
+    sb[nb] = *reinterpret_cast<const uint16_t*>(sbuf + L.bs + t_nrow<ST>(nb) * 16 + 4 * j);
+}
+
+template <int FA, int OPS>
+__device__ __forceinline__ v16f t_mfma(const v8i& a, const v8i& b, const v16f& c, uint32_t sa,
+                                       uint32_t sb) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FA, 4, OPS, (int)sa, OPS,
+                                                         (int)sb);
+}
+
+// Products of sub-step S for blocks (mb, nb) with mb in [MB0, MB1).
+template <int FA, int S, int MB0, int MB1, bool FULL>
+__device__ __forceinline__ void t_mma(v16f (*acc)[4], const TOps& o, const uint32_t* sa,
+                                      const uint32_t* sb, int nmb) {
+#pragma unroll
+  for (int mb = MB0; mb < MB1; ++mb)
+    if (FULL || mb < nmb) {
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+        acc[mb][nb] = t_mfma<FA, S>(o.a[mb], o.b[nb], acc[mb][nb], sa[mb], sb[nb]);
+    }
+}
+
+// Interleave hint: alternate N single products with R LDS reads each.
+template <int N, int R>
+__device__ __forceinline__ void t_sched_mma_ds() {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+  }
+}
+
+// Interleave hint for the second half of a step: each product followed by
+// two LDS reads and one DMA instruction.
+__device__ __forceinline__ void t_sched_mma_vm_ds() {
+#pragma unroll
+  for (int i = 0; i < 12; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+  }
+}
+
+// One K step k = 4q + J (J compile-time). Stage k lives in ring slot k % 3,
+// scale group q in buffer q % 2. X holds the step's sub-step-0 operands and
+// sa/sb its scales on entry; on exit they hold those of step k + 1.
+//   1. sub-step-0 products on X while sub-step-1 operands are read into Y;
+//   2. one row of sub-step-1 products, then: this wave's loads of stage k + 1
+//      landed, workgroup barrier (every wave has left stage k, stage k + 1 is
+//      visible);
+//   3. DMA of stage k + 3 into slot k % 3 (at J == 0 also scale group q + 1,
+//      into the buffer group q - 1 used), reads of step k + 1's operands and
+//      scales, interleaved with the remaining sub-step-1 products.
+// LAST marks the final group (k = nk - 4 + J), where the ring drains.
+template <int FA, int ST, bool FULL, int J, bool LAST>
+__device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const TLane& L,
+                                       int k, int w, int nmb, v16f (*acc)[4], TOps& X, TOps& Y,
+                                       uint32_t* sa, uint32_t* sb) {
+  using Lo = TL<FA>;
+  constexpr bool kNext = !LAST || J < 3;  // step k + 1 exists
+  constexpr bool kIssue = !LAST || J == 0;  // stage k + 3 exists
+  constexpr bool kScales = !LAST && J == 0;  // scale group q + 1 exists
+  // Loads issued after stage k + 1's: stage k + 2 and, when J == 1 outside
+  // the last group, the scale group issued just before it.
+  constexpr int kWait = !LAST ? (J == 1 ? 2 : 1) : (J < 2 ? 1 : (J == 2 ? 0 : -1));
+  const uint8_t* st = lds + (k % kNStage) * Lo::kStage;
+
+  __builtin_amdgcn_sched_barrier(0);
+  t_read_ops<FA, ST, 1, FULL>(st, L, nmb, Y);
+  t_mma<FA, 0, 0, 4, FULL>(acc, X, sa, sb, nmb);
+  if constexpr (FULL) t_sched_mma_ds<12, 1>();
+  __builtin_amdgcn_sched_barrier(0);
+  tlgkm0();
+  t_mma<FA, 1, 0, 1, FULL>(acc, Y, sa, sb, nmb);
+  if constexpr (kWait == 2) tvmcnt<Lo::kStageLoads + Lo::kScaleLoads>();
+  else if constexpr (kWait == 1) tvmcnt<Lo::kStageLoads>();
+  else if constexpr (kWait == 0) tvmcnt<0>();
+  tbarrier();
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (kIssue) {
+    if constexpr (kScales) t_issue_scales<FA>(lds, src, w, k / kSG + 1);
+    t_issue_stage<FA>(lds, src, w, k + kNStage);
+  }
+  uint32_t ra[4], rb[4];
+  if constexpr (kNext) {
+    const int k1 = k + 1;
+    t_read_scales<ST>(lds + Lo::kS + ((k1 / kSG) & 1) * Lo::kSBuf, L, (J + 1) % kSG, ra, rb);
+    t_read_ops<FA, ST, 0, FULL>(lds + (k1 % kNStage) * Lo::kStage, L, nmb, X);
+  }
+  t_mma<FA, 1, 1, 4, FULL>(acc, Y, sa, sb, nmb);
+  if constexpr (FULL) t_sched_mma_vm_ds();
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (kNext) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      sa[i] = ra[i];
+      sb[i] = rb[i];
+    }
+  }
+}
+
+template <int FA, int ST, bool FULL, bool LAST>
+__device__ __forceinline__ void t_group(uint8_t* lds, const TSrc<FA>& src, const TLane& L, int q,
+                                        int w, int nmb, v16f (*acc)[4], TOps& X, TOps& Y,
+                                        uint32_t* sa, uint32_t* sb) {
+  t_step<FA, ST, FULL, 0, LAST>(lds, src, L, 4 * q + 0, w, nmb, acc, X, Y, sa, sb);
+  t_step<FA, ST, FULL, 1, LAST>(lds, src, L, 4 * q + 1, w, nmb, acc, X, Y, sa, sb);
+  t_step<FA, ST, FULL, 2, LAST>(lds, src, L, 4 * q + 2, w, nmb, acc, X, Y, sa, sb);
+  t_step<FA, ST, FULL, 3, LAST>(lds, src, L, 4 * q + 3, w, nmb, acc, X, Y, sa, sb);
+}
+
+// The K loop shared by both stages: nk = K / 128 steps, a multiple of 4.
+// Scale group 0 and stages 0-2 are in flight before the first step.
+template <int FA, int ST, bool FULL>
+__device__ __forceinline__ void t_kloop(uint8_t* lds, const TSrc<FA>& src, const TLane& L,
+                                        int nk, int w, int nmb, v16f (*acc)[4]) {
+  using Lo = TL<FA>;
+  t_issue_scales<FA>(lds, src, w, 0);
+#pragma unroll
+  for (int s = 0; s < kNStage; ++s) t_issue_stage<FA>(lds, src, w, s);
+  tvmcnt<2 * Lo::kStageLoads>();
+  tbarrier();
+
+  TOps X, Y;
+  uint32_t sa[4], sb[4];
+  t_read_ops<FA, ST, 0, FULL>(lds, L, nmb, X);
+  t_read_scales<ST>(lds + Lo::kS, L, 0, sa, sb);
+  const int nq = nk / kSG;
+  for (int q = 0; q < nq - 1; ++q) t_group<FA, ST, FULL, false>(lds, src, L, q, w, nmb, acc, X, Y, sa, sb);
+  t_group<FA, ST, FULL, true>(lds, src, L, nq - 1, w, nmb, acc, X, Y, sa, sb);
+}
+
+// Work item of this workgroup: row tile mt, N tile nt. Launch order is in
+// chunks of kTChunk row tiles x all N tiles (row tile fastest): the 32-odd
+// workgroups of a chunk run together and share both their activation rows
+// and their weight rows in L2. The dispatcher sends workgroup b to XCD b % 8;
+// XCD x takes chunks x, x + 8, x + 16, ... so every chunk stays on one XCD
+// and the chunks past the real tile count (the grid is sized for the upper
+// bound) are spread evenly over the XCDs.
+__device__ __forceinline__ bool t_tile(const TileArgs& t, int4* tile, int* nt) {
+  const int per = kTChunk * t.n_ntiles;
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int chunk = (j / per) * 8 + x, r = j % per;
+  *nt = r / kTChunk;
+  const int mt = chunk * kTChunk + r % kTChunk;
   if (mt >= *t.ntiles) return false;
   *tile = t.tiles[mt];
   return true;
 }
 
-// The K loop shared by both stages: a ring of kStages LDS stages, kStages-1
-// of them in flight. Iteration k waits for its own stage-k loads, then one
-// barrier makes every wave's stage k visible and guarantees every wave has
-// finished reading stage k-1, whose slot is refilled with stage k+kStages-1.
-constexpr int kStages = 4;
-
-template <int FA, int NW>
-__device__ __forceinline__ void tk_loop(uint8_t* lds, const TLoad<FA, NW>& L, int nk, int w,
-                                        int lane, int wm, const int* brow, int nrb, int g, int c16,
-                                        v4f (*acc)[TWaves<FA, NW>::kNCB]) {
-  using S = TStage<FA>;
-  using W = TWaves<FA, NW>;
+template <int FA, int ST>
+__device__ __forceinline__ TLane t_lane(int w, int lane) {
+  const int r = lane & 31, h = lane >> 5;
+  const int wm = w & 1, wn = w >> 1;
+  TLane L;
 #pragma unroll
-  for (int s = 0; s < kStages - 1; ++s)
-    if (s < nk) tissue<FA, NW>(lds + s * S::kBytes, L, w, lane, s * 128);
-  for (int k = 0; k < nk; ++k) {
-    if (k + kStages - 2 < nk) twait_vmcnt<(kStages - 2) * W::kLoads>();
-    else twait_vmcnt<0>();
-    // Workgroup barrier without a memory fence: __syncthreads() would make the
-    // compiler wait for every outstanding load (the younger stages too). The
-    // explicit vmcnt wait above already covers this wave's stage-k loads, and
-    // the asm memory clobber keeps LDS accesses on their side of the barrier.
-    asm volatile("s_barrier" ::: "memory");
-    if (k + kStages - 1 < nk)
-      tissue<FA, NW>(lds + ((k + kStages - 1) % kStages) * S::kBytes, L, w, lane,
-                     (k + kStages - 1) * 128);
-    if (nrb == 4)
-      tcompute<FA, W::kNCB, true>(lds + (k % kStages) * S::kBytes, wm, brow, nrb, g, c16, acc);
-    else
-      tcompute<FA, W::kNCB, false>(lds + (k % kStages) * S::kBytes, wm, brow, nrb, g, c16, acc);
+  for (int s = 0; s < 2; ++s) {
+    const int ar = 128 * wm + r;
+    if constexpr (FA == 0) {
+      // bytes 0-15: physical K [32 s + 16 h, +16); bytes 16-31: [64 + 32 s + 16 h, +16)
+      const int sw = (ar >> 1) & 7;
+      L.a0[s] = ar * 128 + 16 * ((2 * s + h) ^ sw);
+      L.a1[s] = ar * 128 + 16 * ((4 + 2 * s + h) ^ sw);
+    } else {
+      L.a0[s] = ar * 64 + 16 * ((2 * h + s) ^ ((ar >> 2) & 3));
+      L.a1[s] = L.a0[s];
+    }
+    const int br = (ST == 1 ? 64 : 128) * wn + r;
+    L.b[s] = TL<FA>::kB + br * 64 + 16 * ((2 * h + s) ^ ((br >> 2) & 3));
   }
+  L.as = (128 * wm + r) * 16 + 2 * h;
+  L.bs = TBM * 16 + ((ST == 1 ? 64 : 128) * wn + r) * 16 + 2 * h;
+  return L;
 }
 
-template <int FA, int NW>
-__global__ __launch_bounds__(64 * NW, 1) void s1_tiled_kernel(S1Args p) {
-  using W = TWaves<FA, NW>;
-  constexpr int NCB = W::kNCB, NBW = NCB / 2;
+// SwiGLU h = G * U * sigmoid(G) with the hardware exp2 and reciprocal (about
+// one ulp each; G itself carries the much larger accumulation error).
+__device__ __forceinline__ float swiglu_fast(float G, float U) {
+  const float e = __builtin_amdgcn_exp2f(-G * 1.4426950408889634f);
+  return G * U * __builtin_amdgcn_rcpf(1.0f + e);
+}
+
+template <int FA>
+__global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
+  using Lo = TL<FA>;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   int4 tile;
   int nt;
-  if (!ttile(p.t, &tile, &nt)) return;
+  if (!t_tile(p.t, &tile, &nt)) return;
   const int e = tile.x, row0 = tile.y, nrows = tile.z;
-  const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int g = lane >> 4, c16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const int wm = w & 1, wn = w >> 1;
-  const int hc0 = nt * (TBN / 2);  // first h column of the workgroup
+  const int hc0 = nt * (TBN / 2);  // first h column of the tile
+  const int xrow = (p.H / 32) * ActBytes<FA>::kBlock;
 
-  TLoad<FA, NW> L;
+  TSrc<FA> S;
+  S.abase = p.xq;
+  S.asbase = p.xs;
 #pragma unroll
-  for (int i = 0; i < W::kAInstr; ++i) {
-    int r;
-    a_slot<FA, NW>(w, i, lane, &r, &L.a_chunk[i]);
+  for (int i = 0; i < Lo::kAInstr; ++i) {
+    int r, c;
+    t_aslot<FA>(Lo::kAInstr * w + i, lane, &r, &c);
     const int tok = p.sorted[row0 + (r < nrows ? r : 0)] / p.k_total;
-    L.a[i] = p.xq + (size_t)tok * (p.H / 32) * ActBytes<FA>::kBlock;
+    S.a[i] = (uint32_t)(tok * xrow + 16 * c);
   }
-  const size_t ebase = (size_t)e * 2 * p.I;
-  auto wrow = [&](int r) {  // weight row of tile row r: 128 gate rows then 128 up rows
-    return ebase + (r < TBN / 2 ? hc0 + r : p.I + hc0 + (r - TBN / 2));
-  };
+  // weight row (within the expert) of tile row r: 128 gate rows, then the 128 up rows
+  auto wrow = [&](int r) { return r < TBN / 2 ? hc0 + r : p.I + hc0 + (r - TBN / 2); };
+  S.bbase = p.w13 + (size_t)e * 2 * p.I * (p.H / 2);
+  S.bsbase = p.w13s + (size_t)e * 2 * p.I * (p.H / 32);
 #pragma unroll
-  for (int i = 0; i < W::kBInstr; ++i) {
-    int r;
-    b_slot<NW>(w, i, lane, &r, &L.b_chunk[i]);
-    L.b[i] = p.w13 + wrow(r) * (p.H / 2);
+  for (int i = 0; i < Lo::kBInstr; ++i) {
+    int r, c;
+    t_bslot(Lo::kBInstr * w + i, lane, &r, &c);
+    S.b[i] = (uint32_t)(wrow(r) * (p.H / 2) + 16 * c);
   }
   {
-    const int ra = W::kASRows * w + lane % W::kASRows;
+    const int ra = 64 * w + lane;
     const int tok = p.sorted[row0 + (ra < nrows ? ra : 0)] / p.k_total;
-    L.as = p.xs + (size_t)tok * (p.H / 32);
-    L.bs = p.w13s + wrow(W::kBSRows * w + lane % W::kBSRows) * (p.H / 32);
+    S.as = (uint32_t)(tok * (p.H / 32));
+    S.bs = (uint32_t)(wrow(64 * w + lane) * (p.H / 32));
   }
-  // this wave's column blocks: NBW gate blocks then the matching NBW up blocks
-  int brow[NCB];
+  const TLane L = t_lane<FA, 1>(w, lane);
+  const int nmb = min(4, max(0, (nrows - 128 * wm + 31) / 32));
+  v16f acc[4][4];
 #pragma unroll
-  for (int cb = 0; cb < NBW; ++cb) {
-    brow[cb] = 16 * (NBW * wn + cb);
-    brow[NBW + cb] = TBN / 2 + 16 * (NBW * wn + cb);
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = v16f{};
+  if (nrows == TBM) t_kloop<FA, 1, true>(lds, S, L, p.H / 128, w, nmb, acc);
+  else t_kloop<FA, 1, false>(lds, S, L, p.H / 128, w, nmb, acc);
+
+  // Epilogue: h = SwiGLU(gate, up) through LDS as fp32 [256][kHStride], then
+  // per-32 quantisation with 8 lanes per (row, 32-column block).
+  tbarrier();
+  float* hb = reinterpret_cast<float*>(lds);
+  const int r = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+    if (mb < nmb) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int col = 64 * wn + 32 * q + r;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int row = 128 * wm + 32 * mb + 8 * (i / 4) + 4 * g + (i % 4);
+          const float G = acc[mb][q][i], U = acc[mb][2 + q][i];
+          hb[row * kHStride + col] = swiglu_fast(G, U);
+        }
+      }
+    }
   }
-  const int nrb = min(4, max(0, (nrows - 64 * wm + 15) / 16));
-  v4f acc[4][NCB];
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = v4f{0.f, 0.f, 0.f, 0.f};
-  tk_loop<FA, NW>(lds, L, p.H / 128, w, lane, wm, brow, nrb, g, c16, acc);
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    const int off = 64 * wm + 16 * rb;
-    if (off < nrows)
-      s1_epilogue<FA, NBW>(acc[rb], p, row0 + off, nrows - off, hc0 + 16 * NBW * wn, g, c16);
+  __syncthreads();
+  const int sub = threadIdx.x & 7;
+  const int ib = p.I / 32;
+  for (int it = 0; it < TBM * 4 / 32; ++it) {
+    const int task = (threadIdx.x >> 3) + 32 * it;
+    const int row = task >> 2, qb = task & 3;
+    if (row >= nrows) break;  // rows grow with it; the 8 lanes of a task leave together
+    const float4 v = *reinterpret_cast<const float4*>(hb + row * kHStride + 32 * qb + 4 * sub);
+    float m = fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w)));
+    m = fmaxf(m, __shfl_xor(m, 1, 8));
+    m = fmaxf(m, __shfl_xor(m, 2, 8));
+    m = fmaxf(m, __shfl_xor(m, 4, 8));
+    const int X = mx_scale_exp<FA>(m);
+    const size_t orow = (size_t)row0 + row;
+    const int col = hc0 + 32 * qb + 4 * sub;
+    if constexpr (FA == 0) {
+      *reinterpret_cast<uint32_t*>(p.hq + orow * p.I + col) =
+          e4m3_pack4(ldexpf(v.x, -X), ldexpf(v.y, -X), ldexpf(v.z, -X), ldexpf(v.w, -X));
+    } else {
+      const uint32_t c0 = mx_encode<FA>(ldexpf(v.x, -X)), c1 = mx_encode<FA>(ldexpf(v.y, -X));
+      const uint32_t c2 = mx_encode<FA>(ldexpf(v.z, -X)), c3 = mx_encode<FA>(ldexpf(v.w, -X));
+      *reinterpret_cast<uint16_t*>(p.hq + orow * (p.I / 2) + col / 2) =
+          (uint16_t)(c0 | (c1 << 4) | (c2 << 8) | (c3 << 12));
+    }
+    if (sub == 0) p.hs[orow * ib + hc0 / 32 + qb] = (uint8_t)(X + 127);
   }
 }
 
-template <int FA, int NW>
-__global__ __launch_bounds__(64 * NW, 1) void s2_tiled_kernel(S2Args p) {
-  using W = TWaves<FA, NW>;
-  constexpr int NCB = W::kNCB;
+template <int FA>
+__global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
+  using Lo = TL<FA>;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   int4 tile;
   int nt;
-  if (!ttile(p.t, &tile, &nt)) return;
+  if (!t_tile(p.t, &tile, &nt)) return;
   const int e = tile.x, row0 = tile.y, nrows = tile.z;
-  const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int g = lane >> 4, c16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const int wm = w & 1, wn = w >> 1;
-  const int nc0 = nt * TBN;
+  const int nc0 = nt * TBN;  // first output column of the tile
+  const int arow = (p.I / 32) * ActBytes<FA>::kBlock;
 
-  TLoad<FA, NW> L;
+  TSrc<FA> S;
+  S.abase = p.hq + (size_t)row0 * arow;
+  S.asbase = p.hs + (size_t)row0 * (p.I / 32);
 #pragma unroll
-  for (int i = 0; i < W::kAInstr; ++i) {
-    int r;
-    a_slot<FA, NW>(w, i, lane, &r, &L.a_chunk[i]);
-    const size_t ar = (size_t)row0 + (r < nrows ? r : 0);
-    L.a[i] = p.hq + ar * (p.I / 32) * ActBytes<FA>::kBlock;
+  for (int i = 0; i < Lo::kAInstr; ++i) {
+    int r, c;
+    t_aslot<FA>(Lo::kAInstr * w + i, lane, &r, &c);
+    S.a[i] = (uint32_t)((r < nrows ? r : 0) * arow + 16 * c);
   }
-  const size_t ebase = (size_t)e * p.H + nc0;
+  const size_t wr0 = (size_t)e * p.H + nc0;  // first weight row of the tile
+  S.bbase = p.w2 + wr0 * (p.I / 2);
+  S.bsbase = p.w2s + wr0 * (p.I / 32);
 #pragma unroll
-  for (int i = 0; i < W::kBInstr; ++i) {
-    int r;
-    b_slot<NW>(w, i, lane, &r, &L.b_chunk[i]);
-    L.b[i] = p.w2 + (ebase + r) * (p.I / 2);
+  for (int i = 0; i < Lo::kBInstr; ++i) {
+    int r, c;
+    t_bslot(Lo::kBInstr * w + i, lane, &r, &c);
+    S.b[i] = (uint32_t)(r * (p.I / 2) + 16 * c);
   }
   {
-    const int ra = W::kASRows * w + lane % W::kASRows;
-    L.as = p.hs + ((size_t)row0 + (ra < nrows ? ra : 0)) * (p.I / 32);
-    L.bs = p.w2s + (ebase + W::kBSRows * w + lane % W::kBSRows) * (p.I / 32);
+    const int ra = 64 * w + lane;
+    S.as = (uint32_t)((ra < nrows ? ra : 0) * (p.I / 32));
+    S.bs = (uint32_t)((64 * w + lane) * (p.I / 32));
   }
-  int brow[NCB];
+  const TLane L = t_lane<FA, 2>(w, lane);
+  const int nmb = min(4, max(0, (nrows - 128 * wm + 31) / 32));
+  v16f acc[4][4];
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) brow[cb] = 16 * (NCB * wn + cb);
-  const int nrb = min(4, max(0, (nrows - 64 * wm + 15) / 16));
-  v4f acc[4][NCB];
+  for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+    for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = v16f{};
+  if (nrows == TBM) t_kloop<FA, 2, true>(lds, S, L, p.I / 128, w, nmb, acc);
+  else t_kloop<FA, 2, false>(lds, S, L, p.I / 128, w, nmb, acc);
+
+  // Epilogue: fp32 partial rows to their unique assignment slots.
+  tbarrier();
+  int* sidx = reinterpret_cast<int*>(lds);
+  sidx[threadIdx.x] = (int)threadIdx.x < nrows ? p.sorted[row0 + threadIdx.x] : 0;
+  __syncthreads();
+  const int r = lane & 31, g = lane >> 5;
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = v4f{0.f, 0.f, 0.f, 0.f};
-  tk_loop<FA, NW>(lds, L, p.I / 128, w, lane, wm, brow, nrb, g, c16, acc);
+  for (int mb = 0; mb < 4; ++mb) {
+    if (mb < nmb) {
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    const int off = 64 * wm + 16 * rb;
-    if (off < nrows)
-      s2_epilogue<NCB>(acc[rb], p, row0 + off, nrows - off, nc0 + 16 * NCB * wn, g, c16);
+      for (int i = 0; i < 16; ++i) {
+        const int row = 128 * wm + 32 * mb + 8 * (i / 4) + 4 * g + (i % 4);
+        if (row < nrows) {
+          float* dst = p.partials + (size_t)sidx[row] * p.H + nc0 + 128 * wn + r;
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) dst[32 * nb] = acc[mb][nb][i];
+        }
+      }
+    }
   }
 }
 
 int tiled_rows() { return TBM; }
 
 size_t tiled_lds_bytes(int fa) {
-  return kStages * (size_t)(fa == 0 ? TStage<0>::kBytes : TStage<4>::kBytes);
+  return fa == 0 ? (size_t)t_lds_s1<0>() : (size_t)t_lds_s1<4>();
 }
 
-bool tiled_ok(int H, int I) { return I % (TBN / 2) == 0 && H % TBN == 0; }
-
-// Waves per workgroup of the tiled kernels (4 or 8).
-constexpr int kTiledWaves = TILED_WAVES;
+// Scale groups cover 512 K elements in both stages; N tiles are 128 h
+// columns (stage 1) and 256 output columns (stage 2).
+bool tiled_ok(int H, int I) { return H % (128 * kSG) == 0 && I % (128 * kSG) == 0; }
 
 template <int FA>
 static void launch_t1(const S1Args& p, long mt, hipStream_t s) {
   S1Args q = p;
   q.t.n_ntiles = p.I / (TBN / 2);
-  const long chunks = (mt + kChunkM - 1) / kChunkM;
-  const long n = chunks * kChunkM * q.t.n_ntiles;
-  hipLaunchKernelGGL((s1_tiled_kernel<FA, kTiledWaves>), dim3((int)((n + 7) / 8 * 8)),
-                     dim3(64 * kTiledWaves), kStages * TStage<FA>::kBytes, s, q);
+  const long chunks8 = ((mt + kTChunk - 1) / kTChunk + 7) / 8 * 8;
+  const long n = chunks8 * kTChunk * q.t.n_ntiles;
+  hipLaunchKernelGGL((s1_tiled_kernel<FA>), dim3((int)n), dim3(256),
+                     t_lds_s1<FA>(), s, q);
 }
 
 template <int FA>
 static void launch_t2(const S2Args& p, long mt, hipStream_t s) {
   S2Args q = p;
   q.t.n_ntiles = p.H / TBN;
-  const long chunks = (mt + kChunkM - 1) / kChunkM;
-  const long n = chunks * kChunkM * q.t.n_ntiles;
-  hipLaunchKernelGGL((s2_tiled_kernel<FA, kTiledWaves>), dim3((int)((n + 7) / 8 * 8)),
-                     dim3(64 * kTiledWaves), kStages * TStage<FA>::kBytes, s, q);
+  const long chunks8 = ((mt + kTChunk - 1) / kTChunk + 7) / 8 * 8;
+  const long n = chunks8 * kTChunk * q.t.n_ntiles;
+  hipLaunchKernelGGL((s2_tiled_kernel<FA>), dim3((int)n), dim3(256),
+                     TL<FA>::kLoop, s, q);
 }
 
 void launch_s1_tiled(const S1Args& p, long mt, int fa, hipStream_t s) {

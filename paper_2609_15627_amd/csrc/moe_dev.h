@@ -99,6 +99,16 @@ __device__ __forceinline__ uint32_t mx_encode(float q) {
   return (sign << (E::kEBits + E::kMBits)) | mag;
 }
 
+// Four values already divided by their block scale (|q| <= 448) to e4m3
+// codes, packed little-endian (value 0 in byte 0), by the hardware
+// conversion: OCP e4m3, round to nearest even, subnormals kept, the sign of
+// zero kept -- the same codes as mx_encode<0>.
+__device__ __forceinline__ uint32_t e4m3_pack4(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
+  return (uint32_t)w;
+}
+
 // ---------------------------------------------------------------------------
 // Matrix core: D(16x16) += A(16x128) . B(128x16) with one E8M0 scale per lane
 // per operand. Lane l supplies row (l % 16) of A and column (l % 16) of B for

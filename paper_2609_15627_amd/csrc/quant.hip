@@ -40,19 +40,22 @@ __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t* __restri
     amax = fmaxf(amax, fmaxf(fabsf(v[2 * i]), fabsf(v[2 * i + 1])));
   }
   const int X = mx_scale_exp<FMT>(amax);
-  uint32_t c[32];
-#pragma unroll
-  for (int i = 0; i < 32; ++i) c[i] = mx_encode<FMT>(ldexpf(v[i], -X));
   scales[b] = (uint8_t)(X + 127);
   if constexpr (FMT == 0) {
     uint4* dst = reinterpret_cast<uint4*>(codes + b * 32);
     uint32_t p[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      p[i] = c[4 * i] | (c[4 * i + 1] << 8) | (c[4 * i + 2] << 16) | (c[4 * i + 3] << 24);
+      p[i] = e4m3_pack4(ldexpf(v[4 * i], -X), ldexpf(v[4 * i + 1], -X), ldexpf(v[4 * i + 2], -X),
+                        ldexpf(v[4 * i + 3], -X));
     dst[0] = make_uint4(p[0], p[1], p[2], p[3]);
     dst[1] = make_uint4(p[4], p[5], p[6], p[7]);
-  } else if constexpr (FMT == 4) {
+    return;
+  }
+  uint32_t c[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) c[i] = mx_encode<FMT>(ldexpf(v[i], -X));
+  if constexpr (FMT == 4) {
     uint32_t p[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {

@@ -43,29 +43,47 @@ def check_hq_codes(layer, cfg, ref, fmt):
     which is relative to the largest products, not to h itself: an element
     can take a neighbouring grid value (when it sits near a rounding
     midpoint), and elements far below their block's maximum can move a few
-    subnormal steps. Bound: |v_gpu - v_oracle| <= one grid step at the larger
-    magnitude + 1e-4 of the format maximum (448, the block's scaled maximum
-    is at most that), in units of the block scale. Block scales must agree,
-    and differing codes must be rare (at most 1e-3 of the codes)."""
+    subnormal steps. Bound, on dequantised values: |v_gpu - v_oracle| <= one
+    grid step at the larger magnitude + 1e-4 of the block's scaled maximum
+    (448 times the larger block scale). Differing codes must be rare (at most
+    1e-3 of the codes).
+
+    Block scales follow the block maximum: when the oracle's maximum sits
+    within a relative 1e-4 of the boundary 448 * 2^X between two scales, the
+    GPU's fp32 maximum may fall on the other side, and its scale is one off.
+    Only such blocks may differ in scale, and only rarely (at most 1e-3 of
+    the blocks)."""
     if fmt != "e4m3":
         return 0
     hq = layer.workspace_view(2)[: cfg.A * cfg.I].cpu().numpy().reshape(cfg.A, cfg.I)
     hs = layer.workspace_view(3)[: cfg.A * cfg.I // 32].cpu().numpy().reshape(cfg.A, cfg.I // 32)
-    flips = total = 0
+    flips = total = moved = blocks = 0
     for r in ref["per_expert"].values():
         g, o = hq[r["rows"]].astype(np.int64), r["hq"].astype(np.int64)
-        assert np.array_equal(hs[r["rows"]], r["hs"]), "h block scales differ"
-        d = g != o
-        vg = mx.elem_decode(g, "e4m3")
-        vo = mx.elem_decode(o, "e4m3")
+        sg = hs[r["rows"]].astype(np.int64)
+        so = r["hs"].astype(np.int64)
+        ds = sg != so
+        if ds.any():
+            amax = np.abs(r["h"]).reshape(len(r["rows"]), -1, 32).max(2)
+            bound = 448.0 * np.ldexp(1.0, np.minimum(sg, so) - 127)
+            near = (np.abs(sg - so) == 1) & (np.abs(amax - bound) <= 1e-4 * bound)
+            assert (near | ~ds).all(), "h block scales differ away from a scale boundary"
+        moved += int(ds.sum())
+        blocks += ds.size
+        eg = np.repeat(sg, 32, axis=1) - 127
+        eo = np.repeat(so, 32, axis=1) - 127
+        vg = np.ldexp(mx.elem_decode(g, "e4m3"), eg)
+        vo = np.ldexp(mx.elem_decode(o, "e4m3"), eo)
         big = np.maximum(np.abs(vg), np.abs(vo))
         _, ex = np.frexp(big)
-        step = np.ldexp(1.0, np.maximum(ex - 1, -6) - 3)
-        far = d & (np.abs(vg - vo) > step + 1e-4 * 448)
-        assert not far.any(), f"h codes too far apart: {list(zip(g[far], o[far]))[:8]}"
-        flips += int(d.sum())
+        step = np.ldexp(1.0, np.maximum(ex - 1, np.maximum(eg, eo) - 6) - 3)
+        d = vg != vo
+        far = d & (np.abs(vg - vo) > step + 1e-4 * 448 * np.ldexp(1.0, np.maximum(eg, eo)))
+        assert not far.any(), f"h values too far apart: {list(zip(vg[far], vo[far]))[:8]}"
+        flips += int((g != o).sum())
         total += d.size
-    assert flips <= 1e-3 * max(total, 1), (flips, total)
+    assert moved <= 1e-3 * max(blocks, 1), (moved, blocks)
+    assert flips <= 1e-3 * max(total, 1) + 32 * moved, (flips, total)
     return flips
 
 
@@ -105,8 +123,9 @@ def small_case(T, H, I, E, k, S, seed, routing="normal"):
     (64, 1024, 256, 64, 8, 1),    # decode-like spread
     (3, 256, 128, 8, 8, 1),       # k = E
     (1, 128, 128, 1, 1, 0),       # smallest shape
-    (300, 512, 256, 4, 2, 1),     # tiled geometry: ~150-300 rows per expert, ragged tiles
-    (130, 256, 384, 2, 1, 0),     # tiled geometry: ~65 rows per expert, partial row blocks
+    (300, 1024, 512, 4, 2, 1),    # tiled geometry: ~150-300 rows per expert, ragged tiles
+    (600, 512, 1024, 2, 1, 0),    # tiled geometry: a full 256-row tile plus a ragged one
+    (130, 512, 512, 2, 1, 0),     # tiled geometry: ~65 rows per expert, partial row blocks
 ])
 def test_small_layers(m, shape, fmt):
     cfg, inp = small_case(*shape, seed=sum(shape))
@@ -125,7 +144,7 @@ def test_small_layers(m, shape, fmt):
 def test_tiled_geometry_skewed(m):
     """Zipf-skewed routing through the tiled geometry: hot experts with many
     row tiles, cold ones with a handful of rows or none."""
-    cfg = synth.LayerConfig("skew", 600, 512, 16, 4, 256, 0, "zipf", 5, zipf_empty=3)
+    cfg = synth.LayerConfig("skew", 600, 512, 16, 4, 512, 0, "zipf", 5, zipf_empty=3)
     inp = synth.make_inputs(cfg)
     log("tiled skewed")
     weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
@@ -217,7 +236,7 @@ def test_full_size_configs(m, name, ntok):
     log(f"full {name}: forward")
     layer, out = run_layer(m, cfg, x, weights, logits=inp.logits)
     variant = m.moe_last_variant()
-    assert variant == (m.VARIANT_STREAM if name == "decode" else m.VARIANT_TILED)
+    assert variant == (m.VARIANT_TILED if name in ("prefill8k", "skew32k") else m.VARIANT_STREAM)
     ids_ref, w_ref = omoe.route_topk(inp.logits, cfg.k, cfg.n_shared)
     assert np.array_equal(layer.ids.cpu().numpy(), ids_ref)
     perm_ref = omoe.permute(ids_ref, cfg.NE)
