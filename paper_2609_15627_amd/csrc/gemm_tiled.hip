@@ -49,7 +49,7 @@ constexpr int TBN = 256;       // weight rows per tile
 constexpr int kNStage = 3;     // K-step stages in the LDS ring
 constexpr int kSG = 4;         // K steps per scale group (16 scale bytes per row)
 constexpr int kTChunk = 2;     // row tiles per chunk of the launch order
-constexpr int kHStride = 136;  // fp32 row stride of the stage-1 epilogue buffer
+constexpr int kHStride = 132;  // fp32 row stride of the stage-1 epilogue buffer
 
 template <int FA>
 struct TL {
@@ -422,8 +422,13 @@ __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
   if (nrows == TBM) t_kloop<FA, 1, true>(lds, S, L, p.H / 128, w, nmb, acc);
   else t_kloop<FA, 1, false>(lds, S, L, p.H / 128, w, nmb, acc);
 
-  // Epilogue: h = SwiGLU(gate, up) through LDS as fp32 [256][kHStride], then
-  // per-32 quantisation with 8 lanes per (row, 32-column block).
+  // Epilogue, through LDS:
+  //  1. each lane writes its SwiGLU values h as fp32 rows [256][kHStride];
+  //  2. one thread per tile row quantises the row's four 32-column blocks in
+  //     registers (no cross-lane reductions) and writes the codes back over
+  //     the row's first bytes, its four scale bytes after them (a stride of
+  //     132 floats keeps these row-per-lane reads conflict-free);
+  //  3. all threads store the code rows with whole-row 16-byte pieces.
   tbarrier();
   float* hb = reinterpret_cast<float*>(lds);
   const int r = lane & 31, g = lane >> 5;
@@ -443,30 +448,79 @@ __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
     }
   }
   __syncthreads();
-  const int sub = threadIdx.x & 7;
-  const int ib = p.I / 32;
-  for (int it = 0; it < TBM * 4 / 32; ++it) {
-    const int task = (threadIdx.x >> 3) + 32 * it;
-    const int row = task >> 2, qb = task & 3;
-    if (row >= nrows) break;  // rows grow with it; the 8 lanes of a task leave together
-    const float4 v = *reinterpret_cast<const float4*>(hb + row * kHStride + 32 * qb + 4 * sub);
-    float m = fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w)));
-    m = fmaxf(m, __shfl_xor(m, 1, 8));
-    m = fmaxf(m, __shfl_xor(m, 2, 8));
-    m = fmaxf(m, __shfl_xor(m, 4, 8));
-    const int X = mx_scale_exp<FA>(m);
-    const size_t orow = (size_t)row0 + row;
-    const int col = hc0 + 32 * qb + 4 * sub;
-    if constexpr (FA == 0) {
-      *reinterpret_cast<uint32_t*>(p.hq + orow * p.I + col) =
-          e4m3_pack4(ldexpf(v.x, -X), ldexpf(v.y, -X), ldexpf(v.z, -X), ldexpf(v.w, -X));
-    } else {
-      const uint32_t c0 = mx_encode<FA>(ldexpf(v.x, -X)), c1 = mx_encode<FA>(ldexpf(v.y, -X));
-      const uint32_t c2 = mx_encode<FA>(ldexpf(v.z, -X)), c3 = mx_encode<FA>(ldexpf(v.w, -X));
-      *reinterpret_cast<uint16_t*>(p.hq + orow * (p.I / 2) + col / 2) =
-          (uint16_t)(c0 | (c1 << 4) | (c2 << 8) | (c3 << 12));
+  constexpr int kCB = FA == 0 ? 32 : 16;  // code bytes per 32-element block
+  {
+    const int row = threadIdx.x;
+    if (row < nrows) {
+      float* hr = hb + row * kHStride;
+      uint8_t* cr = reinterpret_cast<uint8_t*>(hr);
+      uint32_t sc = 0;
+#pragma unroll
+      for (int qb = 0; qb < 4; ++qb) {
+        float v[32];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float4 t = reinterpret_cast<const float4*>(hr + 32 * qb)[i];
+          v[4 * i] = t.x;
+          v[4 * i + 1] = t.y;
+          v[4 * i + 2] = t.z;
+          v[4 * i + 3] = t.w;
+        }
+        float m = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 32; ++i) m = fmaxf(m, fabsf(v[i]));
+        const int X = mx_scale_exp<FA>(m);
+        sc |= (uint32_t)(X + 127) << (8 * qb);
+        // block qb's codes land in bytes [kCB qb, +kCB) of the row, which
+        // only ever overlap values this thread has already read
+        if constexpr (FA == 0) {
+          uint4* dst = reinterpret_cast<uint4*>(cr + kCB * qb);
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            uint32_t wd[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int e = 16 * h + 4 * i;
+              wd[i] = e4m3_pack4(ldexpf(v[e], -X), ldexpf(v[e + 1], -X), ldexpf(v[e + 2], -X),
+                                 ldexpf(v[e + 3], -X));
+            }
+            dst[h] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+          }
+        } else {
+          uint32_t wd[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            uint32_t q = 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) q |= mx_encode<FA>(ldexpf(v[8 * i + j], -X)) << (4 * j);
+            wd[i] = q;
+          }
+          *reinterpret_cast<uint4*>(cr + kCB * qb) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+        }
+      }
+      *reinterpret_cast<uint32_t*>(cr + 4 * kCB) = sc;
     }
-    if (sub == 0) p.hs[orow * ib + hc0 / 32 + qb] = (uint8_t)(X + 127);
+  }
+  __syncthreads();
+  {
+    constexpr int kPieces = 4 * kCB / 16;  // 16-byte pieces of a row's codes
+    const size_t crow = (size_t)(p.I / 32) * kCB;  // code bytes per hq row
+#pragma unroll
+    for (int it = 0; it < TBM * kPieces / 256; ++it) {
+      const int task = threadIdx.x + 256 * it;
+      const int row = task / kPieces, pc = task % kPieces;
+      if (row < nrows) {
+        const uint8_t* cr = reinterpret_cast<const uint8_t*>(hb + row * kHStride);
+        const uint4 v = *reinterpret_cast<const uint4*>(cr + 16 * pc);
+        *reinterpret_cast<uint4*>(p.hq + ((size_t)row0 + row) * crow + (hc0 / 32) * kCB +
+                                  16 * pc) = v;
+      }
+    }
+    const int row = threadIdx.x;
+    if (row < nrows)
+      *reinterpret_cast<uint32_t*>(p.hs + ((size_t)row0 + row) * (p.I / 32) + hc0 / 32) =
+          *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(
+                                                 hb + row * kHStride) + 4 * kCB);
   }
 }
 
