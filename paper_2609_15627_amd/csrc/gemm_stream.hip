@@ -9,45 +9,65 @@
 // that expanding FP4 to INT8 doubled weight traffic and slowed the gate
 // kernel; Rejected or reverted directions).
 //
-// Operands go straight from global memory into registers, double-buffered
-// one step of 128*J K elements ahead (frag_load / stream_k). The weight
-// rows' E8M0 scales are the exception: each workgroup copies its rows' whole
-// scale rows into LDS once, up front (whole contiguous lines), and the K
-// loop reads them there. Gathering a few scale bytes per row per step from global
-// memory re-touched each 128-byte scale line over the whole K loop, long
-// enough for it to leave L2 between uses: measured on the decode layer, the
-// weight scales were fetched about six times over (0.65 GB of 2.58 GB).
+// Measured on the decode layer, and what it shaped:
+//  - under full HBM load a load takes tens of microseconds, so a
+//    workgroup's start (tile, sorted row, token, then scale rows: a chain of
+//    dependent loads) is as long as its streaming. The first step's code
+//    loads go out before the scale rows are staged, so those two latencies
+//    overlap. (Streaming two N tiles per workgroup to pay the chain once was
+//    slower: fewer, longer workgroups leave a ragged last wave.)
+//  - weight scales gathered a few bytes per row per step from global memory
+//    were fetched about six times over (each 128-byte line re-touched across
+//    the whole K loop, long enough to leave L2) and made each step wait for
+//    all outstanding loads. The workgroup copies its whole scale rows into
+//    LDS by DMA instead;
+//  - the compiler's wait insertion only counts exactly while every
+//    outstanding vector memory operation is an ordinary load it can see: an
+//    LDS DMA, an inline-asm LDS read, or stores in flight make it wait for
+//    everything. So one explicit full wait follows the prologue, and the
+//    step loop has no DMA, no stores and no branch around a load; each
+//    step's loads go out as one group ahead of the products that do not need
+//    them.
 //
 // Stage 1 (gate/up): each wave owns 16*NBW h columns; it streams those gate
 // rows and the matching up rows, so SwiGLU and the per-32 re-quantisation of
-// h (the quantisation block spans two 16-column tiles of the same wave) run in
-// registers. Stage 2 (down): each wave owns 16*NBW output columns of H and
+// h (the quantisation block spans two 16-column tiles of the same wave) run
+// in registers. Stage 2 (down): each wave owns 16*NBW output columns and
 // writes fp32 partials to the unique row a = sorted[r] of every assignment.
 #include "gemm_common.h"
 #include "gemm_launch.h"
 
 namespace moe {
 
-// Copy nbytes (a multiple of 16, 16-byte aligned at both ends) of
-// contiguous global memory to LDS: whole 1 KiB runs per wave instruction.
-// Plain loads and LDS stores rather than LDS DMA: with a DMA pending, the
-// compiler's wait insertion cannot tell the later global loads apart and
-// waits for all of them in the streaming loop.
-__device__ __forceinline__ void copy_rows_to_lds(uint8_t* dst, const uint8_t* src, int nbytes,
-                                                 int lane) {
-  for (int o = 16 * lane; o < nbytes; o += 1024)
-    *reinterpret_cast<v4u*>(dst + o) = *reinterpret_cast<const v4u*>(src + o);
+
+
+typedef __attribute__((address_space(3))) void lds_ptr_t;
+
+// nbytes (a multiple of 16) of contiguous global memory to LDS by 16-byte
+// DMA: 1 KiB of contiguous bytes per instruction.
+__device__ __forceinline__ void dma_rows16(uint8_t* dst, const uint8_t* src, int nbytes, int lane) {
+  for (int o = 0; o < nbytes; o += 1024)
+    if (o + 16 * lane < nbytes)
+      __builtin_amdgcn_global_load_lds(src + o + 16 * lane, (lds_ptr_t*)(dst + o), 16, 0, 0);
 }
 
-// Copy 16 gathered rows of kb bytes each (kb a multiple of 4) to LDS as a
-// dense [16][kb] block; rows(r) gives row r's address.
+// 16 gathered rows of kb bytes each (kb a multiple of 4) to LDS as a dense
+// [16][kb] block by 4-byte DMA; rows(r) gives row r's address.
 template <typename RowFn>
-__device__ __forceinline__ void copy_gather16_to_lds(uint8_t* dst, RowFn rows, int kb, int lane) {
-  const int words = kb / 4;  // 4-byte pieces per row
-  for (int q = lane; q < 16 * words; q += 64)
-    *reinterpret_cast<uint32_t*>(dst + 4 * q) =
-        *reinterpret_cast<const uint32_t*>(rows(q / words) + 4 * (q % words));
+__device__ __forceinline__ void dma_gather16(uint8_t* dst, RowFn rows, int kb, int lane) {
+  const int words = kb / 4;
+  for (int o = 0; o < 16 * words; o += 64) {
+    const int q = o + lane;
+    if (q < 16 * words)
+      __builtin_amdgcn_global_load_lds(rows(q / words) + 4 * (q % words),
+                                       (lds_ptr_t*)(dst + 4 * o), 4, 0, 0);
+  }
 }
+
+// Wait for every outstanding vector memory operation: after the prologue's
+// DMA the compiler can no longer count the loads exactly; one explicit wait
+// restores exact waits for the step loop.
+__device__ __forceinline__ void wait_all_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
 // Registers of one K step: activation pieces + scales, NB weight rows + scales.
 template <int FA, int J, int NB>
@@ -59,19 +79,8 @@ struct Frag {
   uint32_t bs[NB];
 };
 
-// gather_scales on a weight scale row held in LDS (byte offset `o`).
-template <int J>
-__device__ __forceinline__ uint32_t gather_scales_lds(uint32_t o, int g) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  const uint32_t* w = reinterpret_cast<const uint32_t*>(lds + o);
-  uint32_t r = 0;
-#pragma unroll
-  for (int j = 0; j < J; ++j) r |= ((w[j] >> (8 * g)) & 0xffu) << (8 * j);
-  return r;
-}
-
-// Loads of one K step starting at 32-element block `step` (a multiple of 4).
-// Product j of the step covers the 128 elements [step*32 + 128j, +128):
+// Code loads of one K step starting at 32-element block `step` (a multiple
+// of 4). Product j of the step covers the 128 elements [step*32 + 128j, +128):
 //  - a weight lane (column c16, lane group g) supplies block step + 4j + g,
 //    16 contiguous bytes; one load instruction reads 64 contiguous bytes of
 //    each of the wave's 16 rows;
@@ -81,31 +90,59 @@ __device__ __forceinline__ uint32_t gather_scales_lds(uint32_t o, int g) {
 //    of the product's 128 (an FP4 lane's 32 elements are K = 32g..), so it
 //    takes elements [16g, 16g+16) and [64+16g, 64+16g+16) of the product;
 //  - scales: the scale lane g is block g of the product (block 4j + g).
-//  - every lane loads unconditionally (rows past the tile's end read a valid
-//    row of the tile; their accumulator rows are never stored), so the loop
-//    holds no branches around loads and the waits count exact.
-template <int FA, int J, int NB, bool NT>
-__device__ __forceinline__ void frag_load(Frag<FA, J, NB>& f, const uint8_t* a_row,
-                                          uint32_t as_lds, const uint8_t* const* b_rows,
-                                          const uint32_t* bs_lds, int step, int g) {
-  {
+// Every lane loads (rows past the tile's end read a valid row of the tile;
+// their accumulator rows are never stored).
+template <int FA, int J, int NB>
+__device__ __forceinline__ void frag_codes(Frag<FA, J, NB>& f, const uint8_t* a_row,
+                                           const uint8_t* const* b_rows, size_t b_off, int step,
+                                           int g) {
+  // the step's loads go out as one group, ahead of the products that follow
+  // them in program order (the scheduler would otherwise interleave them with
+  // those products and leave each load only a few instructions of lead)
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int j = 0; j < J; ++j) {
-      if constexpr (FA == 0) {
-        const uint8_t* base = a_row + (size_t)step * 32 + 128 * j + 16 * g;
-        f.a[2 * j] = ld16<false>(base);
-        f.a[2 * j + 1] = ld16<false>(base + 64);
-      } else {
-        f.a[j] = ld16<false>(a_row + (size_t)(step + 4 * j + g) * 16);
-      }
+  for (int j = 0; j < J; ++j) {
+    if constexpr (FA == 0) {
+      const uint8_t* base = a_row + (size_t)step * 32 + 128 * j + 16 * g;
+      f.a[2 * j] = ld16<false>(base);
+      f.a[2 * j + 1] = ld16<false>(base + 64);
+    } else {
+      f.a[j] = ld16<false>(a_row + (size_t)(step + 4 * j + g) * 16);
     }
-    f.as = gather_scales_lds<J>(as_lds + step, g);
   }
+#pragma unroll
+  for (int n = 0; n < NB; ++n)
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+      f.b[n][j] = ld16<false>(b_rows[n] + b_off + (size_t)(step + 4 * j + g) * 16);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Byte g of each of the J scale words packed into bytes 0..J-1.
+template <int J>
+__device__ __forceinline__ uint32_t pick_scales(const uint32_t* w, int g) {
+  uint32_t r = 0;
+#pragma unroll
+  for (int j = 0; j < J; ++j) r |= ((w[j] >> (8 * g)) & 0xffu) << (8 * j);
+  return r;
+}
+
+// Scales of step `step` into f: activation row at LDS byte offset xa,
+// weight rows at wbuf + wo[n].
+template <int FA, int J, int NB>
+__device__ __forceinline__ void frag_scales(Frag<FA, J, NB>& f, uint32_t xa, uint32_t wbuf,
+                                            const uint32_t* wo, int step, int g) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  uint32_t w[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) w[j] = *reinterpret_cast<const uint32_t*>(lds + xa + step + 4 * j);
+  f.as = pick_scales<J>(w, g);
 #pragma unroll
   for (int n = 0; n < NB; ++n) {
 #pragma unroll
-    for (int j = 0; j < J; ++j) f.b[n][j] = ld16<NT>(b_rows[n] + (size_t)(step + 4 * j + g) * 16);
-    f.bs[n] = gather_scales_lds<J>(bs_lds[n] + step, g);
+    for (int j = 0; j < J; ++j)
+      w[j] = *reinterpret_cast<const uint32_t*>(lds + wbuf + wo[n] + step + 4 * j);
+    f.bs[n] = pick_scales<J>(w, g);
   }
 }
 
@@ -130,159 +167,161 @@ __device__ __forceinline__ void frag_mma(const Frag<FA, J, NB>& f, v4f* acc) {
   });
 }
 
-// Full K loop for one wave: NB weight rows (16 each, one per lane column),
-// one 16-row activation tile. K = nblk32 * 32 with nblk32 % 4 == 0. Steps of
-// 4J blocks are double-buffered: the steady-state loop always has the next
-// step's loads in flight while the current step's products run, with no
-// branch around a load, so each wait covers exactly the step it needs. A
-// tail of single 128-element steps follows.
-template <int FA, int J, int NB, bool NT>
-__device__ __forceinline__ void stream_k(const uint8_t* a_row, uint32_t as_lds,
-                                         const uint8_t* const* b_rows, const uint32_t* bs_lds,
-                                         int nblk32, int g, v4f* acc) {
-  const int kc_blocks = 4 * J;
-  const int nsteps = nblk32 / kc_blocks;
-  if (nsteps > 0) {
-    Frag<FA, J, NB> f0, f1;
-    frag_load<FA, J, NB, NT>(f0, a_row, as_lds, b_rows, bs_lds, 0, g);
-    int c = 0;
-    for (; c + 2 < nsteps; c += 2) {  // f0 holds step c; steps c + 1 and c + 2 exist
-      frag_load<FA, J, NB, NT>(f1, a_row, as_lds, b_rows, bs_lds, (c + 1) * kc_blocks, g);
+// The K loop of one wave: nst steps of 4J blocks, double-buffered in
+// registers. pro() runs right after the first step's code loads are issued
+// (it stages the scale rows, so both latencies overlap). With nst even
+// (EVEN) the loop runs step pairs with no branch around a load; odd nst
+// (K/32 not a multiple of 8) takes a plain loop.
+template <int FA, int J, int NB, bool EVEN, typename Pro>
+__device__ __forceinline__ void stream_k(const uint8_t* a_row, const uint8_t* const* b_rows,
+                                         int nst, uint32_t xa, uint32_t wb, const uint32_t* wo,
+                                         int g, v4f* acc, Pro pro) {
+  constexpr int kc = 4 * J;
+  Frag<FA, J, NB> f0, f1;
+  if constexpr (EVEN) {
+    frag_codes<FA, J, NB>(f0, a_row, b_rows, 0, 0, g);
+    pro();
+    wait_all_vmem();  // the first step and the scale rows are needed next anyway
+    for (int c = 0; c + 2 < nst; c += 2) {  // f0 holds step c
+      frag_codes<FA, J, NB>(f1, a_row, b_rows, 0, (c + 1) * kc, g);
+      frag_scales<FA, J, NB>(f0, xa, wb, wo, c * kc, g);
       frag_mma<FA, J, NB>(f0, acc);
-      frag_load<FA, J, NB, NT>(f0, a_row, as_lds, b_rows, bs_lds, (c + 2) * kc_blocks, g);
+      frag_codes<FA, J, NB>(f0, a_row, b_rows, 0, (c + 2) * kc, g);
+      frag_scales<FA, J, NB>(f1, xa, wb, wo, (c + 1) * kc, g);
       frag_mma<FA, J, NB>(f1, acc);
     }
-    if (c + 1 < nsteps) {
-      frag_load<FA, J, NB, NT>(f1, a_row, as_lds, b_rows, bs_lds, (c + 1) * kc_blocks, g);
-      frag_mma<FA, J, NB>(f0, acc);
-      frag_mma<FA, J, NB>(f1, acc);
-    } else {
+    frag_codes<FA, J, NB>(f1, a_row, b_rows, 0, (nst - 1) * kc, g);
+    frag_scales<FA, J, NB>(f0, xa, wb, wo, (nst - 2) * kc, g);
+    frag_mma<FA, J, NB>(f0, acc);
+    frag_scales<FA, J, NB>(f1, xa, wb, wo, (nst - 1) * kc, g);
+    frag_mma<FA, J, NB>(f1, acc);
+  } else {
+    pro();
+    wait_all_vmem();
+    for (int c = 0; c < nst; ++c) {
+      frag_codes<FA, J, NB>(f0, a_row, b_rows, 0, c * kc, g);
+      frag_scales<FA, J, NB>(f0, xa, wb, wo, c * kc, g);
       frag_mma<FA, J, NB>(f0, acc);
     }
-  }
-  for (int blk = nsteps * kc_blocks; blk < nblk32; blk += 4) {
-    Frag<FA, 1, NB> f;
-    frag_load<FA, 1, NB, NT>(f, a_row, as_lds, b_rows, bs_lds, blk, g);
-    frag_mma<FA, 1, NB>(f, acc);
   }
 }
 
-template <int FA, int J, int NBW, bool NT, int WPB>
-__global__ __launch_bounds__(64 * WPB) void s1_stream_kernel(S1Args p) {
+template <int FA, int J, int NBW, bool EVEN>
+__global__ __launch_bounds__(64) void s1_stream_kernel(S1Args p) {
   static_assert(NBW % 2 == 0, "a quantisation block spans two 16-column tiles");
+  constexpr int NB = 2 * NBW;
   constexpr int kAB = ActBytes<FA>::kBlock;
   int4 tile;
   int nt;
   if (!tile_of_block(p.t, &tile, &nt)) return;
   const int e = tile.x, row0 = tile.y, nrows = tile.z;
-  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
-  const int g = lane >> 4, c16 = lane & 15;
-  const int hc0 = nt * (WPB * NBW * 16) + w * (NBW * 16);  // first h column of this wave
+  const int lane = threadIdx.x, g = lane >> 4, c16 = lane & 15;
+  const int kb = p.H / 32;
+  const int hc0 = nt * (NBW * 16);  // first h column of the wave
+  const size_t ebase = (size_t)e * 2 * p.I;
+
+  // LDS: the tile's 16 activation scale rows, then the wave's 16 NBW gate
+  // and 16 NBW up weight scale rows.
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int half = NBW * 16 * kb;  // bytes of the gate (or up) scale rows
 
   const int tok = p.sorted[row0 + (c16 < nrows ? c16 : 0)] / p.k_total;
   const uint8_t* a_row = p.xq + (size_t)tok * (p.H / 32) * kAB;
-
-  // Scale rows to LDS first: the tile's 16 activation rows, then the wave's
-  // 16 NBW gate rows and the matching up rows; the K loop streams the codes.
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  const int kb = p.H / 32;
-  const size_t ebase = (size_t)e * 2 * p.I;
-  uint8_t* my = lds + w * ((2 * NBW + 1) * 16 * kb);
-  copy_gather16_to_lds(
-      my,
-      [&](int r) {
-        const int t = p.sorted[row0 + (r < nrows ? r : 0)] / p.k_total;
-        return p.xs + (size_t)t * kb;
-      },
-      kb, lane);
-  uint8_t* myb = my + 16 * kb;
-  copy_rows_to_lds(myb, p.w13s + (ebase + hc0) * kb, NBW * 16 * kb, lane);
-  copy_rows_to_lds(myb + NBW * 16 * kb, p.w13s + (ebase + p.I + hc0) * kb, NBW * 16 * kb, lane);
-  const uint32_t as_lds = (uint32_t)(my - lds) + c16 * kb;
-  const uint8_t* b_rows[2 * NBW];
-  uint32_t bs_lds[2 * NBW];
+  const uint8_t* b_rows[NB];
+  uint32_t wo[NB];
 #pragma unroll
   for (int b = 0; b < NBW; ++b) {
     const size_t gr = ebase + hc0 + 16 * b + c16;  // gate row
-    const size_t ur = gr + p.I;                    // up row
     b_rows[b] = p.w13 + gr * (p.H / 2);
-    b_rows[NBW + b] = p.w13 + ur * (p.H / 2);
-    bs_lds[b] = (uint32_t)(myb - lds) + (16 * b + c16) * kb;
-    bs_lds[NBW + b] = (uint32_t)(myb - lds) + (NBW * 16 + 16 * b + c16) * kb;
+    b_rows[NBW + b] = p.w13 + (gr + p.I) * (p.H / 2);
+    wo[b] = (16 * b + c16) * kb;
+    wo[NBW + b] = (NBW * 16 + 16 * b + c16) * kb;
   }
-  v4f acc[2 * NBW];
+  v4f acc[NB];
 #pragma unroll
-  for (int n = 0; n < 2 * NBW; ++n) acc[n] = v4f{0.f, 0.f, 0.f, 0.f};
-  stream_k<FA, J, 2 * NBW, NT>(a_row, as_lds, b_rows, bs_lds, p.H / 32, g, acc);
-
+  for (int n = 0; n < NB; ++n) acc[n] = v4f{0.f, 0.f, 0.f, 0.f};
+  stream_k<FA, J, NB, EVEN>(a_row, b_rows, kb / (4 * J), c16 * kb, 16 * kb, wo, g, acc, [&]() {
+    dma_gather16(
+        lds,
+        [&](int r) {
+          const int t = p.sorted[row0 + (r < nrows ? r : 0)] / p.k_total;
+          return p.xs + (size_t)t * kb;
+        },
+        kb, lane);
+    dma_rows16(lds + 16 * kb, p.w13s + (ebase + hc0) * kb, half, lane);
+    dma_rows16(lds + 16 * kb + half, p.w13s + (ebase + p.I + hc0) * kb, half, lane);
+  });
   s1_epilogue<FA, NBW>(acc, p, row0, nrows, hc0, g, c16);
 }
 
-template <int FA, int J, int NBW, bool NT, int WPB>
-__global__ __launch_bounds__(64 * WPB) void s2_stream_kernel(S2Args p) {
+template <int FA, int J, int NBW, bool EVEN>
+__global__ __launch_bounds__(64) void s2_stream_kernel(S2Args p) {
+  constexpr int NB = NBW;
   constexpr int kAB = ActBytes<FA>::kBlock;
   int4 tile;
   int nt;
   if (!tile_of_block(p.t, &tile, &nt)) return;
   const int e = tile.x, row0 = tile.y, nrows = tile.z;
-  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
-  const int g = lane >> 4, c16 = lane & 15;
-  const int nc0 = nt * (WPB * NBW * 16) + w * (NBW * 16);  // first output column of this wave
+  const int lane = threadIdx.x, g = lane >> 4, c16 = lane & 15;
+  const int kb = p.I / 32;
+  const int nc0 = nt * (NBW * 16);  // first output column of the wave
+  const size_t rbase = (size_t)e * p.H + nc0;
 
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const size_t ar = (size_t)row0 + (c16 < nrows ? c16 : 0);
   const uint8_t* a_row = p.hq + ar * (p.I / 32) * kAB;
-
-  // Scale rows to LDS first: the tile's 16 activation rows, then the wave's
-  // 16 NBW consecutive weight rows.
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  const int kb = p.I / 32;
-  uint8_t* my = lds + w * ((NBW + 1) * 16 * kb);
-  copy_gather16_to_lds(
-      my, [&](int r) { return p.hs + ((size_t)row0 + (r < nrows ? r : 0)) * kb; }, kb, lane);
-  uint8_t* myb = my + 16 * kb;
-  copy_rows_to_lds(myb, p.w2s + ((size_t)e * p.H + nc0) * kb, NBW * 16 * kb, lane);
-  const uint32_t as_lds = (uint32_t)(my - lds) + c16 * kb;
-  const uint8_t* b_rows[NBW];
-  uint32_t bs_lds[NBW];
+  const uint8_t* b_rows[NB];
+  uint32_t wo[NB];
 #pragma unroll
-  for (int b = 0; b < NBW; ++b) {
-    const size_t rr = (size_t)e * p.H + nc0 + 16 * b + c16;
-    b_rows[b] = p.w2 + rr * (p.I / 2);
-    bs_lds[b] = (uint32_t)(myb - lds) + (16 * b + c16) * kb;
+  for (int b = 0; b < NB; ++b) {
+    b_rows[b] = p.w2 + (rbase + 16 * b + c16) * (p.I / 2);
+    wo[b] = (16 * b + c16) * kb;
   }
-  v4f acc[NBW];
+  v4f acc[NB];
 #pragma unroll
-  for (int n = 0; n < NBW; ++n) acc[n] = v4f{0.f, 0.f, 0.f, 0.f};
-  stream_k<FA, J, NBW, NT>(a_row, as_lds, b_rows, bs_lds, p.I / 32, g, acc);
-
+  for (int n = 0; n < NB; ++n) acc[n] = v4f{0.f, 0.f, 0.f, 0.f};
+  stream_k<FA, J, NB, EVEN>(a_row, b_rows, kb / (4 * J), c16 * kb, 16 * kb, wo, g, acc, [&]() {
+    dma_gather16(
+        lds, [&](int r) { return p.hs + ((size_t)row0 + (r < nrows ? r : 0)) * kb; }, kb, lane);
+    dma_rows16(lds + 16 * kb, p.w2s + rbase * kb, NB * 16 * kb, lane);
+  });
   s2_epilogue<NBW>(acc, p, row0, nrows, nc0, g, c16);
+}
+
+// Kernel instance: steps of 8 blocks (kb = K/32 a multiple of 16), else of
+// 4 with an even count (kb % 8 == 0), else a plain loop.
+template <typename K2, typename K1, typename K0, typename P>
+static void launch_stream(int kb, K2 k2, K1 k1, K0 k0, long mt, int ntl, const P& p0,
+                          hipStream_t s, size_t lds) {
+  P q = p0;
+  q.t.n_ntiles = ntl;
+  q.t.ngroup = n_group_of(ntl);
+  const long n = mt * ntl;
+  const dim3 grid((int)((n + 7) / 8 * 8));
+  if (kb % 16 == 0) hipLaunchKernelGGL(k2, grid, dim3(64), lds, s, q);
+  else if (kb % 8 == 0) hipLaunchKernelGGL(k1, grid, dim3(64), lds, s, q);
+  else hipLaunchKernelGGL(k0, grid, dim3(64), lds, s, q);
 }
 
 template <int FA, int NBW1>
 static void launch_s1(const S1Args& p, long mt, hipStream_t s) {
-  S1Args q = p;
-  q.t.n_ntiles = p.I / (NBW1 * 16);
-  q.t.ngroup = n_group_of(q.t.n_ntiles);
-  const long n = mt * q.t.n_ntiles;
-  hipLaunchKernelGGL((s1_stream_kernel<FA, 2, NBW1, false, 1>), dim3((int)((n + 7) / 8 * 8)),
-                     dim3(64), (2 * NBW1 + 1) * 16 * (p.H / 32), s, q);
+  const int kb = p.H / 32;
+  launch_stream(kb, s1_stream_kernel<FA, 2, NBW1, true>, s1_stream_kernel<FA, 1, NBW1, true>,
+                s1_stream_kernel<FA, 1, NBW1, false>, mt, p.I / (NBW1 * 16), p, s,
+                (size_t)(1 + 2 * NBW1) * 16 * kb);
 }
 
 template <int FA, int NBW2>
 static void launch_s2(const S2Args& p, long mt, hipStream_t s) {
-  S2Args q = p;
-  q.t.n_ntiles = p.H / (NBW2 * 16);
-  q.t.ngroup = n_group_of(q.t.n_ntiles);
-  const long n = mt * q.t.n_ntiles;
-  hipLaunchKernelGGL((s2_stream_kernel<FA, 2, NBW2, false, 1>), dim3((int)((n + 7) / 8 * 8)),
-                     dim3(64), (NBW2 + 1) * 16 * (p.I / 32), s, q);
+  const int kb = p.I / 32;
+  launch_stream(kb, s2_stream_kernel<FA, 2, NBW2, true>, s2_stream_kernel<FA, 1, NBW2, true>,
+                s2_stream_kernel<FA, 1, NBW2, false>, mt, p.H / (NBW2 * 16), p, s,
+                (size_t)(1 + NBW2) * 16 * kb);
 }
 
-// One wave per workgroup, steps of 256 K elements, 32 h columns per wave in
-// stage 1 and 64 output columns per wave in stage 2. Measured alternatives
-// (non-temporal weight loads, 2 or 4 waves per workgroup, 128- or 512-element
-// steps, deeper register rings, direct-to-LDS rings, persistent waves) were
-// slower on the decode layer.
+// One wave per workgroup, steps of 256 K elements (128 when K/32 is not a
+// multiple of 16), 32 h columns per wave in stage 1 and 64 output columns
+// per wave in stage 2.
 void launch_s1_stream(const S1Args& p, long mt, int fa, hipStream_t s) {
   if (fa == 0) launch_s1<0, 2>(p, mt, s);
   else launch_s1<4, 2>(p, mt, s);
@@ -299,23 +338,17 @@ void launch_s2_stream(const S2Args& p, long mt, int fa, hipStream_t s) {
 template <int FA>
 __global__ void probe_kernel(const uint8_t* a, const uint8_t* sa, const uint8_t* b,
                              const uint8_t* sb, float* d) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  const int lane = threadIdx.x, g = lane >> 4, c16 = lane & 15;
-  // scales live in LDS as in the GEMM: row c16's four bytes of A at 4 c16,
-  // of B at 64 + 4 c16
-  if (g == 0) {
-    *reinterpret_cast<uint32_t*>(lds + 4 * c16) = *reinterpret_cast<const uint32_t*>(sa + 4 * c16);
-    *reinterpret_cast<uint32_t*>(lds + 64 + 4 * c16) =
-        *reinterpret_cast<const uint32_t*>(sb + 4 * c16);
-  }
-  __syncthreads();
   constexpr int kAB = ActBytes<FA>::kBlock;
+  const int lane = threadIdx.x, g = lane >> 4, c16 = lane & 15;
   const uint8_t* ar = a + (size_t)c16 * 4 * kAB;
   const uint8_t* br = b + (size_t)c16 * 64;
-  const uint32_t bso = 64 + 4 * c16;
   v4f acc = v4f{0.f, 0.f, 0.f, 0.f};
   Frag<FA, 1, 1> f;
-  frag_load<FA, 1, 1, false>(f, ar, 4 * c16, &br, &bso, 0, g);
+  frag_codes<FA, 1, 1>(f, ar, &br, 0, 0, g);
+  const uint32_t wa = *reinterpret_cast<const uint32_t*>(sa + 4 * c16);
+  const uint32_t wb = *reinterpret_cast<const uint32_t*>(sb + 4 * c16);
+  f.as = pick_scales<1>(&wa, g);
+  f.bs[0] = pick_scales<1>(&wb, g);
   frag_mma<FA, 1, 1>(f, &acc);
 #pragma unroll
   for (int i = 0; i < 4; ++i) d[(4 * g + i) * 16 + c16] = acc[i];
@@ -324,9 +357,9 @@ __global__ void probe_kernel(const uint8_t* a, const uint8_t* sa, const uint8_t*
 hipError_t launch_probe(const uint8_t* a, const uint8_t* sa, int fmt, const uint8_t* b,
                         const uint8_t* sb, float* d, hipStream_t s) {
   if (fmt == 0)
-    hipLaunchKernelGGL(probe_kernel<0>, dim3(1), dim3(64), 128, s, a, sa, b, sb, d);
+    hipLaunchKernelGGL(probe_kernel<0>, dim3(1), dim3(64), 0, s, a, sa, b, sb, d);
   else if (fmt == 4)
-    hipLaunchKernelGGL(probe_kernel<4>, dim3(1), dim3(64), 128, s, a, sa, b, sb, d);
+    hipLaunchKernelGGL(probe_kernel<4>, dim3(1), dim3(64), 0, s, a, sa, b, sb, d);
   else
     return hipErrorNotSupported;
   return hipGetLastError();
