@@ -10,26 +10,54 @@ namespace moe {
 // Tile list: expert e with c rows gets ceil(c / BM) row tiles. One block of
 // 1024 threads: tile counts, exclusive scan, then every thread fills tiles
 // i = tid, tid + 1024, ... by binary search over the per-expert tile starts.
+//
+// Chunk list (the tiled geometry launches two row tiles at a time, so that
+// both share their weight rows in L2): an expert's tiles pair up among
+// themselves, so its weights are never split across two chunks; the odd
+// tile left over by an expert pairs with the next expert's leftover. Chunk
+// order: all within-expert pairs (expert order), then the leftover pairs.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void build_tiles_kernel(const int32_t* __restrict__ offsets,
                                                            int NE, int BM, int4* __restrict__ tiles,
-                                                           int* __restrict__ ntiles) {
+                                                           int* __restrict__ ntiles,
+                                                           int2* __restrict__ chunks,
+                                                           int* __restrict__ nchunks) {
   extern __shared__ int start[];  // [NE + 1]
-  int m[2];
+  int m[2], tot[3][2];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int e = threadIdx.x + 1024 * q;
     m[q] = e < NE ? (offsets[e + 1] - offsets[e] + BM - 1) / BM : 0;
   }
-  int t0, t1;
-  const int p0 = block_exclusive_scan_1024(m[0], &t0);
-  const int p1 = block_exclusive_scan_1024(m[1], &t1) + t0;
-  if (threadIdx.x < NE) start[threadIdx.x] = p0;
-  if (threadIdx.x + 1024 < NE) start[threadIdx.x + 1024] = p1;
-  const int total = t0 + t1;
+  int p0[3], p1[3];  // exclusive prefix of: tiles, within-expert pairs, leftover singles
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const int v0 = k == 0 ? m[0] : (k == 1 ? m[0] / 2 : m[0] % 2);
+    const int v1 = k == 0 ? m[1] : (k == 1 ? m[1] / 2 : m[1] % 2);
+    p0[k] = block_exclusive_scan_1024(v0, &tot[k][0]);
+    p1[k] = block_exclusive_scan_1024(v1, &tot[k][1]) + tot[k][0];
+  }
+  const int total = tot[0][0] + tot[0][1];
+  const int pairs = tot[1][0] + tot[1][1];
+  const int singles = tot[2][0] + tot[2][1];
+  if (threadIdx.x < NE) start[threadIdx.x] = p0[0];
+  if (threadIdx.x + 1024 < NE) start[threadIdx.x + 1024] = p1[0];
   if (threadIdx.x == 0) {
     start[NE] = total;
     *ntiles = total;
+    *nchunks = pairs + (singles + 1) / 2;
+    if (singles & 1) chunks[pairs + singles / 2].y = -1;
+  }
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int e = threadIdx.x + 1024 * q;
+    if (e >= NE) continue;
+    const int ts = q ? p1[0] : p0[0], pr = q ? p1[1] : p0[1], sg = q ? p1[2] : p0[2];
+    for (int j = 0; j < m[q] / 2; ++j) chunks[pr + j] = make_int2(ts + 2 * j, ts + 2 * j + 1);
+    if (m[q] & 1) {
+      int* c = reinterpret_cast<int*>(&chunks[pairs + sg / 2]);
+      c[sg & 1] = ts + m[q] - 1;
+    }
   }
   __syncthreads();
   for (int i = threadIdx.x; i < total; i += 1024) {
@@ -59,7 +87,9 @@ GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt) 
   w.off[1] = o;  o += al((size_t)T * (H / 32));
   w.off[2] = o;  o += al(A * I * bits / 8);
   w.off[3] = o;  o += al(A * (I / 32));
-  w.off[4] = o;  o += al(sizeof(int4) * ((size_t)tile_bound((long)A, NE, 16) + 1) + 16);
+  // tile list (int4 x bound), its count, the chunk list (int2 x bound), its count
+  const size_t tb = (size_t)tile_bound((long)A, NE, 16) + 1;
+  w.off[4] = o;  o += al(sizeof(int4) * tb + 16 + sizeof(int2) * tb + 16);
   w.off[5] = o;
   return w;
 }
@@ -90,13 +120,16 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
   const int BM = tiled ? tiled_rows() : 16;
   const long A = (long)a.T * a.k_total;
   const int mt = tile_bound(A, a.NE, BM);
+  const int tb = tile_bound(A, a.NE, 16) + 1;
   int4* tiles = reinterpret_cast<int4*>(a.ws + w.off[4]);
-  int* ntiles = reinterpret_cast<int*>(tiles + tile_bound(A, a.NE, 16) + 1);
+  int* ntiles = reinterpret_cast<int*>(tiles + tb);
+  int2* chunks = reinterpret_cast<int2*>(ntiles + 4);
+  int* nchunks = reinterpret_cast<int*>(chunks + tb);
   if (stages & 1) {
     hipError_t err = launch_quantize_act(a.x, a.T, a.H, a.fmt, a.ws + w.off[0], a.ws + w.off[1], s);
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(build_tiles_kernel, dim3(1), dim3(1024), (a.NE + 1) * sizeof(int), s,
-                       a.offsets, a.NE, BM, tiles, ntiles);
+                       a.offsets, a.NE, BM, tiles, ntiles, chunks, nchunks);
   }
   if (stages & 2) {
     S1Args p1;
@@ -110,7 +143,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p1.H = a.H;
     p1.I = a.I;
     p1.k_total = a.k_total;
-    p1.t = TileArgs{tiles, ntiles, mt, 0, 1};
+    p1.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks};
     if (tiled) launch_s1_tiled(p1, mt, a.fmt, s);
     else launch_s1_stream(p1, mt, a.fmt, s);
   }
@@ -124,7 +157,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p2.partials = a.partials;
     p2.H = a.H;
     p2.I = a.I;
-    p2.t = TileArgs{tiles, ntiles, mt, 0, 1};
+    p2.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks};
     if (tiled) launch_s2_tiled(p2, mt, a.fmt, s);
     else launch_s2_stream(p2, mt, a.fmt, s);
   }

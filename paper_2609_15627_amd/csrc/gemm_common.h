@@ -47,6 +47,8 @@ struct TileArgs {
   int mt_bound;         // tiles the grid was sized for
   int n_ntiles;         // N tiles per expert
   int ngroup;           // consecutive N tiles per group (divides n_ntiles)
+  const int2* chunks;   // pairs of row tiles launched together (-1: none)
+  const int* nchunks;   // number of valid chunks
 };
 
 // Host side: the largest of 8, 4, 2, 1 that divides n.

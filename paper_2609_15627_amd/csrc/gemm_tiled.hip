@@ -48,7 +48,6 @@ constexpr int TBM = 256;       // sorted rows per tile
 constexpr int TBN = 256;       // weight rows per tile
 constexpr int kNStage = 3;     // K-step stages in the LDS ring
 constexpr int kSG = 4;         // K steps per scale group (16 scale bytes per row)
-constexpr int kTChunk = 2;     // row tiles per chunk of the launch order
 constexpr int kHStride = 132;  // fp32 row stride of the stage-1 epilogue buffer
 
 template <int FA>
@@ -323,21 +322,23 @@ __device__ __forceinline__ void t_kloop(uint8_t* lds, const TSrc<FA>& src, const
   t_group<FA, ST, FULL, true>(lds, src, L, nq - 1, w, nmb, acc, X, Y, sa, sb);
 }
 
-// Work item of this workgroup: row tile mt, N tile nt. Launch order is in
-// chunks of kTChunk row tiles x all N tiles (row tile fastest): the 32-odd
-// workgroups of a chunk run together and share both their activation rows
-// and their weight rows in L2. The dispatcher sends workgroup b to XCD b % 8;
-// XCD x takes chunks x, x + 8, x + 16, ... so every chunk stays on one XCD
-// and the chunks past the real tile count (the grid is sized for the upper
-// bound) are spread evenly over the XCDs.
+// Work item of this workgroup: a row tile of chunk c, N tile nt. A chunk is
+// two row tiles (of one expert where it has two) x all N tiles, row tile
+// fastest: its 32-odd workgroups run together and share their activation
+// rows and their weight rows in L2. The dispatcher sends workgroup b to XCD
+// b % 8; XCD x takes chunks x, x + 8, x + 16, ... so every chunk stays on
+// one XCD and the chunks past the real count (the grid is sized for the
+// upper bound) are spread evenly over the XCDs.
 __device__ __forceinline__ bool t_tile(const TileArgs& t, int4* tile, int* nt) {
-  const int per = kTChunk * t.n_ntiles;
+  const int per = 2 * t.n_ntiles;
   const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
   const int chunk = (j / per) * 8 + x, r = j % per;
-  *nt = r / kTChunk;
-  const int mt = chunk * kTChunk + r % kTChunk;
-  if (mt >= *t.ntiles) return false;
-  *tile = t.tiles[mt];
+  *nt = r >> 1;
+  if (chunk >= *t.nchunks) return false;
+  const int2 c = t.chunks[chunk];
+  const int ti = (r & 1) ? c.y : c.x;
+  if (ti < 0) return false;
+  *tile = t.tiles[ti];
   return true;
 }
 
@@ -606,8 +607,8 @@ template <int FA>
 static void launch_t1(const S1Args& p, long mt, hipStream_t s) {
   S1Args q = p;
   q.t.n_ntiles = p.I / (TBN / 2);
-  const long chunks8 = ((mt + kTChunk - 1) / kTChunk + 7) / 8 * 8;
-  const long n = chunks8 * kTChunk * q.t.n_ntiles;
+  const long chunks8 = (mt + 7) / 8 * 8;  // chunks <= row tiles <= mt
+  const long n = chunks8 * 2 * q.t.n_ntiles;
   hipLaunchKernelGGL((s1_tiled_kernel<FA>), dim3((int)n), dim3(256),
                      t_lds_s1<FA>(), s, q);
 }
@@ -616,8 +617,8 @@ template <int FA>
 static void launch_t2(const S2Args& p, long mt, hipStream_t s) {
   S2Args q = p;
   q.t.n_ntiles = p.H / TBN;
-  const long chunks8 = ((mt + kTChunk - 1) / kTChunk + 7) / 8 * 8;
-  const long n = chunks8 * kTChunk * q.t.n_ntiles;
+  const long chunks8 = (mt + 7) / 8 * 8;  // chunks <= row tiles <= mt
+  const long n = chunks8 * 2 * q.t.n_ntiles;
   hipLaunchKernelGGL((s2_tiled_kernel<FA>), dim3((int)n), dim3(256),
                      TL<FA>::kLoop, s, q);
 }
