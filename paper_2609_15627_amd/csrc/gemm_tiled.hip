@@ -156,40 +156,44 @@ struct TOps {
   v8i b[4];
 };
 
-template <int FA, int ST, int S, bool FULL>
-__device__ __forceinline__ void t_read_ops(const uint8_t* st, const TLane& L, int nmb, TOps& o) {
+// Operand reads of sub-step S for the wave's first NMB row blocks (none at
+// all when the wave has no rows).
+template <int FA, int ST, int S, int NMB>
+__device__ __forceinline__ void t_read_ops(const uint8_t* st, const TLane& L, TOps& o) {
   using Lo = TL<FA>;
+  if constexpr (NMB > 0) {
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) {
-    const v4u v = *reinterpret_cast<const v4u*>(st + L.b[S] + t_nrow<ST>(nb) * 64);
-    o.b[nb] = v8i{(int)v.x, (int)v.y, (int)v.z, (int)v.w, 0, 0, 0, 0};
+    for (int nb = 0; nb < 4; ++nb) {
+      const v4u v = *reinterpret_cast<const v4u*>(st + L.b[S] + t_nrow<ST>(nb) * 64);
+      o.b[nb] = v8i{(int)v.x, (int)v.y, (int)v.z, (int)v.w, 0, 0, 0, 0};
+    }
   }
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) {
-    if (FULL || mb < nmb) {
-      const v4u lo = *reinterpret_cast<const v4u*>(st + L.a0[S] + mb * 32 * Lo::kARow);
-      if constexpr (FA == 0) {
-        const v4u hi = *reinterpret_cast<const v4u*>(st + L.a1[S] + mb * 32 * Lo::kARow);
-        o.a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w,
-                      (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
-      } else {
-        o.a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, 0, 0, 0, 0};
-      }
+  for (int mb = 0; mb < NMB; ++mb) {
+    const v4u lo = *reinterpret_cast<const v4u*>(st + L.a0[S] + mb * 32 * Lo::kARow);
+    if constexpr (FA == 0) {
+      const v4u hi = *reinterpret_cast<const v4u*>(st + L.a1[S] + mb * 32 * Lo::kARow);
+      o.a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w,
+                    (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+    } else {
+      o.a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, 0, 0, 0, 0};
     }
   }
 }
 
 // Scale byte pairs of step j of a group: byte s of the result is the scale
 // of sub-step s for this lane.
-template <int ST>
+template <int ST, int NMB>
 __device__ __forceinline__ void t_read_scales(const uint8_t* sbuf, const TLane& L, int j,
                                               uint32_t* sa, uint32_t* sb) {
+  if constexpr (NMB > 0) {
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
-    sa[mb] = *reinterpret_cast<const uint16_t*>(sbuf + L.as + mb * 32 * 16 + 4 * j);
+    for (int mb = 0; mb < NMB; ++mb)
+      sa[mb] = *reinterpret_cast<const uint16_t*>(sbuf + L.as + mb * 32 * 16 + 4 * j);
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb)
-    sb[nb] = *reinterpret_cast<const uint16_t*>(sbuf + L.bs + t_nrow<ST>(nb) * 16 + 4 * j);
+    for (int nb = 0; nb < 4; ++nb)
+      sb[nb] = *reinterpret_cast<const uint16_t*>(sbuf + L.bs + t_nrow<ST>(nb) * 16 + 4 * j);
+  }
 }
 
 template <int FA, int OPS>
@@ -200,53 +204,59 @@ __device__ __forceinline__ v16f t_mfma(const v8i& a, const v8i& b, const v16f& c
 }
 
 // Products of sub-step S for blocks (mb, nb) with mb in [MB0, MB1).
-template <int FA, int S, int MB0, int MB1, bool FULL>
+template <int FA, int S, int MB0, int MB1>
 __device__ __forceinline__ void t_mma(v16f (*acc)[4], const TOps& o, const uint32_t* sa,
-                                      const uint32_t* sb, int nmb) {
+                                      const uint32_t* sb) {
 #pragma unroll
   for (int mb = MB0; mb < MB1; ++mb)
-    if (FULL || mb < nmb) {
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb)
-        acc[mb][nb] = t_mfma<FA, S>(o.a[mb], o.b[nb], acc[mb][nb], sa[mb], sb[nb]);
-    }
+    for (int nb = 0; nb < 4; ++nb)
+      acc[mb][nb] = t_mfma<FA, S>(o.a[mb], o.b[nb], acc[mb][nb], sa[mb], sb[nb]);
 }
 
-// Interleave hint: alternate N single products with R LDS reads each.
-template <int N, int R>
-__device__ __forceinline__ void t_sched_mma_ds() {
+// Interleave hint: M single products, each followed by D LDS reads and V
+// DMA instructions (what is left over is scheduled freely).
+template <int M, int D, int V>
+__device__ __forceinline__ void t_sched() {
 #pragma unroll
-  for (int i = 0; i < N; ++i) {
+  for (int i = 0; i < M; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+    if constexpr (D > 0) __builtin_amdgcn_sched_group_barrier(0x100, D, 0);
+    if constexpr (V > 0) __builtin_amdgcn_sched_group_barrier(0x020, V, 0);
   }
 }
 
-// Interleave hint for the second half of a step: each product followed by
-// two LDS reads and one DMA instruction.
-__device__ __forceinline__ void t_sched_mma_vm_ds() {
-#pragma unroll
-  for (int i = 0; i < 12; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-  }
+constexpr int t_ceil(int a, int b) { return b > 0 ? (a + b - 1) / b : 0; }
+constexpr int t_min(int a, int b) { return a < b ? a : b; }
+
+// Interleave hint for the second half of a step: the LDS reads go first (the
+// DMA writes that follow them in program order may not pass them), R per
+// product, then the DMA instructions spread over the remaining products.
+template <int M, int D, int V>
+__device__ __forceinline__ void t_sched_b() {
+  constexpr int R = M > 0 ? (t_ceil(D, M) > 4 ? t_ceil(D, M) : 4) : 0;
+  constexpr int M1 = t_min(M, t_ceil(D, R));
+  constexpr int M2 = M - M1;
+  t_sched<M1, R, 0>();
+  t_sched<M2, 0, t_ceil(V, M2)>();
 }
 
-// One K step k = 4q + J (J compile-time). Stage k lives in ring slot k % 3,
-// scale group q in buffer q % 2. X holds the step's sub-step-0 operands and
-// sa/sb its scales on entry; on exit they hold those of step k + 1.
+// One K step k = 4q + J (J compile-time) of a wave that owns NMB row blocks
+// (0..4, uniform per wave; a wave without rows still moves data and takes
+// part in the barriers). Stage k lives in ring slot k % 3, scale group q in
+// buffer q % 2. X holds the step's sub-step-0 operands and sa/sb its scales
+// on entry; on exit they hold those of step k + 1.
 //   1. sub-step-0 products on X while sub-step-1 operands are read into Y;
 //   2. one row of sub-step-1 products, then: this wave's loads of stage k + 1
 //      landed, workgroup barrier (every wave has left stage k, stage k + 1 is
 //      visible);
-//   3. DMA of stage k + 3 into slot k % 3 (at J == 0 also scale group q + 1,
-//      into the buffer group q - 1 used), reads of step k + 1's operands and
-//      scales, interleaved with the remaining sub-step-1 products.
+//   3. reads of step k + 1's operands and scales, then the DMA of stage k + 3
+//      into slot k % 3 (at J == 0 also scale group q + 1, into the buffer
+//      group q - 1 used), interleaved with the remaining sub-step-1 products.
 // LAST marks the final group (k = nk - 4 + J), where the ring drains.
-template <int FA, int ST, bool FULL, int J, bool LAST>
+template <int FA, int ST, int NMB, int J, bool LAST>
 __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const TLane& L,
-                                       int k, int w, int nmb, v16f (*acc)[4], TOps& X, TOps& Y,
+                                       int k, int w, v16f (*acc)[4], TOps& X, TOps& Y,
                                        uint32_t* sa, uint32_t* sb) {
   using Lo = TL<FA>;
   constexpr bool kNext = !LAST || J < 3;  // step k + 1 exists
@@ -255,32 +265,37 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   // Loads issued after stage k + 1's: stage k + 2 and, when J == 1 outside
   // the last group, the scale group issued just before it.
   constexpr int kWait = !LAST ? (J == 1 ? 2 : 1) : (J < 2 ? 1 : (J == 2 ? 0 : -1));
+  constexpr int kAPieces = FA == 0 ? 2 : 1;
+  constexpr int kOpReads = NMB > 0 ? 4 + kAPieces * NMB : 0;
+  constexpr int kScaleReads = NMB > 0 ? 4 + NMB : 0;
   const uint8_t* st = lds + (k % kNStage) * Lo::kStage;
 
   __builtin_amdgcn_sched_barrier(0);
-  t_read_ops<FA, ST, 1, FULL>(st, L, nmb, Y);
-  t_mma<FA, 0, 0, 4, FULL>(acc, X, sa, sb, nmb);
-  if constexpr (FULL) t_sched_mma_ds<12, 1>();
+  t_read_ops<FA, ST, 1, NMB>(st, L, Y);
+  t_mma<FA, 0, 0, NMB>(acc, X, sa, sb);
+  t_sched<4 * NMB, t_ceil(kOpReads, 4 * NMB), 0>();
   __builtin_amdgcn_sched_barrier(0);
   tlgkm0();
-  t_mma<FA, 1, 0, 1, FULL>(acc, Y, sa, sb, nmb);
+  t_mma<FA, 1, 0, NMB < 1 ? NMB : 1>(acc, Y, sa, sb);
   if constexpr (kWait == 2) tvmcnt<Lo::kStageLoads + Lo::kScaleLoads>();
   else if constexpr (kWait == 1) tvmcnt<Lo::kStageLoads>();
   else if constexpr (kWait == 0) tvmcnt<0>();
   tbarrier();
   __builtin_amdgcn_sched_barrier(0);
+  uint32_t ra[4], rb[4];
+  if constexpr (kNext) {
+    const int k1 = k + 1;
+    t_read_scales<ST, NMB>(lds + Lo::kS + ((k1 / kSG) & 1) * Lo::kSBuf, L, (J + 1) % kSG, ra, rb);
+    t_read_ops<FA, ST, 0, NMB>(lds + (k1 % kNStage) * Lo::kStage, L, X);
+  }
   if constexpr (kIssue) {
     if constexpr (kScales) t_issue_scales<FA>(lds, src, w, k / kSG + 1);
     t_issue_stage<FA>(lds, src, w, k + kNStage);
   }
-  uint32_t ra[4], rb[4];
-  if constexpr (kNext) {
-    const int k1 = k + 1;
-    t_read_scales<ST>(lds + Lo::kS + ((k1 / kSG) & 1) * Lo::kSBuf, L, (J + 1) % kSG, ra, rb);
-    t_read_ops<FA, ST, 0, FULL>(lds + (k1 % kNStage) * Lo::kStage, L, nmb, X);
-  }
-  t_mma<FA, 1, 1, 4, FULL>(acc, Y, sa, sb, nmb);
-  if constexpr (FULL) t_sched_mma_vm_ds();
+  t_mma<FA, 1, 1, NMB>(acc, Y, sa, sb);
+  constexpr int kM = NMB > 1 ? 4 * (NMB - 1) : 0;
+  t_sched_b<kM, kNext ? kOpReads + kScaleReads : 0,
+            kIssue ? Lo::kStageLoads + (kScales ? Lo::kScaleLoads : 0) : 0>();
   __builtin_amdgcn_sched_barrier(0);
   if constexpr (kNext) {
 #pragma unroll
@@ -291,21 +306,21 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   }
 }
 
-template <int FA, int ST, bool FULL, bool LAST>
+template <int FA, int ST, int NMB, bool LAST>
 __device__ __forceinline__ void t_group(uint8_t* lds, const TSrc<FA>& src, const TLane& L, int q,
-                                        int w, int nmb, v16f (*acc)[4], TOps& X, TOps& Y,
-                                        uint32_t* sa, uint32_t* sb) {
-  t_step<FA, ST, FULL, 0, LAST>(lds, src, L, 4 * q + 0, w, nmb, acc, X, Y, sa, sb);
-  t_step<FA, ST, FULL, 1, LAST>(lds, src, L, 4 * q + 1, w, nmb, acc, X, Y, sa, sb);
-  t_step<FA, ST, FULL, 2, LAST>(lds, src, L, 4 * q + 2, w, nmb, acc, X, Y, sa, sb);
-  t_step<FA, ST, FULL, 3, LAST>(lds, src, L, 4 * q + 3, w, nmb, acc, X, Y, sa, sb);
+                                        int w, v16f (*acc)[4], TOps& X, TOps& Y, uint32_t* sa,
+                                        uint32_t* sb) {
+  t_step<FA, ST, NMB, 0, LAST>(lds, src, L, 4 * q + 0, w, acc, X, Y, sa, sb);
+  t_step<FA, ST, NMB, 1, LAST>(lds, src, L, 4 * q + 1, w, acc, X, Y, sa, sb);
+  t_step<FA, ST, NMB, 2, LAST>(lds, src, L, 4 * q + 2, w, acc, X, Y, sa, sb);
+  t_step<FA, ST, NMB, 3, LAST>(lds, src, L, 4 * q + 3, w, acc, X, Y, sa, sb);
 }
 
 // The K loop shared by both stages: nk = K / 128 steps, a multiple of 4.
 // Scale group 0 and stages 0-2 are in flight before the first step.
-template <int FA, int ST, bool FULL>
-__device__ __forceinline__ void t_kloop(uint8_t* lds, const TSrc<FA>& src, const TLane& L,
-                                        int nk, int w, int nmb, v16f (*acc)[4]) {
+template <int FA, int ST, int NMB>
+__device__ __forceinline__ void t_kloop_n(uint8_t* lds, const TSrc<FA>& src, const TLane& L, int nk,
+                                       int w, v16f (*acc)[4]) {
   using Lo = TL<FA>;
   t_issue_scales<FA>(lds, src, w, 0);
 #pragma unroll
@@ -315,11 +330,24 @@ __device__ __forceinline__ void t_kloop(uint8_t* lds, const TSrc<FA>& src, const
 
   TOps X, Y;
   uint32_t sa[4], sb[4];
-  t_read_ops<FA, ST, 0, FULL>(lds, L, nmb, X);
-  t_read_scales<ST>(lds + Lo::kS, L, 0, sa, sb);
+  t_read_ops<FA, ST, 0, NMB>(lds, L, X);
+  t_read_scales<ST, NMB>(lds + Lo::kS, L, 0, sa, sb);
   const int nq = nk / kSG;
-  for (int q = 0; q < nq - 1; ++q) t_group<FA, ST, FULL, false>(lds, src, L, q, w, nmb, acc, X, Y, sa, sb);
-  t_group<FA, ST, FULL, true>(lds, src, L, nq - 1, w, nmb, acc, X, Y, sa, sb);
+  for (int q = 0; q < nq - 1; ++q) t_group<FA, ST, NMB, false>(lds, src, L, q, w, acc, X, Y, sa, sb);
+  t_group<FA, ST, NMB, true>(lds, src, L, nq - 1, w, acc, X, Y, sa, sb);
+}
+
+// nmb: row blocks of 32 this wave owns in the tile (wave-uniform).
+template <int FA, int ST>
+__device__ __forceinline__ void t_kloop(uint8_t* lds, const TSrc<FA>& src, const TLane& L, int nk,
+                                        int w, int nmb, v16f (*acc)[4]) {
+  switch (nmb) {
+    case 4: t_kloop_n<FA, ST, 4>(lds, src, L, nk, w, acc); break;
+    case 3: t_kloop_n<FA, ST, 3>(lds, src, L, nk, w, acc); break;
+    case 2: t_kloop_n<FA, ST, 2>(lds, src, L, nk, w, acc); break;
+    case 1: t_kloop_n<FA, ST, 1>(lds, src, L, nk, w, acc); break;
+    default: t_kloop_n<FA, ST, 0>(lds, src, L, nk, w, acc); break;
+  }
 }
 
 // Work item of this workgroup: a row tile of chunk c, N tile nt. A chunk is
@@ -414,14 +442,13 @@ __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
     S.bs = (uint32_t)(wrow(64 * w + lane) * (p.H / 32));
   }
   const TLane L = t_lane<FA, 1>(w, lane);
-  const int nmb = min(4, max(0, (nrows - 128 * wm + 31) / 32));
+  const int nmb = __builtin_amdgcn_readfirstlane(min(4, max(0, (nrows - 128 * wm + 31) / 32)));
   v16f acc[4][4];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = v16f{};
-  if (nrows == TBM) t_kloop<FA, 1, true>(lds, S, L, p.H / 128, w, nmb, acc);
-  else t_kloop<FA, 1, false>(lds, S, L, p.H / 128, w, nmb, acc);
+  t_kloop<FA, 1>(lds, S, L, p.H / 128, w, nmb, acc);
 
   // Epilogue, through LDS:
   //  1. each lane writes its SwiGLU values h as fp32 rows [256][kHStride];
@@ -562,14 +589,13 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
     S.bs = (uint32_t)((64 * w + lane) * (p.I / 32));
   }
   const TLane L = t_lane<FA, 2>(w, lane);
-  const int nmb = min(4, max(0, (nrows - 128 * wm + 31) / 32));
+  const int nmb = __builtin_amdgcn_readfirstlane(min(4, max(0, (nrows - 128 * wm + 31) / 32)));
   v16f acc[4][4];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = v16f{};
-  if (nrows == TBM) t_kloop<FA, 2, true>(lds, S, L, p.I / 128, w, nmb, acc);
-  else t_kloop<FA, 2, false>(lds, S, L, p.I / 128, w, nmb, acc);
+  t_kloop<FA, 2>(lds, S, L, p.I / 128, w, nmb, acc);
 
   // Epilogue: fp32 partial rows to their unique assignment slots.
   tbarrier();
