@@ -11,6 +11,9 @@ namespace moe {
 // 1024 threads: tile counts, exclusive scan, then every thread fills tiles
 // i = tid, tid + 1024, ... by binary search over the per-expert tile starts.
 //
+// The work queue of the persistent tiled kernels starts at zero here; each
+// of their launches leaves it at zero when it ends.
+//
 // Chunk list (the tiled geometry launches two row tiles at a time, so that
 // both share their weight rows in L2): an expert's tiles pair up among
 // themselves, so its weights are never split across two chunks; the odd
@@ -21,7 +24,8 @@ __global__ __launch_bounds__(1024) void build_tiles_kernel(const int32_t* __rest
                                                            int NE, int BM, int4* __restrict__ tiles,
                                                            int* __restrict__ ntiles,
                                                            int2* __restrict__ chunks,
-                                                           int* __restrict__ nchunks) {
+                                                           int* __restrict__ nchunks,
+                                                           int* __restrict__ queue) {
   extern __shared__ int start[];  // [NE + 1]
   int m[2], tot[3][2];
 #pragma unroll
@@ -42,6 +46,7 @@ __global__ __launch_bounds__(1024) void build_tiles_kernel(const int32_t* __rest
   const int singles = tot[2][0] + tot[2][1];
   if (threadIdx.x < NE) start[threadIdx.x] = p0[0];
   if (threadIdx.x + 1024 < NE) start[threadIdx.x + 1024] = p1[0];
+  if (threadIdx.x < kQueueInts) queue[threadIdx.x] = 0;
   if (threadIdx.x == 0) {
     start[NE] = total;
     *ntiles = total;
@@ -87,9 +92,10 @@ GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt) 
   w.off[1] = o;  o += al((size_t)T * (H / 32));
   w.off[2] = o;  o += al(A * I * bits / 8);
   w.off[3] = o;  o += al(A * (I / 32));
-  // tile list (int4 x bound), its count, the chunk list (int2 x bound), its count
+  // tile list (int4 x bound), its count, the chunk list (int2 x bound), its
+  // count, the work queue
   const size_t tb = (size_t)tile_bound((long)A, NE, 16) + 1;
-  w.off[4] = o;  o += al(sizeof(int4) * tb + 16 + sizeof(int2) * tb + 16);
+  w.off[4] = o;  o += al(sizeof(int4) * tb + 16 + sizeof(int2) * tb + 16 + 4 * kQueueInts);
   w.off[5] = o;
   return w;
 }
@@ -125,11 +131,12 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
   int* ntiles = reinterpret_cast<int*>(tiles + tb);
   int2* chunks = reinterpret_cast<int2*>(ntiles + 4);
   int* nchunks = reinterpret_cast<int*>(chunks + tb);
+  int* queue = nchunks + 4;
   if (stages & 1) {
     hipError_t err = launch_quantize_act(a.x, a.T, a.H, a.fmt, a.ws + w.off[0], a.ws + w.off[1], s);
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(build_tiles_kernel, dim3(1), dim3(1024), (a.NE + 1) * sizeof(int), s,
-                       a.offsets, a.NE, BM, tiles, ntiles, chunks, nchunks);
+                       a.offsets, a.NE, BM, tiles, ntiles, chunks, nchunks, queue);
   }
   if (stages & 2) {
     S1Args p1;
@@ -143,7 +150,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p1.H = a.H;
     p1.I = a.I;
     p1.k_total = a.k_total;
-    p1.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks};
+    p1.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks, queue};
     if (tiled) launch_s1_tiled(p1, mt, a.fmt, s);
     else launch_s1_stream(p1, mt, a.fmt, s);
   }
@@ -157,7 +164,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p2.partials = a.partials;
     p2.H = a.H;
     p2.I = a.I;
-    p2.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks};
+    p2.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks, queue};
     if (tiled) launch_s2_tiled(p2, mt, a.fmt, s);
     else launch_s2_stream(p2, mt, a.fmt, s);
   }

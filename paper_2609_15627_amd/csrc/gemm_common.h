@@ -41,6 +41,8 @@ __device__ __forceinline__ uint32_t gather_scales(const uint8_t* p, int g) {
   return r;
 }
 
+constexpr int kQueueInts = 16;  // ints of the persistent geometry's work queue
+
 struct TileArgs {
   const int4* tiles;    // (expert, first sorted row, rows, 0)
   const int* ntiles;    // number of valid tiles
@@ -49,6 +51,7 @@ struct TileArgs {
   int ngroup;           // consecutive N tiles per group (divides n_ntiles)
   const int2* chunks;   // pairs of row tiles launched together (-1: none)
   const int* nchunks;   // number of valid chunks
+  int* queue;           // work tickets of the persistent geometry: [8] per XCD, [8] finished
 };
 
 // Host side: the largest of 8, 4, 2, 1 that divides n.

@@ -350,24 +350,75 @@ __device__ __forceinline__ void t_kloop(uint8_t* lds, const TSrc<FA>& src, const
   }
 }
 
-// Work item of this workgroup: a row tile of chunk c, N tile nt. A chunk is
-// two row tiles (of one expert where it has two) x all N tiles, row tile
-// fastest: its 32-odd workgroups run together and share their activation
-// rows and their weight rows in L2. The dispatcher sends workgroup b to XCD
-// b % 8; XCD x takes chunks x, x + 8, x + 16, ... so every chunk stays on
-// one XCD and the chunks past the real count (the grid is sized for the
-// upper bound) are spread evenly over the XCDs.
-__device__ __forceinline__ bool t_tile(const TileArgs& t, int4* tile, int* nt) {
-  const int per = 2 * t.n_ntiles;
-  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
-  const int chunk = (j / per) * 8 + x, r = j % per;
+// Work distribution (persistent kernels, one workgroup per CU). A work
+// item is one row tile x one N tile. A chunk is two row tiles (of one expert
+// where it has two) x all N tiles, row tile fastest; the chunk's items run
+// at about the same time on one XCD and share their activation rows and
+// weight rows in that XCD's L2. Chunk c belongs to queue c % 8; workgroup b
+// takes tickets from queue b % 8 (the dispatcher places workgroup b on XCD
+// b % 8) and, once that queue is empty, from the others. Which workgroup
+// computes an item does not change any result: every item writes its own
+// outputs.
+__device__ __forceinline__ int t_queue_items(int nch, int x, int per) {
+  return (nch > x ? (nch - x + 7) / 8 : 0) * per;
+}
+
+// Next item as 8 * (index within its queue) + queue, or -1 when none is left.
+__device__ __forceinline__ int t_grab(const TileArgs& t, int nch, int per) {
+  const int x = blockIdx.x & 7;
+  for (int v = 0; v < 8; ++v) {
+    const int q = (x + v) & 7;
+    const int n = t_queue_items(nch, q, per);
+    if (n == 0) continue;
+    const int i = __hip_atomic_fetch_add(t.queue + q, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (i >= 0 && i < n) return 8 * i + q;
+  }
+  return -1;
+}
+
+// Row tile and N tile of an item; false for the empty half of a chunk.
+__device__ __forceinline__ bool t_item(const TileArgs& t, int item, int per, int4* tile, int* nt) {
+  const int q = item & 7, i = item >> 3;
+  const int chunk = 8 * (i / per) + q, r = i % per;
   *nt = r >> 1;
-  if (chunk >= *t.nchunks) return false;
   const int2 c = t.chunks[chunk];
   const int ti = (r & 1) ? c.y : c.x;
   if (ti < 0) return false;
   *tile = t.tiles[ti];
   return true;
+}
+
+// Called once per workgroup after its last item: the last one to finish
+// returns the queue to zero for the next launch (all others have taken
+// their final ticket by then).
+__device__ __forceinline__ void t_finish(const TileArgs& t) {
+  const int done = __hip_atomic_fetch_add(t.queue + 8, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+  if (done == (int)gridDim.x - 1) {
+    for (int q = 0; q <= 8; ++q)
+      __hip_atomic_store(t.queue + q, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// The persistent loop: thread 0 takes a ticket and hands it to the other
+// waves through an LDS word in the second scale buffer, which the K loop
+// first writes after the barrier of its first step (every wave has read the
+// ticket by then).
+template <int FA, typename Body>
+__device__ __forceinline__ void t_persist(const TileArgs& t, uint8_t* lds, Body body) {
+  int* slot = reinterpret_cast<int*>(lds + TL<FA>::kS + TL<FA>::kSBuf);
+  const int per = 2 * t.n_ntiles;
+  const int nch = *t.nchunks;
+  for (;;) {
+    if (threadIdx.x == 0) *slot = t_grab(t, nch, per);
+    __syncthreads();
+    const int item = __builtin_amdgcn_readfirstlane(*slot);  // uniform: scalar tile loads
+    if (item < 0) break;
+    int4 tile;
+    int nt;
+    if (t_item(t, item, per, &tile, &nt)) body(tile, nt);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) t_finish(t);
 }
 
 template <int FA, int ST>
@@ -403,14 +454,14 @@ __device__ __forceinline__ float swiglu_fast(float G, float U) {
 }
 
 template <int FA>
-__global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
+__device__ __forceinline__ void s1_tile(const S1Args& p, uint8_t* lds, int4 tile, int nt) {
   using Lo = TL<FA>;
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  int4 tile;
-  int nt;
-  if (!t_tile(p.t, &tile, &nt)) return;
   const int e = tile.x, row0 = tile.y, nrows = tile.z;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  // lane-derived offsets are recomputed per tile rather than held in
+  // registers across the persistent loop (the opaque copy blocks hoisting)
+  int lane = threadIdx.x % kWave;
+  asm volatile("" : "+v"(lane));
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int wm = w & 1, wn = w >> 1;
   const int hc0 = nt * (TBN / 2);  // first h column of the tile
   const int xrow = (p.H / 32) * ActBytes<FA>::kBlock;
@@ -553,14 +604,14 @@ __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
 }
 
 template <int FA>
-__global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
+__device__ __forceinline__ void s2_tile(const S2Args& p, uint8_t* lds, int4 tile, int nt) {
   using Lo = TL<FA>;
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  int4 tile;
-  int nt;
-  if (!t_tile(p.t, &tile, &nt)) return;
   const int e = tile.x, row0 = tile.y, nrows = tile.z;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  // lane-derived offsets are recomputed per tile rather than held in
+  // registers across the persistent loop (the opaque copy blocks hoisting)
+  int lane = threadIdx.x % kWave;
+  asm volatile("" : "+v"(lane));
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int wm = w & 1, wn = w >> 1;
   const int nc0 = nt * TBN;  // first output column of the tile
   const int arow = (p.I / 32) * ActBytes<FA>::kBlock;
@@ -619,6 +670,18 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
   }
 }
 
+template <int FA>
+__global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  t_persist<FA>(p.t, lds, [&](int4 tile, int nt) { s1_tile<FA>(p, lds, tile, nt); });
+}
+
+template <int FA>
+__global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  t_persist<FA>(p.t, lds, [&](int4 tile, int nt) { s2_tile<FA>(p, lds, tile, nt); });
+}
+
 int tiled_rows() { return TBM; }
 
 size_t tiled_lds_bytes(int fa) {
@@ -629,13 +692,24 @@ size_t tiled_lds_bytes(int fa) {
 // columns (stage 1) and 256 output columns (stage 2).
 bool tiled_ok(int H, int I) { return H % (128 * kSG) == 0 && I % (128 * kSG) == 0; }
 
+// One workgroup per CU (each holds a CU's LDS), never more than the items.
+static int persistent_grid(long mt, int n_ntiles) {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 256;
+    return n > 0 ? n : 256;
+  }();
+  const long items = mt * n_ntiles;
+  return (int)(items < cus ? (items > 0 ? items : 1) : cus);
+}
+
 template <int FA>
 static void launch_t1(const S1Args& p, long mt, hipStream_t s) {
   S1Args q = p;
   q.t.n_ntiles = p.I / (TBN / 2);
-  const long chunks8 = (mt + 7) / 8 * 8;  // chunks <= row tiles <= mt
-  const long n = chunks8 * 2 * q.t.n_ntiles;
-  hipLaunchKernelGGL((s1_tiled_kernel<FA>), dim3((int)n), dim3(256),
+  hipLaunchKernelGGL((s1_tiled_kernel<FA>), dim3(persistent_grid(mt, q.t.n_ntiles)), dim3(256),
                      t_lds_s1<FA>(), s, q);
 }
 
@@ -643,9 +717,7 @@ template <int FA>
 static void launch_t2(const S2Args& p, long mt, hipStream_t s) {
   S2Args q = p;
   q.t.n_ntiles = p.H / TBN;
-  const long chunks8 = (mt + 7) / 8 * 8;  // chunks <= row tiles <= mt
-  const long n = chunks8 * 2 * q.t.n_ntiles;
-  hipLaunchKernelGGL((s2_tiled_kernel<FA>), dim3((int)n), dim3(256),
+  hipLaunchKernelGGL((s2_tiled_kernel<FA>), dim3(persistent_grid(mt, q.t.n_ntiles)), dim3(256),
                      TL<FA>::kLoop, s, q);
 }
 
