@@ -318,13 +318,21 @@ __device__ __forceinline__ void t_group(uint8_t* lds, const TSrc<FA>& src, const
 
 // The K loop shared by both stages: nk = K / 128 steps, a multiple of 4.
 // Scale group 0 and stages 0-2 are in flight before the first step.
-template <int FA, int ST, int NMB>
-__device__ __forceinline__ void t_kloop_n(uint8_t* lds, const TSrc<FA>& src, const TLane& L, int nk,
-                                       int w, v16f (*acc)[4]) {
-  using Lo = TL<FA>;
+template <int FA>
+__device__ __forceinline__ void t_prologue(uint8_t* lds, const TSrc<FA>& src, int w) {
   t_issue_scales<FA>(lds, src, w, 0);
 #pragma unroll
   for (int s = 0; s < kNStage; ++s) t_issue_stage<FA>(lds, src, w, s);
+}
+
+// PRO: issue the prologue here (else the caller issued it earlier; loads or
+// stores issued after it only make the first wait stricter, since loads
+// complete in order).
+template <int FA, int ST, int NMB, bool PRO>
+__device__ __forceinline__ void t_kloop_n(uint8_t* lds, const TSrc<FA>& src, const TLane& L, int nk,
+                                       int w, v16f (*acc)[4]) {
+  using Lo = TL<FA>;
+  if constexpr (PRO) t_prologue<FA>(lds, src, w);
   tvmcnt<2 * Lo::kStageLoads>();
   tbarrier();
 
@@ -338,15 +346,15 @@ __device__ __forceinline__ void t_kloop_n(uint8_t* lds, const TSrc<FA>& src, con
 }
 
 // nmb: row blocks of 32 this wave owns in the tile (wave-uniform).
-template <int FA, int ST>
+template <int FA, int ST, bool PRO>
 __device__ __forceinline__ void t_kloop(uint8_t* lds, const TSrc<FA>& src, const TLane& L, int nk,
                                         int w, int nmb, v16f (*acc)[4]) {
   switch (nmb) {
-    case 4: t_kloop_n<FA, ST, 4>(lds, src, L, nk, w, acc); break;
-    case 3: t_kloop_n<FA, ST, 3>(lds, src, L, nk, w, acc); break;
-    case 2: t_kloop_n<FA, ST, 2>(lds, src, L, nk, w, acc); break;
-    case 1: t_kloop_n<FA, ST, 1>(lds, src, L, nk, w, acc); break;
-    default: t_kloop_n<FA, ST, 0>(lds, src, L, nk, w, acc); break;
+    case 4: t_kloop_n<FA, ST, 4, PRO>(lds, src, L, nk, w, acc); break;
+    case 3: t_kloop_n<FA, ST, 3, PRO>(lds, src, L, nk, w, acc); break;
+    case 2: t_kloop_n<FA, ST, 2, PRO>(lds, src, L, nk, w, acc); break;
+    case 1: t_kloop_n<FA, ST, 1, PRO>(lds, src, L, nk, w, acc); break;
+    default: t_kloop_n<FA, ST, 0, PRO>(lds, src, L, nk, w, acc); break;
   }
 }
 
@@ -399,26 +407,27 @@ __device__ __forceinline__ void t_finish(const TileArgs& t) {
   }
 }
 
-// The persistent loop: thread 0 takes a ticket and hands it to the other
-// waves through an LDS word in the second scale buffer, which the K loop
-// first writes after the barrier of its first step (every wave has read the
-// ticket by then).
-template <int FA, typename Body>
-__device__ __forceinline__ void t_persist(const TileArgs& t, uint8_t* lds, Body body) {
-  int* slot = reinterpret_cast<int*>(lds + TL<FA>::kS + TL<FA>::kSBuf);
-  const int per = 2 * t.n_ntiles;
-  const int nch = *t.nchunks;
+// Barrier for the persistent loop: this wave's LDS accesses are complete,
+// then all waves meet (no wait for global memory).
+__device__ __forceinline__ void t_sync_lds() {
+  tlgkm0();
+  tbarrier();
+}
+
+// Next work item of the workgroup (false: none left). Thread 0 takes the
+// tickets and hands them to the other waves through the LDS word `slot`,
+// which nothing else writes between the two barriers; skips the empty half
+// of a chunk.
+__device__ __forceinline__ bool t_next(const TileArgs& t, int* slot, int nch, int per,
+                                       int4* tile, int* nt) {
   for (;;) {
+    t_sync_lds();  // every wave has read the previous ticket
     if (threadIdx.x == 0) *slot = t_grab(t, nch, per);
-    __syncthreads();
+    t_sync_lds();
     const int item = __builtin_amdgcn_readfirstlane(*slot);  // uniform: scalar tile loads
-    if (item < 0) break;
-    int4 tile;
-    int nt;
-    if (t_item(t, item, per, &tile, &nt)) body(tile, nt);
-    __syncthreads();
+    if (item < 0) return false;
+    if (t_item(t, item, per, tile, nt)) return true;
   }
-  if (threadIdx.x == 0) t_finish(t);
 }
 
 template <int FA, int ST>
@@ -499,7 +508,7 @@ __device__ __forceinline__ void s1_tile(const S1Args& p, uint8_t* lds, int4 tile
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = v16f{};
-  t_kloop<FA, 1>(lds, S, L, p.H / 128, w, nmb, acc);
+  t_kloop<FA, 1, true>(lds, S, L, p.H / 128, w, nmb, acc);
 
   // Epilogue, through LDS:
   //  1. each lane writes its SwiGLU values h as fp32 rows [256][kHStride];
@@ -603,84 +612,127 @@ __device__ __forceinline__ void s1_tile(const S1Args& p, uint8_t* lds, int4 tile
   }
 }
 
+// Stage-2 work item: DMA sources and shape of one tile.
 template <int FA>
-__device__ __forceinline__ void s2_tile(const S2Args& p, uint8_t* lds, int4 tile, int nt) {
+struct S2Tile {
+  TSrc<FA> S;
+  int row0, nrows, nc0;
+};
+
+template <int FA>
+__device__ __forceinline__ S2Tile<FA> s2_setup(const S2Args& p, int4 tile, int nt, int w, int lane) {
   using Lo = TL<FA>;
   const int e = tile.x, row0 = tile.y, nrows = tile.z;
-  // lane-derived offsets are recomputed per tile rather than held in
-  // registers across the persistent loop (the opaque copy blocks hoisting)
-  int lane = threadIdx.x % kWave;
-  asm volatile("" : "+v"(lane));
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int wm = w & 1, wn = w >> 1;
-  const int nc0 = nt * TBN;  // first output column of the tile
   const int arow = (p.I / 32) * ActBytes<FA>::kBlock;
-
-  TSrc<FA> S;
-  S.abase = p.hq + (size_t)row0 * arow;
-  S.asbase = p.hs + (size_t)row0 * (p.I / 32);
+  S2Tile<FA> c;
+  c.row0 = row0;
+  c.nrows = nrows;
+  c.nc0 = nt * TBN;  // first output column of the tile
+  c.S.abase = p.hq + (size_t)row0 * arow;
+  c.S.asbase = p.hs + (size_t)row0 * (p.I / 32);
 #pragma unroll
   for (int i = 0; i < Lo::kAInstr; ++i) {
-    int r, c;
-    t_aslot<FA>(Lo::kAInstr * w + i, lane, &r, &c);
-    S.a[i] = (uint32_t)((r < nrows ? r : 0) * arow + 16 * c);
+    int r, ch;
+    t_aslot<FA>(Lo::kAInstr * w + i, lane, &r, &ch);
+    c.S.a[i] = (uint32_t)((r < nrows ? r : 0) * arow + 16 * ch);
   }
-  const size_t wr0 = (size_t)e * p.H + nc0;  // first weight row of the tile
-  S.bbase = p.w2 + wr0 * (p.I / 2);
-  S.bsbase = p.w2s + wr0 * (p.I / 32);
+  const size_t wr0 = (size_t)e * p.H + c.nc0;  // first weight row of the tile
+  c.S.bbase = p.w2 + wr0 * (p.I / 2);
+  c.S.bsbase = p.w2s + wr0 * (p.I / 32);
 #pragma unroll
   for (int i = 0; i < Lo::kBInstr; ++i) {
-    int r, c;
-    t_bslot(Lo::kBInstr * w + i, lane, &r, &c);
-    S.b[i] = (uint32_t)(r * (p.I / 2) + 16 * c);
+    int r, ch;
+    t_bslot(Lo::kBInstr * w + i, lane, &r, &ch);
+    c.S.b[i] = (uint32_t)(r * (p.I / 2) + 16 * ch);
   }
-  {
-    const int ra = 64 * w + lane;
-    S.as = (uint32_t)((ra < nrows ? ra : 0) * (p.I / 32));
-    S.bs = (uint32_t)((64 * w + lane) * (p.I / 32));
-  }
-  const TLane L = t_lane<FA, 2>(w, lane);
-  const int nmb = __builtin_amdgcn_readfirstlane(min(4, max(0, (nrows - 128 * wm + 31) / 32)));
-  v16f acc[4][4];
-#pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = v16f{};
-  t_kloop<FA, 2>(lds, S, L, p.I / 128, w, nmb, acc);
+  const int ra = 64 * w + lane;
+  c.S.as = (uint32_t)((ra < nrows ? ra : 0) * (p.I / 32));
+  c.S.bs = (uint32_t)((64 * w + lane) * (p.I / 32));
+  return c;
+}
 
-  // Epilogue: fp32 partial rows to their unique assignment slots.
-  tbarrier();
-  int* sidx = reinterpret_cast<int*>(lds);
-  sidx[threadIdx.x] = (int)threadIdx.x < nrows ? p.sorted[row0 + threadIdx.x] : 0;
-  __syncthreads();
-  const int r = lane & 31, g = lane >> 5;
+// Persistent stage-2 kernel. Per tile: K loop; then the next tile's first
+// DMA stages go out before this tile's epilogue (fp32 partial rows to their
+// unique assignment slots), so the epilogue's stores cover their latency.
+// The epilogue only uses the second scale buffer (assignment slots of the
+// tile's rows, and the ticket word), which no prologue writes.
+template <int FA>
+__global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
+  using Lo = TL<FA>;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  int* sidx = reinterpret_cast<int*>(lds + Lo::kS + Lo::kSBuf);
+  int* slot = reinterpret_cast<int*>(lds + Lo::kS + Lo::kSBuf + TBM * 16);
+  const int per = 2 * p.t.n_ntiles, nch = *p.t.nchunks;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int wm = w & 1, wn = w >> 1;
+  int4 tile;
+  int nt;
+  bool have = t_next(p.t, slot, nch, per, &tile, &nt);
+  if (have) {
+    int lane = threadIdx.x % kWave;
+    asm volatile("" : "+v"(lane));
+    t_prologue<FA>(lds, s2_setup<FA>(p, tile, nt, w, lane).S, w);
+  }
+  while (have) {
+    // lane-derived offsets are recomputed per tile rather than held in
+    // registers across the persistent loop (the opaque copy blocks hoisting)
+    int lane = threadIdx.x % kWave;
+    asm volatile("" : "+v"(lane));
+    const S2Tile<FA> c = s2_setup<FA>(p, tile, nt, w, lane);
+    const TLane L = t_lane<FA, 2>(w, lane);
+    const int nrows = c.nrows;
+    const int nmb = __builtin_amdgcn_readfirstlane(min(4, max(0, (nrows - 128 * wm + 31) / 32)));
+    v16f acc[4][4];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) {
-    if (mb < nmb) {
+    for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int row = 128 * wm + 32 * mb + 8 * (i / 4) + 4 * g + (i % 4);
-        if (row < nrows) {
-          float* dst = p.partials + (size_t)sidx[row] * p.H + nc0 + 128 * wn + r;
+      for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = v16f{};
+    t_kloop<FA, 2, false>(lds, c.S, L, p.I / 128, w, nmb, acc);
+
+    const int sv = (int)threadIdx.x < nrows ? p.sorted[c.row0 + threadIdx.x] : 0;
+    int4 tile2;
+    int nt2;
+    have = t_next(p.t, slot, nch, per, &tile2, &nt2);
+    sidx[threadIdx.x] = sv;
+    if (have) t_prologue<FA>(lds, s2_setup<FA>(p, tile2, nt2, w, lane).S, w);
+    t_sync_lds();
+
+    const int r = lane & 31, g = lane >> 5;
 #pragma unroll
-          for (int nb = 0; nb < 4; ++nb) dst[32 * nb] = acc[mb][nb][i];
+    for (int mb = 0; mb < 4; ++mb) {
+      if (mb < nmb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int row = 128 * wm + 32 * mb + 8 * (i / 4) + 4 * g + (i % 4);
+          if (row < nrows) {
+            float* dst = p.partials + (size_t)sidx[row] * p.H + c.nc0 + 128 * wn + r;
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb) dst[32 * nb] = acc[mb][nb][i];
+          }
         }
       }
     }
+    tile = tile2;
+    nt = nt2;
   }
+  if (threadIdx.x == 0) t_finish(p.t);
 }
 
+// Persistent stage-1 kernel. The ticket word lies in the second scale
+// buffer (past its activation scales), which the K loop first writes after
+// the barrier of its first step.
 template <int FA>
 __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
+  using Lo = TL<FA>;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  t_persist<FA>(p.t, lds, [&](int4 tile, int nt) { s1_tile<FA>(p, lds, tile, nt); });
+  int* slot = reinterpret_cast<int*>(lds + Lo::kS + Lo::kSBuf + TBM * 16);
+  const int per = 2 * p.t.n_ntiles, nch = *p.t.nchunks;
+  int4 tile;
+  int nt;
+  while (t_next(p.t, slot, nch, per, &tile, &nt)) s1_tile<FA>(p, lds, tile, nt);
+  if (threadIdx.x == 0) t_finish(p.t);
 }
 
-template <int FA>
-__global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  t_persist<FA>(p.t, lds, [&](int4 tile, int nt) { s2_tile<FA>(p, lds, tile, nt); });
-}
 
 int tiled_rows() { return TBM; }
 
