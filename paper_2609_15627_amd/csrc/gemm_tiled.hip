@@ -73,6 +73,19 @@ __device__ __forceinline__ void tdma16(const void* g, uint8_t* l) {
   __builtin_amdgcn_global_load_lds(g, (lds_ptr_t*)l, 16, 0, 0);
 }
 
+// The same 16-byte-per-lane DMA as tdma16 (global `base` + 32-bit lane
+// offset `voff`, LDS destination `l` for lane 0), written out so that the
+// compiler neither orders LDS reads behind it nor waits for it: its
+// completion is covered only by the explicit vmcnt waits of the K loop,
+// followed by a workgroup barrier, before any wave reads the bytes it wrote.
+__device__ __forceinline__ void tdma16_x(const uint8_t* base, uint32_t voff, const uint8_t* l) {
+  const uint32_t m = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)l;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(m), "v"(voff), "s"(base)
+               : "m0");
+}
+
 template <int N>
 __device__ __forceinline__ void tvmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -282,21 +295,77 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   else if constexpr (kWait == 0) tvmcnt<0>();
   tbarrier();
   __builtin_amdgcn_sched_barrier(0);
+  // Second half, in explicit order: after each remaining sub-step-1 product
+  // its share of the next step's LDS reads (front-loaded, two per product)
+  // and of the DMA instructions (spread over all products).
   uint32_t ra[4], rb[4];
-  if constexpr (kNext) {
-    const int k1 = k + 1;
-    t_read_scales<ST, NMB>(lds + Lo::kS + ((k1 / kSG) & 1) * Lo::kSBuf, L, (J + 1) % kSG, ra, rb);
-    t_read_ops<FA, ST, 0, NMB>(lds + (k1 % kNStage) * Lo::kStage, L, X);
-  }
-  if constexpr (kIssue) {
-    if constexpr (kScales) t_issue_scales<FA>(lds, src, w, k / kSG + 1);
-    t_issue_stage<FA>(lds, src, w, k + kNStage);
-  }
-  t_mma<FA, 1, 1, NMB>(acc, Y, sa, sb);
+  v4u blo[4], alo[4], ahi[4];
+  const int k1 = k + 1;
+  const uint8_t* sbuf1 = lds + Lo::kS + ((k1 / kSG) & 1) * Lo::kSBuf;
+  const uint8_t* st1 = lds + (k1 % kNStage) * Lo::kStage;
+  uint8_t* dst = lds + (k % kNStage) * Lo::kStage;  // stage k + 3 reuses slot k % 3
+  const size_t ka = (size_t)(k + kNStage) * Lo::kARow, kb = (size_t)(k + kNStage) * 64;
+  uint8_t* sdst = lds + Lo::kS + ((k / kSG + 1) & 1) * Lo::kSBuf;
+  constexpr int kR = kNext ? kOpReads + kScaleReads : 0;
+  constexpr int kDS = kScales ? Lo::kScaleLoads : 0;
+  constexpr int kD = kIssue ? Lo::kStageLoads + kDS : 0;
   constexpr int kM = NMB > 1 ? 4 * (NMB - 1) : 0;
-  t_sched_b<kM, kNext ? kOpReads + kScaleReads : 0,
-            kIssue ? Lo::kStageLoads + (kScales ? Lo::kScaleLoads : 0) : 0>();
-  __builtin_amdgcn_sched_barrier(0);
+  constexpr int kRPer = kM > 0 ? (t_ceil(kR, kM) > 2 ? t_ceil(kR, kM) : 2) : kR;
+  auto read_one = [&](int r) {
+    if (r < NMB) {
+      ra[r] = *reinterpret_cast<const uint16_t*>(sbuf1 + L.as + r * 32 * 16 + 4 * ((J + 1) % kSG));
+    } else if (r < NMB + 4) {
+      const int nb = r - NMB;
+      rb[nb] = *reinterpret_cast<const uint16_t*>(sbuf1 + L.bs + t_nrow<ST>(nb) * 16 + 4 * ((J + 1) % kSG));
+    } else if (r < NMB + 8) {
+      const int nb = r - NMB - 4;
+      blo[nb] = *reinterpret_cast<const v4u*>(st1 + L.b[0] + t_nrow<ST>(nb) * 64);
+    } else {
+      const int q = r - NMB - 8, mb = q / kAPieces;
+      if (q % kAPieces == 0) alo[mb] = *reinterpret_cast<const v4u*>(st1 + L.a0[0] + mb * 32 * Lo::kARow);
+      else ahi[mb] = *reinterpret_cast<const v4u*>(st1 + L.a1[0] + mb * 32 * Lo::kARow);
+    }
+  };
+  auto dma_one = [&](int d) {
+    if (d < kDS) {
+      const int q1 = k / kSG + 1;
+      if (d == 0) tdma16_x(src.asbase + 16 * q1, src.as, sdst + 1024 * w);
+      else tdma16_x(src.bsbase + 16 * q1, src.bs, sdst + TBM * 16 + 1024 * w);
+    } else if (d - kDS < Lo::kAInstr) {
+      const int i = d - kDS;
+      tdma16_x(src.abase + ka, src.a[i], dst + 1024 * (Lo::kAInstr * w + i));
+    } else {
+      const int i = d - kDS - Lo::kAInstr;
+      tdma16_x(src.bbase + kb, src.b[i], dst + Lo::kB + 1024 * (Lo::kBInstr * w + i));
+    }
+  };
+#pragma unroll
+  for (int i = 0; i < (kM > 0 ? kM : 1); ++i) {
+    if (kM > 0) {
+      const int f = 4 + i;  // flat product index: rows 1.. of sub-step 1
+      acc[f / 4][f % 4] = t_mfma<FA, 1>(Y.a[f / 4], Y.b[f % 4], acc[f / 4][f % 4], sa[f / 4], sb[f % 4]);
+    }
+    const int r0 = kM > 0 ? t_min(kR, i * kRPer) : 0, r1 = kM > 0 ? t_min(kR, (i + 1) * kRPer) : kR;
+#pragma unroll
+    for (int r = r0; r < r1; ++r) read_one(r);
+    const int d0 = kM > 0 ? i * kD / kM : 0, d1 = kM > 0 ? (i + 1) * kD / kM : kD;
+#pragma unroll
+    for (int d = d0; d < d1; ++d) dma_one(d);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if constexpr (kNext && NMB > 0) {
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+      X.b[nb] = v8i{(int)blo[nb].x, (int)blo[nb].y, (int)blo[nb].z, (int)blo[nb].w, 0, 0, 0, 0};
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+      if constexpr (FA == 0)
+        X.a[mb] = v8i{(int)alo[mb].x, (int)alo[mb].y, (int)alo[mb].z, (int)alo[mb].w,
+                      (int)ahi[mb].x, (int)ahi[mb].y, (int)ahi[mb].z, (int)ahi[mb].w};
+      else
+        X.a[mb] = v8i{(int)alo[mb].x, (int)alo[mb].y, (int)alo[mb].z, (int)alo[mb].w, 0, 0, 0, 0};
+    }
+  }
   if constexpr (kNext) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
