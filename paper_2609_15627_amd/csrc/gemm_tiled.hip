@@ -267,6 +267,12 @@ __device__ __forceinline__ void t_sched_b() {
 //      into slot k % 3 (at J == 0 also scale group q + 1, into the buffer
 //      group q - 1 used), interleaved with the remaining sub-step-1 products.
 // LAST marks the final group (k = nk - 4 + J), where the ring drains.
+#ifndef MOE_TILED_PRE
+#define MOE_TILED_PRE 2
+#endif
+// Sub-step-1 products issued before the barrier (they cover its wait).
+constexpr int kPre = MOE_TILED_PRE;
+
 template <int FA, int ST, int NMB, int J, bool LAST>
 __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const TLane& L,
                                        int k, int w, v16f (*acc)[4], TOps& X, TOps& Y,
@@ -281,6 +287,7 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   constexpr int kAPieces = FA == 0 ? 2 : 1;
   constexpr int kOpReads = NMB > 0 ? 4 + kAPieces * NMB : 0;
   constexpr int kScaleReads = NMB > 0 ? 4 + NMB : 0;
+  constexpr int kPreN = 4 * NMB < kPre ? 4 * NMB : kPre;  // sub-step-1 products before the barrier
   const uint8_t* st = lds + (k % kNStage) * Lo::kStage;
 
   __builtin_amdgcn_sched_barrier(0);
@@ -289,7 +296,9 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   t_sched<4 * NMB, t_ceil(kOpReads, 4 * NMB), 0>();
   __builtin_amdgcn_sched_barrier(0);
   tlgkm0();
-  t_mma<FA, 1, 0, NMB < 1 ? NMB : 1>(acc, Y, sa, sb);
+#pragma unroll
+  for (int f = 0; f < kPreN; ++f)
+    acc[f / 4][f % 4] = t_mfma<FA, 1>(Y.a[f / 4], Y.b[f % 4], acc[f / 4][f % 4], sa[f / 4], sb[f % 4]);
   if constexpr (kWait == 2) tvmcnt<Lo::kStageLoads + Lo::kScaleLoads>();
   else if constexpr (kWait == 1) tvmcnt<Lo::kStageLoads>();
   else if constexpr (kWait == 0) tvmcnt<0>();
@@ -309,7 +318,7 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   constexpr int kR = kNext ? kOpReads + kScaleReads : 0;
   constexpr int kDS = kScales ? Lo::kScaleLoads : 0;
   constexpr int kD = kIssue ? Lo::kStageLoads + kDS : 0;
-  constexpr int kM = NMB > 1 ? 4 * (NMB - 1) : 0;
+  constexpr int kM = 4 * NMB - kPreN;
   constexpr int kRPer = kM > 0 ? (t_ceil(kR, kM) > 2 ? t_ceil(kR, kM) : 2) : kR;
   auto read_one = [&](int r) {
     if (r < NMB) {
@@ -342,7 +351,7 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
 #pragma unroll
   for (int i = 0; i < (kM > 0 ? kM : 1); ++i) {
     if (kM > 0) {
-      const int f = 4 + i;  // flat product index: rows 1.. of sub-step 1
+      const int f = kPreN + i;  // flat product index (row-major) of sub-step 1
       acc[f / 4][f % 4] = t_mfma<FA, 1>(Y.a[f / 4], Y.b[f % 4], acc[f / 4][f % 4], sa[f / 4], sb[f % 4]);
     }
     const int r0 = kM > 0 ? t_min(kR, i * kRPer) : 0, r1 = kM > 0 ? t_min(kR, (i + 1) * kRPer) : kR;
