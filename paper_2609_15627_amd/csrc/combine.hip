@@ -2,13 +2,17 @@
 //
 // out[t, h] = bf16_rne(acc), acc = 0, acc = fmaf(w[t, j], P[t*k_total + j, h], acc)
 // for j = 0 .. k_total-1 in this order. One thread per 8 consecutive h:
-// two 16-byte loads per slot, one 16-byte store. No atomics, so the result is
-// the same bits on every run.
+// two 16-byte loads per slot (all slots in flight at once), one 16-byte
+// store. No atomics, so the result is the same bits on every run.
 #include "moe_dev.h"
 #include "moe_launch.h"
 
 namespace moe {
 
+// KT > 0: the slot count is known at compile time, so every slot's loads
+// are issued before the first multiply-add (the adds still run in slot
+// order); KT == 0: any slot count, one slot at a time.
+template <int KT>
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ P,
                                                       const float* __restrict__ w, int T, int H,
                                                       int kt, uint16_t* __restrict__ out) {
@@ -16,11 +20,9 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   const int h8 = H / 8;
   if (idx >= (long)T * h8) return;
   const int t = (int)(idx / h8), c = (int)(idx % h8);
+  if constexpr (KT > 0) kt = KT;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int j = 0; j < kt; ++j) {
-    const float wj = w[(size_t)t * kt + j];
-    const float4* src = reinterpret_cast<const float4*>(P + ((size_t)t * kt + j) * H) + 2 * c;
-    const float4 p0 = src[0], p1 = src[1];
+  auto add = [&](float wj, const float4& p0, const float4& p1) {
     acc[0] = fmaf(wj, p0.x, acc[0]);
     acc[1] = fmaf(wj, p0.y, acc[1]);
     acc[2] = fmaf(wj, p0.z, acc[2]);
@@ -29,6 +31,22 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
     acc[5] = fmaf(wj, p1.y, acc[5]);
     acc[6] = fmaf(wj, p1.z, acc[6]);
     acc[7] = fmaf(wj, p1.w, acc[7]);
+  };
+  const float4* src = reinterpret_cast<const float4*>(P + (size_t)t * kt * H) + 2 * c;
+  const size_t row4 = (size_t)H / 4;  // float4 per partial row
+  if constexpr (KT > 0) {
+    float4 p[KT][2];
+    float wv[KT];
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      p[j][0] = src[j * row4];
+      p[j][1] = src[j * row4 + 1];
+      wv[j] = w[(size_t)t * KT + j];
+    }
+#pragma unroll
+    for (int j = 0; j < KT; ++j) add(wv[j], p[j][0], p[j][1]);
+  } else {
+    for (int j = 0; j < kt; ++j) add(w[(size_t)t * kt + j], src[j * row4], src[j * row4 + 1]);
   }
   uint32_t o[4];
 #pragma unroll
@@ -40,8 +58,20 @@ hipError_t launch_combine(const float* partials, const float* w, int T, int H, i
                           uint16_t* out, hipStream_t s) {
   const long n = (long)T * (H / 8);
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(combine_kernel, dim3((int)((n + 255) / 256)), dim3(256), 0, s, partials, w, T,
-                     H, k_total, out);
+  const dim3 grid((int)((n + 255) / 256)), block(256);
+  switch (k_total) {
+#define MOE_COMBINE_KT(K)                                                                  \
+  case K:                                                                                  \
+    hipLaunchKernelGGL(combine_kernel<K>, grid, block, 0, s, partials, w, T, H, k_total, out); \
+    break;
+    MOE_COMBINE_KT(1) MOE_COMBINE_KT(2) MOE_COMBINE_KT(3) MOE_COMBINE_KT(4) MOE_COMBINE_KT(5)
+    MOE_COMBINE_KT(6) MOE_COMBINE_KT(7) MOE_COMBINE_KT(8) MOE_COMBINE_KT(9) MOE_COMBINE_KT(10)
+    MOE_COMBINE_KT(11) MOE_COMBINE_KT(12) MOE_COMBINE_KT(13) MOE_COMBINE_KT(14) MOE_COMBINE_KT(15)
+    MOE_COMBINE_KT(16)
+#undef MOE_COMBINE_KT
+    default:
+      hipLaunchKernelGGL(combine_kernel<0>, grid, block, 0, s, partials, w, T, H, k_total, out);
+  }
   return hipGetLastError();
 }
 
