@@ -48,7 +48,6 @@ constexpr int TBM = 256;       // sorted rows per tile
 constexpr int TBN = 256;       // weight rows per tile
 constexpr int kNStage = 3;     // K-step stages in the LDS ring
 constexpr int kSG = 4;         // K steps per scale group (16 scale bytes per row)
-constexpr int kHStride = 132;  // fp32 row stride of the stage-1 epilogue buffer
 
 template <int FA>
 struct TL {
@@ -66,18 +65,15 @@ struct TL {
 
 template <int FA>
 constexpr int t_lds_s1() {
-  return TL<FA>::kLoop > TBM * kHStride * 4 ? TL<FA>::kLoop : TBM * kHStride * 4;
+  return TL<FA>::kLoop;
 }
 
-__device__ __forceinline__ void tdma16(const void* g, uint8_t* l) {
-  __builtin_amdgcn_global_load_lds(g, (lds_ptr_t*)l, 16, 0, 0);
-}
-
-// The same 16-byte-per-lane DMA as tdma16 (global `base` + 32-bit lane
-// offset `voff`, LDS destination `l` for lane 0), written out so that the
-// compiler neither orders LDS reads behind it nor waits for it: its
-// completion is covered only by the explicit vmcnt waits of the K loop,
-// followed by a workgroup barrier, before any wave reads the bytes it wrote.
+// 16-byte-per-lane DMA global -> LDS (global `base` + 32-bit lane offset
+// `voff`, LDS destination `l` for lane 0, 1 KiB per instruction), written
+// out so that the compiler neither orders LDS accesses behind it nor waits
+// for it: its completion is covered only by the explicit vmcnt waits of the
+// K loop, each followed by a workgroup barrier, before any wave reads the
+// bytes it wrote.
 __device__ __forceinline__ void tdma16_x(const uint8_t* base, uint32_t voff, const uint8_t* l) {
   const uint32_t m = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)l;
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
@@ -134,18 +130,18 @@ __device__ __forceinline__ void t_issue_stage(uint8_t* lds, const TSrc<FA>& S, i
   const size_t ka = (size_t)k * L::kARow, kb = (size_t)k * 64;
 #pragma unroll
   for (int i = 0; i < L::kAInstr; ++i)
-    tdma16(S.abase + ka + S.a[i], st + 1024 * (L::kAInstr * w + i));
+    tdma16_x(S.abase + ka, S.a[i], st + 1024 * (L::kAInstr * w + i));
 #pragma unroll
   for (int i = 0; i < L::kBInstr; ++i)
-    tdma16(S.bbase + kb + S.b[i], st + L::kB + 1024 * (L::kBInstr * w + i));
+    tdma16_x(S.bbase + kb, S.b[i], st + L::kB + 1024 * (L::kBInstr * w + i));
 }
 
 template <int FA>
 __device__ __forceinline__ void t_issue_scales(uint8_t* lds, const TSrc<FA>& S, int w, int q) {
   using L = TL<FA>;
   uint8_t* sb = lds + L::kS + (q & 1) * L::kSBuf;
-  tdma16(S.asbase + 16 * q + S.as, sb + 1024 * w);
-  tdma16(S.bsbase + 16 * q + S.bs, sb + TBM * 16 + 1024 * w);
+  tdma16_x(S.asbase + 16 * q, S.as, sb + 1024 * w);
+  tdma16_x(S.bsbase + 16 * q, S.bs, sb + TBM * 16 + 1024 * w);
 }
 
 // Per-lane LDS byte offsets of the operand reads (block 0; block b adds a
@@ -209,22 +205,31 @@ __device__ __forceinline__ void t_read_scales(const uint8_t* sbuf, const TLane& 
   }
 }
 
-template <int FA, int OPS>
+// One 32x32x64 product of activation operand a (format FA) and weight
+// operand b (FP4), op_sel OPS picking the sub-step's scale byte. Stage 2
+// computes activations x weights (accumulator rows = activation rows);
+// stage 1 the transpose, weights x activations, so that a lane's
+// accumulator holds 16 h values of one token (rows = weight rows).
+template <int FA, int ST, int OPS>
 __device__ __forceinline__ v16f t_mfma(const v8i& a, const v8i& b, const v16f& c, uint32_t sa,
                                        uint32_t sb) {
-  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FA, 4, OPS, (int)sa, OPS,
-                                                         (int)sb);
+  if constexpr (ST == 1)
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b, a, c, 4, FA, OPS, (int)sb, OPS,
+                                                           (int)sa);
+  else
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FA, 4, OPS, (int)sa, OPS,
+                                                           (int)sb);
 }
 
 // Products of sub-step S for blocks (mb, nb) with mb in [MB0, MB1).
-template <int FA, int S, int MB0, int MB1>
+template <int FA, int ST, int S, int MB0, int MB1>
 __device__ __forceinline__ void t_mma(v16f (*acc)[4], const TOps& o, const uint32_t* sa,
                                       const uint32_t* sb) {
 #pragma unroll
   for (int mb = MB0; mb < MB1; ++mb)
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb)
-      acc[mb][nb] = t_mfma<FA, S>(o.a[mb], o.b[nb], acc[mb][nb], sa[mb], sb[nb]);
+      acc[mb][nb] = t_mfma<FA, ST, S>(o.a[mb], o.b[nb], acc[mb][nb], sa[mb], sb[nb]);
 }
 
 // Interleave hint: M single products, each followed by D LDS reads and V
@@ -292,13 +297,13 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
 
   __builtin_amdgcn_sched_barrier(0);
   t_read_ops<FA, ST, 1, NMB>(st, L, Y);
-  t_mma<FA, 0, 0, NMB>(acc, X, sa, sb);
+  t_mma<FA, ST, 0, 0, NMB>(acc, X, sa, sb);
   t_sched<4 * NMB, t_ceil(kOpReads, 4 * NMB), 0>();
   __builtin_amdgcn_sched_barrier(0);
   tlgkm0();
 #pragma unroll
   for (int f = 0; f < kPreN; ++f)
-    acc[f / 4][f % 4] = t_mfma<FA, 1>(Y.a[f / 4], Y.b[f % 4], acc[f / 4][f % 4], sa[f / 4], sb[f % 4]);
+    acc[f / 4][f % 4] = t_mfma<FA, ST, 1>(Y.a[f / 4], Y.b[f % 4], acc[f / 4][f % 4], sa[f / 4], sb[f % 4]);
   if constexpr (kWait == 2) tvmcnt<Lo::kStageLoads + Lo::kScaleLoads>();
   else if constexpr (kWait == 1) tvmcnt<Lo::kStageLoads>();
   else if constexpr (kWait == 0) tvmcnt<0>();
@@ -352,7 +357,7 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   for (int i = 0; i < (kM > 0 ? kM : 1); ++i) {
     if (kM > 0) {
       const int f = kPreN + i;  // flat product index (row-major) of sub-step 1
-      acc[f / 4][f % 4] = t_mfma<FA, 1>(Y.a[f / 4], Y.b[f % 4], acc[f / 4][f % 4], sa[f / 4], sb[f % 4]);
+      acc[f / 4][f % 4] = t_mfma<FA, ST, 1>(Y.a[f / 4], Y.b[f % 4], acc[f / 4][f % 4], sa[f / 4], sb[f % 4]);
     }
     const int r0 = kM > 0 ? t_min(kR, i * kRPer) : 0, r1 = kM > 0 ? t_min(kR, (i + 1) * kRPer) : kR;
 #pragma unroll
@@ -533,6 +538,49 @@ __device__ __forceinline__ TLane t_lane(int w, int lane) {
   return L;
 }
 
+// Stage-1 work item: DMA sources and shape of one tile.
+template <int FA>
+struct S1Tile {
+  TSrc<FA> S;
+  int row0, nrows, hc0;
+};
+
+template <int FA>
+__device__ __forceinline__ S1Tile<FA> s1_setup(const S1Args& p, int4 tile, int nt, int w, int lane) {
+  using Lo = TL<FA>;
+  const int e = tile.x, row0 = tile.y, nrows = tile.z;
+  const int hc0 = nt * (TBN / 2);  // first h column of the tile
+  const int xrow = (p.H / 32) * ActBytes<FA>::kBlock;
+  S1Tile<FA> c;
+  c.row0 = row0;
+  c.nrows = nrows;
+  c.hc0 = hc0;
+  c.S.abase = p.xq;
+  c.S.asbase = p.xs;
+#pragma unroll
+  for (int i = 0; i < Lo::kAInstr; ++i) {
+    int r, ch;
+    t_aslot<FA>(Lo::kAInstr * w + i, lane, &r, &ch);
+    const int tok = p.sorted[row0 + (r < nrows ? r : 0)] / p.k_total;
+    c.S.a[i] = (uint32_t)(tok * xrow + 16 * ch);
+  }
+  // weight row (within the expert) of tile row r: 128 gate rows, then the 128 up rows
+  auto wrow = [&](int r) { return r < TBN / 2 ? hc0 + r : p.I + hc0 + (r - TBN / 2); };
+  c.S.bbase = p.w13 + (size_t)e * 2 * p.I * (p.H / 2);
+  c.S.bsbase = p.w13s + (size_t)e * 2 * p.I * (p.H / 32);
+#pragma unroll
+  for (int i = 0; i < Lo::kBInstr; ++i) {
+    int r, ch;
+    t_bslot(Lo::kBInstr * w + i, lane, &r, &ch);
+    c.S.b[i] = (uint32_t)(wrow(r) * (p.H / 2) + 16 * ch);
+  }
+  const int ra = 64 * w + lane;
+  const int tok = p.sorted[row0 + (ra < nrows ? ra : 0)] / p.k_total;
+  c.S.as = (uint32_t)(tok * (p.H / 32));
+  c.S.bs = (uint32_t)(wrow(64 * w + lane) * (p.H / 32));
+  return c;
+}
+
 // SwiGLU h = G * U * sigmoid(G) with the hardware exp2 and reciprocal (about
 // one ulp each; G itself carries the much larger accumulation error).
 __device__ __forceinline__ float swiglu_fast(float G, float U) {
@@ -540,153 +588,78 @@ __device__ __forceinline__ float swiglu_fast(float G, float U) {
   return G * U * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
+// Value of lane l ^ 32 (the other half of the wave), by a VALU lane swap.
+__device__ __forceinline__ uint32_t t_xhalf(uint32_t x, int h) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return h ? r[0] : r[1];
+}
+
+// Stage-1 epilogue, in registers. The accumulators hold the transposed tile:
+// block (mb, nb), element i of lane l is weight row t_nrow(nb) + 8 (i / 4) +
+// 4 h + i % 4 (h = l / 32) of the wave, token column 32 mb + l % 32. Gate
+// block q and up block q + 2 cover the same 32 h columns, so the 32 values
+// of one token's quantisation block are lane l's 16 and lane (l ^ 32)'s 16:
+// the block maximum takes one exchange, and two more assemble each lane's
+// contiguous half of the block's codes for one 16-byte (FP8) or 8-byte
+// (FP4) store per token row.
 template <int FA>
-__device__ __forceinline__ void s1_tile(const S1Args& p, uint8_t* lds, int4 tile, int nt) {
-  using Lo = TL<FA>;
-  const int e = tile.x, row0 = tile.y, nrows = tile.z;
-  // lane-derived offsets are recomputed per tile rather than held in
-  // registers across the persistent loop (the opaque copy blocks hoisting)
-  int lane = threadIdx.x % kWave;
-  asm volatile("" : "+v"(lane));
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int wm = w & 1, wn = w >> 1;
-  const int hc0 = nt * (TBN / 2);  // first h column of the tile
-  const int xrow = (p.H / 32) * ActBytes<FA>::kBlock;
-
-  TSrc<FA> S;
-  S.abase = p.xq;
-  S.asbase = p.xs;
-#pragma unroll
-  for (int i = 0; i < Lo::kAInstr; ++i) {
-    int r, c;
-    t_aslot<FA>(Lo::kAInstr * w + i, lane, &r, &c);
-    const int tok = p.sorted[row0 + (r < nrows ? r : 0)] / p.k_total;
-    S.a[i] = (uint32_t)(tok * xrow + 16 * c);
-  }
-  // weight row (within the expert) of tile row r: 128 gate rows, then the 128 up rows
-  auto wrow = [&](int r) { return r < TBN / 2 ? hc0 + r : p.I + hc0 + (r - TBN / 2); };
-  S.bbase = p.w13 + (size_t)e * 2 * p.I * (p.H / 2);
-  S.bsbase = p.w13s + (size_t)e * 2 * p.I * (p.H / 32);
-#pragma unroll
-  for (int i = 0; i < Lo::kBInstr; ++i) {
-    int r, c;
-    t_bslot(Lo::kBInstr * w + i, lane, &r, &c);
-    S.b[i] = (uint32_t)(wrow(r) * (p.H / 2) + 16 * c);
-  }
-  {
-    const int ra = 64 * w + lane;
-    const int tok = p.sorted[row0 + (ra < nrows ? ra : 0)] / p.k_total;
-    S.as = (uint32_t)(tok * (p.H / 32));
-    S.bs = (uint32_t)(wrow(64 * w + lane) * (p.H / 32));
-  }
-  const TLane L = t_lane<FA, 1>(w, lane);
-  const int nmb = __builtin_amdgcn_readfirstlane(min(4, max(0, (nrows - 128 * wm + 31) / 32)));
-  v16f acc[4][4];
-#pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = v16f{};
-  t_kloop<FA, 1, true>(lds, S, L, p.H / 128, w, nmb, acc);
-
-  // Epilogue, through LDS:
-  //  1. each lane writes its SwiGLU values h as fp32 rows [256][kHStride];
-  //  2. one thread per tile row quantises the row's four 32-column blocks in
-  //     registers (no cross-lane reductions) and writes the codes back over
-  //     the row's first bytes, its four scale bytes after them (a stride of
-  //     132 floats keeps these row-per-lane reads conflict-free);
-  //  3. all threads store the code rows with whole-row 16-byte pieces.
-  tbarrier();
-  float* hb = reinterpret_cast<float*>(lds);
-  const int r = lane & 31, g = lane >> 5;
+__device__ __forceinline__ void s1_epilogue(const S1Args& p, v16f (*acc)[4], int row0, int nrows,
+                                            int hc0, int wm, int wn, int lane, int nmb) {
+  constexpr int kCB = FA == 0 ? 32 : 16;  // code bytes per 32-element block
+  const int r = lane & 31, h = lane >> 5;
+  const size_t crow = (size_t)(p.I / 32) * kCB;  // code bytes per hq row
+  const int blk0 = (hc0 + 64 * wn) / 32;         // the wave's two h blocks
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) {
     if (mb < nmb) {
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const int col = 64 * wn + 32 * q + r;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int row = 128 * wm + 32 * mb + 8 * (i / 4) + 4 * g + (i % 4);
-          const float G = acc[mb][q][i], U = acc[mb][2 + q][i];
-          hb[row * kHStride + col] = swiglu_fast(G, U);
-        }
-      }
-    }
-  }
-  __syncthreads();
-  constexpr int kCB = FA == 0 ? 32 : 16;  // code bytes per 32-element block
-  {
-    const int row = threadIdx.x;
-    if (row < nrows) {
-      float* hr = hb + row * kHStride;
-      uint8_t* cr = reinterpret_cast<uint8_t*>(hr);
+      const int tr = 128 * wm + 32 * mb + r;  // token row within the tile
+      uint8_t* crow_p = p.hq + ((size_t)row0 + tr) * crow;
       uint32_t sc = 0;
 #pragma unroll
-      for (int qb = 0; qb < 4; ++qb) {
-        float v[32];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const float4 t = reinterpret_cast<const float4*>(hr + 32 * qb)[i];
-          v[4 * i] = t.x;
-          v[4 * i + 1] = t.y;
-          v[4 * i + 2] = t.z;
-          v[4 * i + 3] = t.w;
-        }
+      for (int q = 0; q < 2; ++q) {
+        float hv[16];
         float m = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 32; ++i) m = fmaxf(m, fabsf(v[i]));
-        const int X = mx_scale_exp<FA>(m);
-        sc |= (uint32_t)(X + 127) << (8 * qb);
-        // block qb's codes land in bytes [kCB qb, +kCB) of the row, which
-        // only ever overlap values this thread has already read
-        if constexpr (FA == 0) {
-          uint4* dst = reinterpret_cast<uint4*>(cr + kCB * qb);
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            uint32_t wd[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int e = 16 * h + 4 * i;
-              wd[i] = e4m3_pack4(ldexpf(v[e], -X), ldexpf(v[e + 1], -X), ldexpf(v[e + 2], -X),
-                                 ldexpf(v[e + 3], -X));
-            }
-            dst[h] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
-          }
-        } else {
-          uint32_t wd[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            uint32_t q = 0;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) q |= mx_encode<FA>(ldexpf(v[8 * i + j], -X)) << (4 * j);
-            wd[i] = q;
-          }
-          *reinterpret_cast<uint4*>(cr + kCB * qb) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+        for (int i = 0; i < 16; ++i) {
+          hv[i] = swiglu_fast(acc[mb][q][i], acc[mb][q + 2][i]);
+          m = fmaxf(m, fabsf(hv[i]));
         }
-      }
-      *reinterpret_cast<uint32_t*>(cr + 4 * kCB) = sc;
-    }
-  }
-  __syncthreads();
-  {
-    constexpr int kPieces = 4 * kCB / 16;  // 16-byte pieces of a row's codes
-    const size_t crow = (size_t)(p.I / 32) * kCB;  // code bytes per hq row
+        m = fmaxf(m, __uint_as_float(t_xhalf(__float_as_uint(m), h)));
+        const int X = mx_scale_exp<FA>(m);
+        sc |= (uint32_t)(X + 127) << (8 * q);
+        // d[k]: positions 8k + 4h .. +3 of the block (four consecutive h columns)
+        uint32_t d[4];
 #pragma unroll
-    for (int it = 0; it < TBM * kPieces / 256; ++it) {
-      const int task = threadIdx.x + 256 * it;
-      const int row = task / kPieces, pc = task % kPieces;
-      if (row < nrows) {
-        const uint8_t* cr = reinterpret_cast<const uint8_t*>(hb + row * kHStride);
-        const uint4 v = *reinterpret_cast<const uint4*>(cr + 16 * pc);
-        *reinterpret_cast<uint4*>(p.hq + ((size_t)row0 + row) * crow + (hc0 / 32) * kCB +
-                                  16 * pc) = v;
+        for (int k = 0; k < 4; ++k) {
+          if constexpr (FA == 0) {
+            d[k] = e4m3_pack4(ldexpf(hv[4 * k], -X), ldexpf(hv[4 * k + 1], -X),
+                              ldexpf(hv[4 * k + 2], -X), ldexpf(hv[4 * k + 3], -X));
+          } else {
+            uint32_t v = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v |= mx_encode<FA>(ldexpf(hv[4 * k + j], -X)) << (4 * j);
+            d[k] = v;
+          }
+        }
+        // lane h = 0 keeps block positions 0-15, lane h = 1 positions 16-31
+        const uint32_t s0 = h ? d[0] : d[2], s1 = h ? d[1] : d[3];
+        const uint32_t r0 = t_xhalf(s0, h), r1 = t_xhalf(s1, h);
+        if (tr < nrows) {
+          if constexpr (FA == 0) {
+            const uint4 v = h ? make_uint4(r0, d[2], r1, d[3]) : make_uint4(d[0], r0, d[1], r1);
+            *reinterpret_cast<uint4*>(crow_p + (blk0 + q) * kCB + 16 * h) = v;
+          } else {
+            const uint2 v = h ? make_uint2(r0 | (d[2] << 16), r1 | (d[3] << 16))
+                              : make_uint2(d[0] | (r0 << 16), d[1] | (r1 << 16));
+            *reinterpret_cast<uint2*>(crow_p + (blk0 + q) * kCB + 8 * h) = v;
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);  // one block at a time: bounded live ranges
       }
+      if (h == 0 && tr < nrows)
+        *reinterpret_cast<uint16_t*>(p.hs + ((size_t)row0 + tr) * (p.I / 32) + blk0) =
+            (uint16_t)sc;
     }
-    const int row = threadIdx.x;
-    if (row < nrows)
-      *reinterpret_cast<uint32_t*>(p.hs + ((size_t)row0 + row) * (p.I / 32) + hc0 / 32) =
-          *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(
-                                                 hb + row * kHStride) + 4 * kCB);
   }
 }
 
@@ -796,21 +769,52 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
   if (threadIdx.x == 0) t_finish(p.t);
 }
 
-// Persistent stage-1 kernel. The ticket word lies in the second scale
-// buffer (past its activation scales), which the K loop first writes after
-// the barrier of its first step.
+// Persistent stage-1 kernel. Per tile: K loop; then the next tile's first
+// DMA stages go out before this tile's epilogue, which works in registers
+// only. The ticket word lies in the second scale buffer (past its activation
+// scales), which no prologue writes.
 template <int FA>
 __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
   using Lo = TL<FA>;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   int* slot = reinterpret_cast<int*>(lds + Lo::kS + Lo::kSBuf + TBM * 16);
   const int per = 2 * p.t.n_ntiles, nch = *p.t.nchunks;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int wm = w & 1, wn = w >> 1;
+  int lane = threadIdx.x % kWave;
   int4 tile;
   int nt;
-  while (t_next(p.t, slot, nch, per, &tile, &nt)) s1_tile<FA>(p, lds, tile, nt);
+  bool have = t_next(p.t, slot, nch, per, &tile, &nt);
+  S1Tile<FA> c;
+  if (have) {
+    c = s1_setup<FA>(p, tile, nt, w, lane);
+    t_prologue<FA>(lds, c.S, w);
+  }
+  while (have) {
+    // lane-derived offsets are recomputed per tile rather than held in
+    // registers across the persistent loop (the opaque copy blocks hoisting)
+    asm volatile("" : "+v"(lane));
+    const TLane L = t_lane<FA, 1>(w, lane);
+    const int nmb = __builtin_amdgcn_readfirstlane(min(4, max(0, (c.nrows - 128 * wm + 31) / 32)));
+    v16f acc[4][4];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = v16f{};
+    t_kloop<FA, 1, false>(lds, c.S, L, p.H / 128, w, nmb, acc);
+
+    int4 tile2;
+    int nt2;
+    have = t_next(p.t, slot, nch, per, &tile2, &nt2);
+    const int row0 = c.row0, nrows = c.nrows, hc0 = c.hc0;
+    if (have) {
+      c = s1_setup<FA>(p, tile2, nt2, w, lane);
+      t_prologue<FA>(lds, c.S, w);
+    }
+    s1_epilogue<FA>(p, acc, row0, nrows, hc0, wm, wn, lane, nmb);
+  }
   if (threadIdx.x == 0) t_finish(p.t);
 }
-
 
 int tiled_rows() { return TBM; }
 
