@@ -10,18 +10,18 @@
 // Data movement, chosen from measurements on gfx950:
 //  - operands travel global -> LDS by DMA (global_load_lds, 16 bytes a lane,
 //    1 KiB of contiguous LDS per instruction) through a ring of three K-step
-//    stages; a load instruction costs about the same per distinct cache line
-//    it touches, so every instruction reads whole 64- or 128-byte row
-//    segments;
+//    stages; every instruction reads whole 64- or 128-byte row segments;
 //  - E8M0 scales move in 16-byte row pieces covering four K steps (a
 //    separate ring of two scale groups), not one word per row per step: a
 //    4-byte gather costs a cache line per lane;
 //  - LDS rows are chunk-swizzled (16-byte chunk c of row r stored at
 //    c ^ f(r)) so the operand reads of the 32x32x64 layout run at full LDS
 //    rate;
-//  - each wave reads the next sub-step's operands from LDS while the matrix
-//    cores work on the current one (two register sets), with one workgroup
-//    barrier per K step.
+//  - matrix-core time is lost to load issue in bursts, not to spread-out
+//    issue: each wave reads the next sub-step's operands one read per
+//    product, and after the step's one workgroup barrier interleaves the
+//    next step's reads (two per product) and DMA instructions with the
+//    remaining products in explicit program order.
 //
 // K order inside a step: the products only need A and B to agree on which
 // physical K elements a lane's bytes stand for. Sub-step s, lane half h takes
@@ -30,12 +30,17 @@
 // 16-bit LDS read per row and step, op_sel s picks the byte.
 //
 // Matrix-core operand layout (32x32x64, measured): lane l supplies row l % 32
-// of A and column l % 32 of B. An FP4 lane holds K elements [32 h, 32 h + 32)
-// of the 64 (h = l / 32), two per byte, low nibble first; an FP8 lane holds
-// K [16 h, 16 h + 16) in bytes 0-15 and K [32 + 16 h, +16) in bytes 16-31.
-// The lane's scale register carries the scale of 32-element K block h in the
-// byte selected by the instruction's op_sel. D: lane l, element i holds row
-// 8 (i / 4) + 4 h + i % 4, column l % 32.
+// of the row operand and column l % 32 of the column operand. An FP4 lane
+// holds K elements [32 h, 32 h + 32) of the 64 (h = l / 32), two per byte,
+// low nibble first; an FP8 lane holds K [16 h, 16 h + 16) in bytes 0-15 and
+// K [32 + 16 h, +16) in bytes 16-31. The lane's scale register carries the
+// scale of 32-element K block h in the byte selected by the instruction's
+// op_sel. D: lane l, element i holds row 8 (i / 4) + 4 h + i % 4, column
+// l % 32.
+//
+// Both kernels are persistent (one workgroup per CU) and take work items
+// from per-XCD queues; the next tile's first DMA stages go out before the
+// current tile's epilogue.
 #include "gemm_common.h"
 #include "gemm_launch.h"
 
