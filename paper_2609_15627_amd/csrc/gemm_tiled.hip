@@ -128,24 +128,37 @@ __device__ __forceinline__ void t_bslot(int ci, int lane, int* row, int* chunk) 
   *chunk = (lane % 4) ^ ((*row >> 2) & 3);
 }
 
+// Activation rows a wave moves by DMA: the 64 rows from t_arow0(w), inside
+// the 128 rows the wave multiplies (rows 128 (w & 1) ..), so a wave without
+// rows to multiply (a tile of at most 128 rows, w odd) moves no activation
+// data either. Its DMA instruction i fills activation tile chunk t_aci.
+__device__ __forceinline__ int t_arow0(int w) { return 128 * (w & 1) + 64 * (w >> 1); }
 template <int FA>
+__device__ __forceinline__ int t_aci(int w, int i) {
+  return t_arow0(w) * TL<FA>::kARow / 1024 + i;
+}
+
+// DMA of stage k; AON: this wave moves activation rows (else only weights).
+template <int FA, bool AON>
 __device__ __forceinline__ void t_issue_stage(uint8_t* lds, const TSrc<FA>& S, int w, int k) {
   using L = TL<FA>;
   uint8_t* st = lds + (k % kNStage) * L::kStage;
   const size_t ka = (size_t)k * L::kARow, kb = (size_t)k * 64;
+  if constexpr (AON) {
 #pragma unroll
-  for (int i = 0; i < L::kAInstr; ++i)
-    tdma16_x(S.abase + ka, S.a[i], st + 1024 * (L::kAInstr * w + i));
+    for (int i = 0; i < L::kAInstr; ++i)
+      tdma16_x(S.abase + ka, S.a[i], st + 1024 * t_aci<FA>(w, i));
+  }
 #pragma unroll
   for (int i = 0; i < L::kBInstr; ++i)
     tdma16_x(S.bbase + kb, S.b[i], st + L::kB + 1024 * (L::kBInstr * w + i));
 }
 
-template <int FA>
+template <int FA, bool AON>
 __device__ __forceinline__ void t_issue_scales(uint8_t* lds, const TSrc<FA>& S, int w, int q) {
   using L = TL<FA>;
   uint8_t* sb = lds + L::kS + (q & 1) * L::kSBuf;
-  tdma16_x(S.asbase + 16 * q, S.as, sb + 1024 * w);
+  if constexpr (AON) tdma16_x(S.asbase + 16 * q, S.as, sb + 16 * t_arow0(w));
   tdma16_x(S.bsbase + 16 * q, S.bs, sb + TBM * 16 + 1024 * w);
 }
 
@@ -298,6 +311,9 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   constexpr int kOpReads = NMB > 0 ? 4 + kAPieces * NMB : 0;
   constexpr int kScaleReads = NMB > 0 ? 4 + NMB : 0;
   constexpr int kPreN = 4 * NMB < kPre ? 4 * NMB : kPre;  // sub-step-1 products before the barrier
+  constexpr bool kAOn = NMB > 0;  // this wave moves activation rows
+  constexpr int kStageLoads = (kAOn ? Lo::kAInstr : 0) + Lo::kBInstr;
+  constexpr int kScaleLoads = kAOn ? 2 : 1;
   const uint8_t* st = lds + (k % kNStage) * Lo::kStage;
 
   __builtin_amdgcn_sched_barrier(0);
@@ -309,8 +325,8 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
 #pragma unroll
   for (int f = 0; f < kPreN; ++f)
     acc[f / 4][f % 4] = t_mfma<FA, ST, 1>(Y.a[f / 4], Y.b[f % 4], acc[f / 4][f % 4], sa[f / 4], sb[f % 4]);
-  if constexpr (kWait == 2) tvmcnt<Lo::kStageLoads + Lo::kScaleLoads>();
-  else if constexpr (kWait == 1) tvmcnt<Lo::kStageLoads>();
+  if constexpr (kWait == 2) tvmcnt<kStageLoads + kScaleLoads>();
+  else if constexpr (kWait == 1) tvmcnt<kStageLoads>();
   else if constexpr (kWait == 0) tvmcnt<0>();
   tbarrier();
   __builtin_amdgcn_sched_barrier(0);
@@ -326,8 +342,9 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   const size_t ka = (size_t)(k + kNStage) * Lo::kARow, kb = (size_t)(k + kNStage) * 64;
   uint8_t* sdst = lds + Lo::kS + ((k / kSG + 1) & 1) * Lo::kSBuf;
   constexpr int kR = kNext ? kOpReads + kScaleReads : 0;
-  constexpr int kDS = kScales ? Lo::kScaleLoads : 0;
-  constexpr int kD = kIssue ? Lo::kStageLoads + kDS : 0;
+  constexpr int kDS = kScales ? kScaleLoads : 0;
+  constexpr int kD = kIssue ? kStageLoads + kDS : 0;
+  constexpr int kDA = kAOn ? Lo::kAInstr : 0;
   constexpr int kM = 4 * NMB - kPreN;
   constexpr int kRPer = kM > 0 ? (t_ceil(kR, kM) > 2 ? t_ceil(kR, kM) : 2) : kR;
   auto read_one = [&](int r) {
@@ -348,13 +365,13 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   auto dma_one = [&](int d) {
     if (d < kDS) {
       const int q1 = k / kSG + 1;
-      if (d == 0) tdma16_x(src.asbase + 16 * q1, src.as, sdst + 1024 * w);
+      if (kAOn && d == 0) tdma16_x(src.asbase + 16 * q1, src.as, sdst + 16 * t_arow0(w));
       else tdma16_x(src.bsbase + 16 * q1, src.bs, sdst + TBM * 16 + 1024 * w);
-    } else if (d - kDS < Lo::kAInstr) {
+    } else if (d - kDS < kDA) {
       const int i = d - kDS;
-      tdma16_x(src.abase + ka, src.a[i], dst + 1024 * (Lo::kAInstr * w + i));
+      tdma16_x(src.abase + ka, src.a[i], dst + 1024 * t_aci<FA>(w, i));
     } else {
-      const int i = d - kDS - Lo::kAInstr;
+      const int i = d - kDS - kDA;
       tdma16_x(src.bbase + kb, src.b[i], dst + Lo::kB + 1024 * (Lo::kBInstr * w + i));
     }
   };
@@ -406,11 +423,18 @@ __device__ __forceinline__ void t_group(uint8_t* lds, const TSrc<FA>& src, const
 
 // The K loop shared by both stages: nk = K / 128 steps, a multiple of 4.
 // Scale group 0 and stages 0-2 are in flight before the first step.
-template <int FA>
-__device__ __forceinline__ void t_prologue(uint8_t* lds, const TSrc<FA>& src, int w) {
-  t_issue_scales<FA>(lds, src, w, 0);
+template <int FA, bool AON>
+__device__ __forceinline__ void t_prologue_n(uint8_t* lds, const TSrc<FA>& src, int w) {
+  t_issue_scales<FA, AON>(lds, src, w, 0);
 #pragma unroll
-  for (int s = 0; s < kNStage; ++s) t_issue_stage<FA>(lds, src, w, s);
+  for (int s = 0; s < kNStage; ++s) t_issue_stage<FA, AON>(lds, src, w, s);
+}
+
+// nmb: the row blocks this wave will multiply in the tile.
+template <int FA>
+__device__ __forceinline__ void t_prologue(uint8_t* lds, const TSrc<FA>& src, int w, int nmb) {
+  if (nmb > 0) t_prologue_n<FA, true>(lds, src, w);
+  else t_prologue_n<FA, false>(lds, src, w);
 }
 
 // PRO: issue the prologue here (else the caller issued it earlier; loads or
@@ -420,8 +444,8 @@ template <int FA, int ST, int NMB, bool PRO>
 __device__ __forceinline__ void t_kloop_n(uint8_t* lds, const TSrc<FA>& src, const TLane& L, int nk,
                                        int w, v16f (*acc)[4]) {
   using Lo = TL<FA>;
-  if constexpr (PRO) t_prologue<FA>(lds, src, w);
-  tvmcnt<2 * Lo::kStageLoads>();
+  if constexpr (PRO) t_prologue_n<FA, (NMB > 0)>(lds, src, w);
+  tvmcnt<2 * ((NMB > 0 ? Lo::kAInstr : 0) + Lo::kBInstr)>();
   tbarrier();
 
   TOps X, Y;
@@ -518,6 +542,12 @@ __device__ __forceinline__ bool t_next(const TileArgs& t, int* slot, int nch, in
   }
 }
 
+// Row blocks of 32 that wave half wm (rows 128 wm ..) multiplies in a tile of
+// nrows rows (wave-uniform).
+__device__ __forceinline__ int t_nmb(int nrows, int wm) {
+  return __builtin_amdgcn_readfirstlane(min(4, max(0, (nrows - 128 * wm + 31) / 32)));
+}
+
 template <int FA, int ST>
 __device__ __forceinline__ TLane t_lane(int w, int lane) {
   const int r = lane & 31, h = lane >> 5;
@@ -565,7 +595,7 @@ __device__ __forceinline__ S1Tile<FA> s1_setup(const S1Args& p, int4 tile, int n
 #pragma unroll
   for (int i = 0; i < Lo::kAInstr; ++i) {
     int r, ch;
-    t_aslot<FA>(Lo::kAInstr * w + i, lane, &r, &ch);
+    t_aslot<FA>(t_aci<FA>(w, i), lane, &r, &ch);
     const int tok = p.sorted[row0 + (r < nrows ? r : 0)] / p.k_total;
     c.S.a[i] = (uint32_t)(tok * xrow + 16 * ch);
   }
@@ -579,7 +609,7 @@ __device__ __forceinline__ S1Tile<FA> s1_setup(const S1Args& p, int4 tile, int n
     t_bslot(Lo::kBInstr * w + i, lane, &r, &ch);
     c.S.b[i] = (uint32_t)(wrow(r) * (p.H / 2) + 16 * ch);
   }
-  const int ra = 64 * w + lane;
+  const int ra = t_arow0(w) + lane;
   const int tok = p.sorted[row0 + (ra < nrows ? ra : 0)] / p.k_total;
   c.S.as = (uint32_t)(tok * (p.H / 32));
   c.S.bs = (uint32_t)(wrow(64 * w + lane) * (p.H / 32));
@@ -689,7 +719,7 @@ __device__ __forceinline__ S2Tile<FA> s2_setup(const S2Args& p, int4 tile, int n
 #pragma unroll
   for (int i = 0; i < Lo::kAInstr; ++i) {
     int r, ch;
-    t_aslot<FA>(Lo::kAInstr * w + i, lane, &r, &ch);
+    t_aslot<FA>(t_aci<FA>(w, i), lane, &r, &ch);
     c.S.a[i] = (uint32_t)((r < nrows ? r : 0) * arow + 16 * ch);
   }
   const size_t wr0 = (size_t)e * p.H + c.nc0;  // first weight row of the tile
@@ -701,7 +731,7 @@ __device__ __forceinline__ S2Tile<FA> s2_setup(const S2Args& p, int4 tile, int n
     t_bslot(Lo::kBInstr * w + i, lane, &r, &ch);
     c.S.b[i] = (uint32_t)(r * (p.I / 2) + 16 * ch);
   }
-  const int ra = 64 * w + lane;
+  const int ra = t_arow0(w) + lane;
   c.S.as = (uint32_t)((ra < nrows ? ra : 0) * (p.I / 32));
   c.S.bs = (uint32_t)((64 * w + lane) * (p.I / 32));
   return c;
@@ -727,7 +757,7 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
   if (have) {
     int lane = threadIdx.x % kWave;
     asm volatile("" : "+v"(lane));
-    t_prologue<FA>(lds, s2_setup<FA>(p, tile, nt, w, lane).S, w);
+    t_prologue<FA>(lds, s2_setup<FA>(p, tile, nt, w, lane).S, w, t_nmb(tile.z, wm));
   }
   while (have) {
     // lane-derived offsets are recomputed per tile rather than held in
@@ -737,7 +767,7 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
     const S2Tile<FA> c = s2_setup<FA>(p, tile, nt, w, lane);
     const TLane L = t_lane<FA, 2>(w, lane);
     const int nrows = c.nrows;
-    const int nmb = __builtin_amdgcn_readfirstlane(min(4, max(0, (nrows - 128 * wm + 31) / 32)));
+    const int nmb = t_nmb(nrows, wm);
     v16f acc[4][4];
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
@@ -750,7 +780,7 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
     int nt2;
     have = t_next(p.t, slot, nch, per, &tile2, &nt2);
     sidx[threadIdx.x] = sv;
-    if (have) t_prologue<FA>(lds, s2_setup<FA>(p, tile2, nt2, w, lane).S, w);
+    if (have) t_prologue<FA>(lds, s2_setup<FA>(p, tile2, nt2, w, lane).S, w, t_nmb(tile2.z, wm));
     t_sync_lds();
 
     const int r = lane & 31, g = lane >> 5;
@@ -793,14 +823,14 @@ __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
   S1Tile<FA> c;
   if (have) {
     c = s1_setup<FA>(p, tile, nt, w, lane);
-    t_prologue<FA>(lds, c.S, w);
+    t_prologue<FA>(lds, c.S, w, t_nmb(c.nrows, wm));
   }
   while (have) {
     // lane-derived offsets are recomputed per tile rather than held in
     // registers across the persistent loop (the opaque copy blocks hoisting)
     asm volatile("" : "+v"(lane));
     const TLane L = t_lane<FA, 1>(w, lane);
-    const int nmb = __builtin_amdgcn_readfirstlane(min(4, max(0, (c.nrows - 128 * wm + 31) / 32)));
+    const int nmb = t_nmb(c.nrows, wm);
     v16f acc[4][4];
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
@@ -814,7 +844,7 @@ __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
     const int row0 = c.row0, nrows = c.nrows, hc0 = c.hc0;
     if (have) {
       c = s1_setup<FA>(p, tile2, nt2, w, lane);
-      t_prologue<FA>(lds, c.S, w);
+      t_prologue<FA>(lds, c.S, w, t_nmb(c.nrows, wm));
     }
     s1_epilogue<FA>(p, acc, row0, nrows, hc0, wm, wn, lane, nmb);
   }
