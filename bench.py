@@ -8,7 +8,8 @@ Default workload: the decode-shaped layer (T=64, H=4096, 256 routed experts
 top-8 + 1 shared, I=2048), whose throughput is `value`. The 8K-token prefill
 layer (same dims) is measured beside it and reported under "prefill".
 
-Prints ONE JSON line (see the design doc for every field's definition).
+Prints ONE JSON line: the decode throughput as `value`, its roofline, the
+per-step breakdown, the prefill measurement and the CPU oracle baseline.
 """
 from __future__ import annotations
 
@@ -76,7 +77,7 @@ def expert_bytes(H, I):
     return 2 * I * H // 2 + 2 * I * H // 32, H * I // 2 + H * I // 32
 
 
-def measure(cfg, weights_np, steps, warmup, fmt):
+def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True):
     import torch
 
     import synth
@@ -96,19 +97,33 @@ def measure(cfg, weights_np, steps, warmup, fmt):
     torch.cuda.synchronize()
     variant = moe.moe_last_variant()
 
-    # timed region: K steps, per-step events between the steps of the layer
+    def timed(step_fn, n):
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        t0.record(stream)
+        for _ in range(n):
+            step_fn()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / n, time.perf_counter() - w0
+
+    # timed region 1: K steps of the layer as one HIP graph launch each (the
+    # graph holds the whole path: route, permute, grouped GEMM, combine)
+    graph_ms = None
+    if use_graph:
+        layer.capture(x, w, logits=logits)
+        for _ in range(warmup):
+            layer.replay()
+        graph_ms, graph_wall = timed(layer.replay, steps)
+    # timed region 2: K steps launched eagerly, kernel by kernel
+    eager_ms, eager_wall = timed(lambda: layer.forward(x, w, logits=logits), steps)
+    # per-step breakdown (separate pass: events between the steps of the layer)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    t0.record(stream)
     for i in range(steps):
         layer.forward(x, w, logits=logits, events=ev[i])
-    t1.record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    total_ms = t0.elapsed_time(t1)
     names = ["route", "permute", "quant_tiles", "gate_up", "down", "combine"]
     stage_ms = {n: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in ev]))
                 for j, n in enumerate(names)}
@@ -124,8 +139,12 @@ def measure(cfg, weights_np, steps, warmup, fmt):
     layer_bytes = touched * (w13b + w2b) + cfg.T * cfg.H * 2 * 2 + cfg.T * cfg.E * 4
     gate_up_flops = 4.0 * cfg.H * cfg.I * A
     layer_flops = 6.0 * cfg.H * cfg.I * A
-    ms = total_ms / steps
+    # the reported step: the faster of the two launch modes (both run every kernel of the path)
+    use_g = graph_ms is not None and graph_ms < eager_ms
+    ms = graph_ms if use_g else eager_ms
+    wall = graph_wall if use_g else eager_wall
     return dict(ms_per_step=ms, wall_s=wall, tokens_per_s=cfg.T / (ms * 1e-3), stage_ms=stage_ms,
+                eager_ms_per_step=eager_ms, graph_ms_per_step=graph_ms, graph=use_g,
                 touched=touched, variant=variant, gate_up_bytes=gate_up_bytes,
                 down_bytes=down_bytes, layer_bytes=layer_bytes, gate_up_flops=gate_up_flops,
                 layer_flops=layer_flops)
@@ -162,6 +181,8 @@ def main():
     ap.add_argument("--no-prefill", action="store_true", help="skip the 8K prefill measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=4)
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time eager launches only (default: one HIP graph launch per step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the "
                          "reference for scaling HBM byte counters) and exit")
@@ -194,7 +215,7 @@ def main():
     log(f"generating weights for {cfg.name}")
     weights_np = synth.gen_all_experts(cfg.with_(E=cfg.E, n_shared=max(cfg.n_shared, 0)))
     log("measuring")
-    r = measure(cfg, weights_np, args.steps, args.warmup, args.fmt)
+    r = measure(cfg, weights_np, args.steps, args.warmup, args.fmt, not args.no_graph)
     log(f"{cfg.name}: {r['ms_per_step']:.4f} ms/step, stages {r['stage_ms']}")
     gu_ms = r["stage_ms"]["gate_up"]
     achieved = r["gate_up_bytes"] / (gu_ms * 1e-3) / 1e9
@@ -214,7 +235,10 @@ def main():
         "config": {"workload": f"{cfg.name}: T={cfg.T} H={cfg.H} E={cfg.E}+{cfg.n_shared} "
                                f"k={cfg.k} I={cfg.I}, FP4 e2m1 weights with E8M0 per-32 scales",
                    "global_batch": cfg.T, "act_format": args.fmt,
-                   "experts_touched": r["touched"], "variant": r["variant"]},
+                   "experts_touched": r["touched"], "variant": r["variant"],
+                   "launch": "hip_graph" if r["graph"] else "eager"},
+        "eager_ms_per_step": r["eager_ms_per_step"],
+        "graph_ms_per_step": r["graph_ms_per_step"],
         "roofline": {"kernel": "gate_up (stage 1)", "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": stored_traffic("s1_stream_kernel", cfg.name),
@@ -225,12 +249,15 @@ def main():
     if not args.no_prefill and cfg.name == "decode":
         pcfg = synth.CONFIGS["prefill8k"]
         log("measuring prefill8k")
-        p = measure(pcfg, weights_np, max(3, args.steps // 10), 2, args.fmt)
+        p = measure(pcfg, weights_np, max(3, args.steps // 10), 2, args.fmt, not args.no_graph)
         gu = p["stage_ms"]["gate_up"]
         tf = p["gate_up_flops"] / (gu * 1e-3) / 1e12
         line["prefill"] = {
             "workload": f"prefill8k: T={pcfg.T}, same dims", "tokens_per_s": p["tokens_per_s"],
-            "ms_per_step": p["ms_per_step"], "stage_ms": p["stage_ms"], "variant": p["variant"],
+            "ms_per_step": p["ms_per_step"], "eager_ms_per_step": p["eager_ms_per_step"],
+            "graph_ms_per_step": p["graph_ms_per_step"],
+            "launch": "hip_graph" if p["graph"] else "eager",
+            "stage_ms": p["stage_ms"], "variant": p["variant"],
             "roofline": {"kernel": "gate_up (stage 1)", "bound": "mfma", "achieved": tf,
                          "peak": MFMA_PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
                          "frac": tf / MFMA_PEAK_FP8_TFLOPS,

@@ -32,7 +32,7 @@ in a sum. The steps, in order, each cite what fixes them:
                           FP32 top-k reduction). The oracle sums in fp64 and
                           rounds once to bf16.
 
-Readings where the paper is silent (all listed in the design doc): softmax scoring
+Readings where the paper is silent: softmax scoring
 with renormalisation over the k picks and routed scale 1; SwiGLU
 h = silu(gate) * up; rows 0..I-1 of W13 are gate, I..2I-1 are up; the shared
 expert is expert index E with weight 1, added after the routed slots.

@@ -19,7 +19,7 @@ Formats
   the element format here is one of e4m3 (MXFP8), e2m3 (MXFP6), e2m1 (MXFP4)
   with an E8M0 block scale.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
 * nibble order: element 2i sits in bits 0-3 of byte i, element 2i+1 in bits 4-7;
 * E8M0 byte b decodes to 2**(b-127); b == 255 is NaN (OCP MX v1.0);
 * the activation block scale is the smallest power of two 2**X that lets the

@@ -285,3 +285,27 @@ class MoELayer:
         out = moe_combine_fixed_order(self.partials, self.w, out=self.out, stream=stream)
         ev(6)
         return out
+
+    def capture(self, x, weights, logits=None, w_router=None):
+        """Record one ``forward`` into a HIP graph, so that a decode step is one
+        graph launch instead of six kernel launches. The graph reads x, the
+        weights and the logits from the tensors given here (copy new inputs
+        into them before a replay) and writes ``self.out``. Every kernel of
+        the layer clears what it needs itself (no memset nodes) and the
+        persistent GEMM's work queue is left at zero by each launch, so
+        replays are independent."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):  # first call outside the graph: lazy host state
+            self.forward(x, weights, logits=logits, w_router=w_router)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            self.forward(x, weights, logits=logits, w_router=w_router)
+        return self.out
+
+    def replay(self):
+        """Re-run the captured forward on the current stream; returns ``self.out``."""
+        self.graph.replay()
+        return self.out
