@@ -105,6 +105,47 @@ moe_status moe_router_logits(const uint16_t* x, const uint16_t* w_router, int T,
 moe_status moe_route_topk(const float* logits, int T, int E, int k, int n_shared, int32_t* topk_ids,
                           float* topk_w, void* stream);
 
+/* ---- f1: routing variants -------------------------------------------------
+ * moe_route_topk_ex generalises moe_route_topk. The paper fixes the router's
+ * top-k (top-6 for the model: System and model context / Execution
+ * structure) and a deterministic selection order, and is silent on the
+ * scoring. These options follow DeepSeek's published router design; each is
+ * a reading, not a statement of the paper:
+ *   score      MOE_SCORE_SOFTMAX: s_e = exp(l_e - max l) / sum_e' exp(l_e' - max l)
+ *              MOE_SCORE_SIGMOID: s_e = 1 / (1 + exp(-l_e))
+ *   bias       fp32 [E] (device) or NULL: the selection key of expert e is
+ *              s_e + bias[e]; the bias steers selection only, weights use s_e
+ *   n_group,   experts form n_group groups of E / n_group consecutive ids; a
+ *   topk_group group's score is the sum of its two largest keys (its only key
+ *              when groups have one expert); the topk_group groups with the
+ *              largest scores (ties to the lower group) stay and every other
+ *              expert is excluded; n_group = 1 disables grouping
+ *   renorm     nonzero: the k weights are divided by their sum (in pick order)
+ *   scale      multiplies the k weights (routed scaling factor)
+ * Picks: the k largest keys among the remaining experts, ordered by (key
+ * descending, expert id ascending). Weights: s of each pick, renormalised as
+ * asked, times scale; the shared expert's column (n_shared = 1) keeps weight
+ * 1.0. Arithmetic in fp32; the softmax denominator is summed in a fixed
+ * order. Without a bias, keys are compared as the raw logits (s is
+ * increasing in l), so the picks are exact; with a bias or with groups, a
+ * key tie within fp32 rounding can resolve either way against a reference.
+ * {MOE_SCORE_SOFTMAX, NULL, 1, 1, 1, 1.0f} is exactly moe_route_topk.
+ * Requires opts != NULL, 1 <= n_group <= 64, n_group divides E,
+ * 1 <= topk_group <= n_group, k <= topk_group * E / n_group, plus the
+ * requirements of moe_route_topk. */
+typedef enum { MOE_SCORE_SOFTMAX = 0, MOE_SCORE_SIGMOID = 1 } moe_score_fn;
+typedef struct {
+  moe_score_fn score;
+  const float* bias;
+  int n_group;
+  int topk_group;
+  int renorm;
+  float scale;
+} moe_route_opts;
+moe_status moe_route_topk_ex(const float* logits, int T, int E, int k, int n_shared,
+                             const moe_route_opts* opts, int32_t* topk_ids, float* topk_w,
+                             void* stream);
+
 /* ---- a3: token -> expert permutation ---------------------------------------
  * Stable counting sort of the A = T * k_total assignments a = t*k_total + j by
  * expert id topk_ids[a] (the paper's expert sorter: Prefill optimization /

@@ -78,6 +78,60 @@ def route_topk(logits, k: int, n_shared: int = 0):
     return ids, w
 
 
+def route_topk_ex(logits, k: int, n_shared: int = 0, score: str = "softmax", bias=None,
+                  n_group: int = 1, topk_group: int = 1, renorm: bool = True,
+                  scale: float = 1.0):
+    """Routing variants (readings: the paper fixes top-k and a deterministic
+    order but not the scoring; these follow DeepSeek's published router).
+
+    Scores s: softmax over the E logits, or the logistic sigmoid of each.
+    Selection key: s + bias (bias steers selection only), or the logit itself
+    without a bias (same order as s). With ``n_group`` > 1 the experts form
+    n_group groups of E / n_group consecutive ids; a group scores the sum of
+    its two largest values of s + bias (its single value for one-expert
+    groups); the ``topk_group`` best groups (ties to the lower group) stay and
+    the other experts are excluded. Picks: the k largest keys, ordered by (key
+    descending, id ascending). Weights: s of the picks, divided by their sum
+    if ``renorm``, times ``scale``. The shared column is as in route_topk.
+
+    Returns (ids int32 [T, k + n_shared], w fp64 [T, k + n_shared]).
+    """
+    lg = np.asarray(logits).astype(np.float64)
+    t, e = lg.shape
+    if not 1 <= k <= e:
+        raise ValueError("need 1 <= k <= E")
+    if n_group < 1 or e % n_group or not 1 <= topk_group <= n_group:
+        raise ValueError("bad grouping")
+    if score == "softmax":
+        z = np.exp(lg - lg.max(axis=1, keepdims=True))
+        s = z / z.sum(axis=1, keepdims=True)
+    elif score == "sigmoid":
+        s = 1.0 / (1.0 + np.exp(-lg))
+    else:
+        raise ValueError(f"score: {score!r}")
+    b = None if bias is None else np.asarray(bias, np.float64)
+    key = lg.copy() if b is None else s + b
+    if n_group > 1:
+        gs = e // n_group
+        v = (s if b is None else s + b).reshape(t, n_group, gs)
+        top = -np.sort(-v, axis=2)
+        gscore = top[:, :, 0] if gs == 1 else top[:, :, 0] + top[:, :, 1]
+        gkeep = np.argsort(-gscore, axis=1, kind="stable")[:, :topk_group]
+        allowed = np.zeros((t, n_group), bool)
+        np.put_along_axis(allowed, gkeep, True, axis=1)
+        key = np.where(np.repeat(allowed, gs, axis=1), key, -np.inf)
+    order = np.argsort(-key, axis=1, kind="stable")[:, :k]
+    w = np.take_along_axis(s, order, axis=1)
+    if renorm:
+        w = w / w.sum(axis=1, keepdims=True)
+    w = w * scale
+    ids = order.astype(np.int32)
+    if n_shared:
+        ids = np.concatenate([ids, np.full((t, 1), e, np.int32)], axis=1)
+        w = np.concatenate([w, np.ones((t, 1))], axis=1)
+    return ids, w
+
+
 def permute(ids, n_experts_total: int):
     """Stable counting sort of the assignments a = t*k_total + j by expert id.
 

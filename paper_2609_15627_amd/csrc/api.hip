@@ -68,6 +68,25 @@ moe_status moe_route_topk(const float* logits, int T, int E, int k, int n_shared
                                          as_stream(stream)));
 }
 
+moe_status moe_route_topk_ex(const float* logits, int T, int E, int k, int n_shared,
+                             const moe_route_opts* opts, int32_t* topk_ids, float* topk_w,
+                             void* stream) {
+  if (!opts) return MOE_ERR_INVALID_ARG;
+  if (T < 0 || E < 1 || E > MOE_MAX_EXPERTS || k < 1 || k > E) return MOE_ERR_INVALID_ARG;
+  if (n_shared != 0 && n_shared != 1) return MOE_ERR_INVALID_ARG;
+  if (k + n_shared > MOE_MAX_K_TOTAL || !tokens_ok(T, k + n_shared)) return MOE_ERR_INVALID_ARG;
+  if (opts->score != MOE_SCORE_SOFTMAX && opts->score != MOE_SCORE_SIGMOID)
+    return MOE_ERR_INVALID_ARG;
+  const int ng = opts->n_group, tg = opts->topk_group;
+  if (ng < 1 || ng > 64 || E % ng != 0 || tg < 1 || tg > ng || k > tg * (E / ng))
+    return MOE_ERR_INVALID_ARG;
+  if (T > 0 && (!logits || !topk_ids || !topk_w)) return MOE_ERR_INVALID_ARG;
+  const moe::RouteOpts o{opts->score == MOE_SCORE_SIGMOID ? 1 : 0, opts->bias, ng, tg,
+                         opts->renorm ? 1 : 0, opts->scale};
+  return launched(moe::launch_route_topk_ex(logits, T, E, k, n_shared, o, topk_ids, topk_w,
+                                            as_stream(stream)));
+}
+
 size_t moe_permute_workspace_bytes(int T, int n_experts_total, int k_total) {
   if (T < 0 || n_experts_total < 1 || k_total < 1) return 0;
   return moe::permute_workspace_bytes(T, n_experts_total, k_total);

@@ -13,6 +13,17 @@ hipError_t launch_router_logits(const uint16_t* x, const uint16_t* wr, int T, in
 hipError_t launch_route_topk(const float* logits, int T, int E, int k, int n_shared, int32_t* ids,
                              float* w, hipStream_t s);
 
+// Routing variants (scoring, selection bias, group-limited selection,
+// renormalisation, scaling); sigmoid: 0 softmax, 1 sigmoid.
+struct RouteOpts {
+  int sigmoid;
+  const float* bias;
+  int n_group, topk_group, renorm;
+  float scale;
+};
+hipError_t launch_route_topk_ex(const float* logits, int T, int E, int k, int n_shared,
+                                const RouteOpts& o, int32_t* ids, float* w, hipStream_t s);
+
 size_t permute_workspace_bytes(int T, int NE, int k_total);
 hipError_t launch_permute(const int32_t* ids, int T, int NE, int k_total, int32_t* counts,
                           int32_t* offsets, int32_t* sorted, int32_t* pos, void* ws,

@@ -107,6 +107,187 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
   }
 }
 
+// Routing variants. One wave per token, lane l holds experts l, l + 64, ...
+// Keys: without a bias the raw logits (every score is increasing in the
+// logit); with one, s_e + bias[e] in fp32. Groups: each group's top-two key
+// sum is reduced over the wave (lane g keeps group g's score), k rounds of
+// arg-max over the lanes pick the kept groups, and their ballot masks the
+// experts of the other groups. Then k rounds of arg-max over the keys pick
+// the experts, as in route_topk_kernel.
+__device__ __forceinline__ void top2_merge(float& a1, float& a2, float b1, float b2) {
+  // (a1 >= a2), (b1 >= b2): the two largest of the four
+  const float hi = fmaxf(a1, b1);
+  const float lo = a1 >= b1 ? fmaxf(a2, b1) : fmaxf(a1, b2);
+  a1 = hi;
+  a2 = lo;
+}
+
+template <int EPL>
+__global__ __launch_bounds__(256) void route_topk_ex_kernel(const float* __restrict__ logits, int T,
+                                                            int E, int k, int n_shared,
+                                                            RouteOpts o,
+                                                            int32_t* __restrict__ ids,
+                                                            float* __restrict__ wts) {
+  const int t = (int)(((long)blockIdx.x * blockDim.x + threadIdx.x) / kWave);
+  const int lane = threadIdx.x % kWave;
+  if (t >= T) return;
+  const float* row = logits + (size_t)t * E;
+  float l[EPL], key[EPL];
+  bool live[EPL];
+  float lmax = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < EPL; ++j) {
+    const int e = lane + kWave * j;
+    live[j] = e < E;
+    const float x = live[j] ? row[e] : -INFINITY;
+    l[j] = (x != x) ? -INFINITY : x;  // NaN reads as -inf
+    lmax = fmaxf(lmax, l[j]);
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) lmax = fmaxf(lmax, shfl_xor_f(lmax, m));
+  // softmax denominator, summed in a fixed order (lane order j, then butterfly)
+  float den = 0.0f;
+  if (!o.sigmoid) {
+#pragma unroll
+    for (int j = 0; j < EPL; ++j)
+      if (live[j]) den += expf(l[j] - lmax);
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) den += shfl_xor_f(den, m);
+  }
+  auto score = [&](float x) {
+    return o.sigmoid ? 1.0f / (1.0f + expf(-x)) : expf(x - lmax) / den;
+  };
+#pragma unroll
+  for (int j = 0; j < EPL; ++j) {
+    const int e = lane + kWave * j;
+    key[j] = !live[j] ? -INFINITY : (o.bias ? score(l[j]) + o.bias[e] : l[j]);
+  }
+  if (o.n_group > 1) {
+    const int gs = E / o.n_group;
+    float my_gs = -INFINITY;
+    for (int g = 0; g < o.n_group; ++g) {
+      float a1 = -INFINITY, a2 = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < EPL; ++j) {
+        const int e = lane + kWave * j;
+        if (live[j] && e / gs == g) {
+          // group scores always use the fp32 key value s + bias
+          const float v = o.bias ? key[j] : score(l[j]);
+          top2_merge(a1, a2, v, -INFINITY);
+        }
+      }
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const float b1 = shfl_xor_f(a1, m), b2 = shfl_xor_f(a2, m);
+        top2_merge(a1, a2, b1, b2);
+      }
+      if (lane == g) my_gs = gs == 1 ? a1 : a1 + a2;
+    }
+    // keep topk_group groups: arg-max rounds over (score descending, group ascending)
+    bool kept = false;
+    for (int r = 0; r < o.topk_group; ++r) {
+      float bv = (lane < o.n_group && !kept) ? my_gs : -INFINITY;
+      int bi = (lane < o.n_group && !kept) ? lane : 0x7fffffff;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const float ov = shfl_xor_f(bv, m);
+        const int oi = shfl_xor_i(bi, m);
+        if (ov > bv || (ov == bv && oi < bi)) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      if (lane == bi) kept = true;
+    }
+    const uint64_t mask = __ballot(kept);
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const int e = lane + kWave * j;
+      if (live[j] && !((mask >> (e / gs)) & 1)) live[j] = false;
+    }
+  }
+  float my_key = 0.0f, my_l = 0.0f;
+  int my_id = 0;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY, bl = 0.0f;
+    int bi = 0x7fffffff;
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const int e = lane + kWave * j;
+      if (live[j] && (key[j] > bv || (key[j] == bv && e < bi))) {
+        bv = key[j];
+        bi = e;
+        bl = l[j];
+      }
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const float ov = shfl_xor_f(bv, m), ol = shfl_xor_f(bl, m);
+      const int oi = shfl_xor_i(bi, m);
+      if (ov > bv || (ov == bv && oi < bi)) {
+        bv = ov;
+        bi = oi;
+        bl = ol;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < EPL; ++j)
+      if (lane + kWave * j == bi) live[j] = false;
+    if (lane == r) {
+      my_key = bv;
+      my_id = bi;
+      my_l = bl;
+    }
+  }
+  (void)my_key;
+  float wv;
+  if (!o.sigmoid && o.renorm) {
+    // exactly moe_route_topk's weights: exp(l_j - l_0) / sum over the picks
+    const float l0 = __shfl(my_l, 0, kWave);
+    wv = lane < k ? expf(my_l - l0) : 0.0f;
+  } else {
+    wv = lane < k ? score(my_l) : 0.0f;
+  }
+  if (o.renorm) {
+    float sum = 0.0f;
+    for (int j = 0; j < k; ++j) sum += __shfl(wv, j, kWave);
+    wv = wv / sum;
+  }
+  wv *= o.scale;
+  const int kt = k + n_shared;
+  int32_t* id_row = ids + (size_t)t * kt;
+  float* w_row = wts + (size_t)t * kt;
+  if (lane < k) {
+    id_row[lane] = my_id;
+    w_row[lane] = wv;
+  } else if (lane == k && n_shared) {
+    id_row[lane] = E;
+    w_row[lane] = 1.0f;
+  }
+}
+
+hipError_t launch_route_topk_ex(const float* logits, int T, int E, int k, int n_shared,
+                                const RouteOpts& o, int32_t* ids, float* w, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const int blocks = (T + 3) / 4;
+  const int epl = (E + kWave - 1) / kWave;
+#define MOE_ROUTE_EX(N)                                                                       \
+  hipLaunchKernelGGL(route_topk_ex_kernel<N>, dim3(blocks), dim3(256), 0, s, logits, T, E, k, \
+                     n_shared, o, ids, w)
+  if (epl <= 1)
+    MOE_ROUTE_EX(1);
+  else if (epl <= 2)
+    MOE_ROUTE_EX(2);
+  else if (epl <= 4)
+    MOE_ROUTE_EX(4);
+  else if (epl <= 8)
+    MOE_ROUTE_EX(8);
+  else
+    MOE_ROUTE_EX(16);
+#undef MOE_ROUTE_EX
+  return hipGetLastError();
+}
+
 hipError_t launch_router_logits(const uint16_t* x, const uint16_t* wr, int T, int H, int E,
                                 float* logits, hipStream_t s) {
   const long waves = (long)T * E;

@@ -28,6 +28,7 @@ _SZ = ctypes.c_size_t
 _SIGNATURES = {
     "moe_router_logits": (_I, [_P, _P, _I, _I, _I, _P, _P]),
     "moe_route_topk": (_I, [_P, _I, _I, _I, _I, _P, _P, _P]),
+    "moe_route_topk_ex": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P]),
     "moe_permute_workspace_bytes": (_SZ, [_I, _I, _I]),
     "moe_permute": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _P, _SZ, _P]),
     "moe_quantize_act": (_I, [_P, _I, _I, _I, _P, _P, _P]),
@@ -104,7 +105,16 @@ def moe_router_logits(x, w_router, logits=None, stream=None):
     return logits
 
 
-def moe_route_topk(logits, k, n_shared=0, topk_ids=None, topk_w=None, stream=None):
+class _RouteOpts(ctypes.Structure):
+    _fields_ = [("score", ctypes.c_int), ("bias", ctypes.c_void_p), ("n_group", ctypes.c_int),
+                ("topk_group", ctypes.c_int), ("renorm", ctypes.c_int), ("scale", ctypes.c_float)]
+
+
+def moe_route_topk(logits, k, n_shared=0, topk_ids=None, topk_w=None, stream=None,
+                   score="softmax", bias=None, n_group=1, topk_group=1, renorm=True, scale=1.0):
+    """Top-k routing. With the default options this is ``moe_route_topk``;
+    otherwise ``moe_route_topk_ex`` (score "softmax" | "sigmoid", selection
+    bias fp32 [E], group-limited selection, renormalisation, scaling)."""
     T, E = logits.shape
     kt = k + n_shared
     _need(logits, torch.float32, (T, E), "logits")
@@ -114,8 +124,21 @@ def moe_route_topk(logits, k, n_shared=0, topk_ids=None, topk_w=None, stream=Non
         topk_w = torch.empty((T, kt), dtype=torch.float32, device=logits.device)
     _need(topk_ids, torch.int32, (T, kt), "topk_ids")
     _need(topk_w, torch.float32, (T, kt), "topk_w")
-    _check(lib.moe_route_topk(_ptr(logits), T, E, k, n_shared, _ptr(topk_ids), _ptr(topk_w),
-                              _stream(stream)), "moe_route_topk")
+    default = (score == "softmax" and bias is None and n_group == 1 and bool(renorm)
+               and scale == 1.0)
+    if default:
+        _check(lib.moe_route_topk(_ptr(logits), T, E, k, n_shared, _ptr(topk_ids), _ptr(topk_w),
+                                  _stream(stream)), "moe_route_topk")
+        return topk_ids, topk_w
+    if score not in ("softmax", "sigmoid"):
+        raise ValueError(f"score: {score!r}")
+    if bias is not None:
+        _need(bias, torch.float32, (E,), "bias")
+    opts = _RouteOpts(1 if score == "sigmoid" else 0, None if bias is None else bias.data_ptr(),
+                      n_group, topk_group, 1 if renorm else 0, scale)
+    _check(lib.moe_route_topk_ex(_ptr(logits), T, E, k, n_shared, ctypes.byref(opts),
+                                 _ptr(topk_ids), _ptr(topk_w), _stream(stream)),
+           "moe_route_topk_ex")
     return topk_ids, topk_w
 
 
