@@ -150,6 +150,53 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True):
                 layer_flops=layer_flops)
 
 
+def measure_router(cfg, steps):
+    """The router front-end: fused projection + top-k (moe_router_topk) against
+    the two-call path (moe_router_logits, then moe_route_topk), bf16 router
+    weights N(0, 0.02) of the workload's dims."""
+    import torch
+
+    import synth
+    from paper_2609_15627_amd import moe
+
+    dev = torch.device("cuda:0")
+    x = torch.from_numpy(synth.gen_x(cfg).view(np.int16)).to(dev).view(torch.bfloat16)
+    rng = np.random.default_rng(7)
+    wr32 = (0.02 * rng.standard_normal((cfg.E, cfg.H))).astype(np.float32)
+    wr = torch.from_numpy((wr32.view(np.uint32) >> 16).astype(np.uint16).view(np.int16)).to(
+        dev).view(torch.bfloat16)
+    kt = cfg.k + cfg.n_shared
+    ids = torch.empty((cfg.T, kt), dtype=torch.int32, device=dev)
+    w = torch.empty((cfg.T, kt), dtype=torch.float32, device=dev)
+    lg = torch.empty((cfg.T, cfg.E), dtype=torch.float32, device=dev)
+
+    def fused():  # one call; with a logits buffer the library picks its path by T
+        moe.moe_router_topk(x, wr, cfg.k, cfg.n_shared, logits=lg, topk_ids=ids, topk_w=w)
+
+    def two_call():
+        moe.moe_router_logits(x, wr, logits=lg)
+        moe.moe_route_topk(lg, cfg.k, cfg.n_shared, ids, w)
+
+    out = {}
+    for name, fn, n in (("router_topk_ms", fused, steps),
+                        ("two_call_ms", two_call, max(2, steps // 10))):
+        fn()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(n):
+            fn()
+        t1.record()
+        torch.cuda.synchronize()
+        out[name] = t0.elapsed_time(t1) / n
+    nbytes = cfg.T * cfg.H * 2 + cfg.E * cfg.H * 2 + cfg.T * kt * 8
+    out["path"] = "fused" if cfg.T >= 1024 else "logits kernel + routing kernel"
+    out["router_topk_GBps"] = nbytes / (out["router_topk_ms"] * 1e-3) / 1e9
+    out["router_topk_TFLOPs"] = 2.0 * cfg.T * cfg.H * cfg.E / (out["router_topk_ms"] * 1e-3) / 1e12
+    return out
+
+
 def cpu_baseline(cfg, weights_np, ntok, fmt):
     """The fp64 oracle, as it is, on a bounded token sample of the same workload."""
     import synth
@@ -181,6 +228,7 @@ def main():
     ap.add_argument("--no-prefill", action="store_true", help="skip the 8K prefill measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=4)
+    ap.add_argument("--no-router", action="store_true", help="skip the router front-end timing")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager launches only (default: one HIP graph launch per step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -267,6 +315,10 @@ def main():
             "layer_mfma_frac_of_fp4_peak": p["layer_flops"] / (p["ms_per_step"] * 1e-3) / 1e12
             / MFMA_PEAK_FP4_TFLOPS,
         }
+    if not args.no_router and cfg.name == "decode":
+        log("measuring the router front-end")
+        line["router"] = {"decode": measure_router(cfg, args.steps),
+                          "prefill8k": measure_router(synth.CONFIGS["prefill8k"], 20)}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         line["cpu_baseline"] = cpu_baseline(cfg, weights_np, args.cpu_tokens, args.fmt)

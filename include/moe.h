@@ -146,6 +146,26 @@ moe_status moe_route_topk_ex(const float* logits, int T, int E, int k, int n_sha
                              const moe_route_opts* opts, int32_t* topk_ids, float* topk_w,
                              void* stream);
 
+/* ---- f1: fused router projection and routing ------------------------------
+ * One call for logits = x . w_router^T (as moe_router_logits, products
+ * accumulated in fp32 by the matrix cores, so the summation order differs
+ * from moe_router_logits) followed by the routing of moe_route_topk_ex (opts
+ * NULL: the defaults of moe_route_topk), without a logits round trip
+ * through memory. A logit tie within fp32 accumulation error can resolve
+ * either way against a reference.
+ *   x         bf16 [T, H]      w_router  bf16 [E, H]
+ *   logits    fp32 [T, E] (written if not NULL)
+ *   topk_ids, topk_w as moe_route_topk
+ * With a logits buffer and T < 1024 the call runs moe_router_logits and
+ * moe_route_topk_ex instead (two kernels; faster for few tokens, where a
+ * fused workgroup streams the whole router matrix for a handful of tokens).
+ * Requires H % 128 == 0, 1 <= E <= 256, plus the requirements of
+ * moe_route_topk_ex; E > 256 returns MOE_ERR_UNSUPPORTED (use
+ * moe_router_logits + moe_route_topk_ex). */
+moe_status moe_router_topk(const uint16_t* x, const uint16_t* w_router, int T, int H, int E, int k,
+                           int n_shared, const moe_route_opts* opts, float* logits,
+                           int32_t* topk_ids, float* topk_w, void* stream);
+
 /* ---- a3: token -> expert permutation ---------------------------------------
  * Stable counting sort of the A = T * k_total assignments a = t*k_total + j by
  * expert id topk_ids[a] (the paper's expert sorter: Prefill optimization /

@@ -68,10 +68,12 @@ moe_status moe_route_topk(const float* logits, int T, int E, int k, int n_shared
                                          as_stream(stream)));
 }
 
-moe_status moe_route_topk_ex(const float* logits, int T, int E, int k, int n_shared,
-                             const moe_route_opts* opts, int32_t* topk_ids, float* topk_w,
-                             void* stream) {
-  if (!opts) return MOE_ERR_INVALID_ARG;
+// Below this many tokens moe_router_topk computes the logits and routes them
+// in two kernels when the caller gives a logits buffer.
+constexpr int kRouterFusedMinTokens = 1024;
+
+// Validation shared by moe_route_topk_ex and moe_router_topk (opts not NULL).
+static moe_status check_route(int T, int E, int k, int n_shared, const moe_route_opts* opts) {
   if (T < 0 || E < 1 || E > MOE_MAX_EXPERTS || k < 1 || k > E) return MOE_ERR_INVALID_ARG;
   if (n_shared != 0 && n_shared != 1) return MOE_ERR_INVALID_ARG;
   if (k + n_shared > MOE_MAX_K_TOTAL || !tokens_ok(T, k + n_shared)) return MOE_ERR_INVALID_ARG;
@@ -80,11 +82,46 @@ moe_status moe_route_topk_ex(const float* logits, int T, int E, int k, int n_sha
   const int ng = opts->n_group, tg = opts->topk_group;
   if (ng < 1 || ng > 64 || E % ng != 0 || tg < 1 || tg > ng || k > tg * (E / ng))
     return MOE_ERR_INVALID_ARG;
+  return MOE_OK;
+}
+
+static moe::RouteOpts route_opts(const moe_route_opts* opts) {
+  return moe::RouteOpts{opts->score == MOE_SCORE_SIGMOID ? 1 : 0, opts->bias, opts->n_group,
+                        opts->topk_group, opts->renorm ? 1 : 0, opts->scale};
+}
+
+moe_status moe_router_topk(const uint16_t* x, const uint16_t* w_router, int T, int H, int E, int k,
+                           int n_shared, const moe_route_opts* opts, float* logits,
+                           int32_t* topk_ids, float* topk_w, void* stream) {
+  static const moe_route_opts kDefault{MOE_SCORE_SOFTMAX, nullptr, 1, 1, 1, 1.0f};
+  if (!opts) opts = &kDefault;
+  const moe_status st = check_route(T, E, k, n_shared, opts);
+  if (st != MOE_OK) return st;
+  if (H <= 0 || H % 128 != 0) return MOE_ERR_INVALID_ARG;
+  if (E > 256) return MOE_ERR_UNSUPPORTED;
+  if (T > 0 && (!x || !w_router || !topk_ids || !topk_w)) return MOE_ERR_INVALID_ARG;
+  // Few tokens: each fused workgroup streams the whole router matrix, which
+  // takes longer than computing the logits with many waves and routing them
+  // separately; that needs the logits buffer.
+  if (logits && T < kRouterFusedMinTokens) {
+    hipError_t err = moe::launch_router_logits(x, w_router, T, H, E, logits, as_stream(stream));
+    if (err != hipSuccess) return MOE_ERR_LAUNCH;
+    return launched(moe::launch_route_topk_ex(logits, T, E, k, n_shared, route_opts(opts),
+                                              topk_ids, topk_w, as_stream(stream)));
+  }
+  return launched(moe::launch_router_topk(x, w_router, T, H, E, k, n_shared, route_opts(opts),
+                                          logits, topk_ids, topk_w, as_stream(stream)));
+}
+
+moe_status moe_route_topk_ex(const float* logits, int T, int E, int k, int n_shared,
+                             const moe_route_opts* opts, int32_t* topk_ids, float* topk_w,
+                             void* stream) {
+  if (!opts) return MOE_ERR_INVALID_ARG;
+  const moe_status st = check_route(T, E, k, n_shared, opts);
+  if (st != MOE_OK) return st;
   if (T > 0 && (!logits || !topk_ids || !topk_w)) return MOE_ERR_INVALID_ARG;
-  const moe::RouteOpts o{opts->score == MOE_SCORE_SIGMOID ? 1 : 0, opts->bias, ng, tg,
-                         opts->renorm ? 1 : 0, opts->scale};
-  return launched(moe::launch_route_topk_ex(logits, T, E, k, n_shared, o, topk_ids, topk_w,
-                                            as_stream(stream)));
+  return launched(moe::launch_route_topk_ex(logits, T, E, k, n_shared, route_opts(opts), topk_ids,
+                                            topk_w, as_stream(stream)));
 }
 
 size_t moe_permute_workspace_bytes(int T, int n_experts_total, int k_total) {

@@ -21,6 +21,9 @@ struct RouteOpts {
   int n_group, topk_group, renorm;
   float scale;
 };
+hipError_t launch_router_topk(const uint16_t* x, const uint16_t* wr, int T, int H, int E, int k,
+                              int n_shared, const RouteOpts& o, float* logits, int32_t* ids,
+                              float* w, hipStream_t s);
 hipError_t launch_route_topk_ex(const float* logits, int T, int E, int k, int n_shared,
                                 const RouteOpts& o, int32_t* ids, float* w, hipStream_t s);
 

@@ -29,6 +29,7 @@ _SIGNATURES = {
     "moe_router_logits": (_I, [_P, _P, _I, _I, _I, _P, _P]),
     "moe_route_topk": (_I, [_P, _I, _I, _I, _I, _P, _P, _P]),
     "moe_route_topk_ex": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P]),
+    "moe_router_topk": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
     "moe_permute_workspace_bytes": (_SZ, [_I, _I, _I]),
     "moe_permute": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _P, _SZ, _P]),
     "moe_quantize_act": (_I, [_P, _I, _I, _I, _P, _P, _P]),
@@ -140,6 +141,38 @@ def moe_route_topk(logits, k, n_shared=0, topk_ids=None, topk_w=None, stream=Non
                                  _ptr(topk_ids), _ptr(topk_w), _stream(stream)),
            "moe_route_topk_ex")
     return topk_ids, topk_w
+
+
+def moe_router_topk(x, w_router, k, n_shared=0, logits=None, topk_ids=None, topk_w=None,
+                    stream=None, score="softmax", bias=None, n_group=1, topk_group=1,
+                    renorm=True, scale=1.0, want_logits=False):
+    """Fused router projection + routing (E <= 256). Returns (ids, w) or, with
+    ``want_logits``, (ids, w, logits)."""
+    T, H = x.shape
+    E = w_router.shape[0]
+    kt = k + n_shared
+    _need(x, torch.bfloat16, (T, H), "x")
+    _need(w_router, torch.bfloat16, (E, H), "w_router")
+    if want_logits and logits is None:
+        logits = torch.empty((T, E), dtype=torch.float32, device=x.device)
+    if logits is not None:
+        _need(logits, torch.float32, (T, E), "logits")
+    if topk_ids is None:
+        topk_ids = torch.empty((T, kt), dtype=torch.int32, device=x.device)
+    if topk_w is None:
+        topk_w = torch.empty((T, kt), dtype=torch.float32, device=x.device)
+    _need(topk_ids, torch.int32, (T, kt), "topk_ids")
+    _need(topk_w, torch.float32, (T, kt), "topk_w")
+    if score not in ("softmax", "sigmoid"):
+        raise ValueError(f"score: {score!r}")
+    if bias is not None:
+        _need(bias, torch.float32, (E,), "bias")
+    opts = _RouteOpts(1 if score == "sigmoid" else 0, None if bias is None else bias.data_ptr(),
+                      n_group, topk_group, 1 if renorm else 0, scale)
+    _check(lib.moe_router_topk(_ptr(x), _ptr(w_router), T, H, E, k, n_shared,
+                               ctypes.byref(opts), _ptr(logits), _ptr(topk_ids), _ptr(topk_w),
+                               _stream(stream)), "moe_router_topk")
+    return (topk_ids, topk_w, logits) if want_logits else (topk_ids, topk_w)
 
 
 def moe_permute_workspace_bytes(T, n_experts_total, k_total):

@@ -109,3 +109,68 @@ def test_route_variant_rejects(m):
     for bad in (dict(n_group=3), dict(n_group=4, topk_group=5), dict(n_group=4, topk_group=1)):
         with pytest.raises(m.MoeError):
             m.moe_route_topk(lg, 6, 0, **bad)
+
+
+# ----------------------------------------------------------- fused router (f1)
+def _router_case(T, H, E, seed):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((T, H)).astype(np.float32)
+    wr = (0.02 * rng.standard_normal((E, H))).astype(np.float32)
+    xb = (x.view(np.uint32) >> 16).astype(np.uint16)       # truncation to bf16 bits
+    wb = (wr.view(np.uint32) >> 16).astype(np.uint16)
+    return xb, wb
+
+
+@pytest.mark.parametrize("T,H,E,k,S,opts", [
+    (8192, 4096, 256, 8, 1, {}),                                   # prefill-sized, defaults
+    (64, 4096, 256, 6, 0, dict(score="sigmoid", scale=2.5)),       # decode, the model's top-6
+    (100, 1024, 256, 8, 1, dict(score="sigmoid", n_group=8, topk_group=4, bias=True)),
+    (37, 256, 8, 2, 0, {}),                                        # ragged token block, E < 64
+    (1500, 512, 64, 4, 0, dict(score="sigmoid")),                  # fused path, ragged last block
+    (65, 512, 100, 7, 1, dict(renorm=False)),                      # E not a multiple of 64
+])
+def test_router_topk_fused(m, T, H, E, k, S, opts):
+    xb, wb = _router_case(T, H, E, T + H + E)
+    o = dict(opts)
+    if o.pop("bias", None):
+        o["bias"] = (0.05 * np.random.default_rng(1).standard_normal(E)).astype(np.float32)
+    log(f"fused router T={T} H={H} E={E} k={k} opts={sorted(o)}")
+    x = torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16)
+    wr = torch.from_numpy(wb.view(np.int16)).cuda().view(torch.bfloat16)
+    bias = None if "bias" not in o else torch.from_numpy(o["bias"]).cuda()
+    ids, w, lg = m.moe_router_topk(x, wr, k, S, want_logits=True, **{**o, "bias": bias})
+    torch.cuda.synchronize()
+    ids, w, lg = ids.cpu().numpy(), w.cpu().numpy().astype(np.float64), lg.cpu().numpy()
+    # logits: exact bf16 products summed in fp32, H / 16 accumulation steps of
+    # the matrix core, each rounding by at most 2^-24 of a partial sum bounded
+    # by sum_h |x_h w_h|
+    ref = omoe.router_logits(xb, wb)
+    mag = np.abs(omoe.mx.bf16_to_f64(xb)) @ np.abs(omoe.mx.bf16_to_f64(wb)).T
+    assert np.all(np.abs(lg - ref) <= (H / 16 + 16) * 2.0 ** -24 * mag + 1e-30)
+    # routing of the GPU's own logits must match the oracle's routing of them exactly
+    # where the keys are logits, and within near ties otherwise
+    ids_ref, w_ref = omoe.route_topk_ex(lg, k, S, **o)
+    diff = (ids != ids_ref).any(axis=1)
+    if "bias" not in o and o.get("n_group", 1) == 1:
+        assert not diff.any()
+    else:
+        assert diff.mean() <= 1e-2
+    same = ~diff
+    assert np.all(np.abs(w[same] - w_ref[same]) <= 1e-5 * np.abs(w_ref[same]) + 1e-7)
+    # and against the fp64 logits: picks differ only at logit near-ties
+    ids64, _ = omoe.route_topk_ex(ref, k, S, **o)
+    d64 = (ids[:, :k] != ids64[:, :k]).any(axis=1)
+    log(f"  picks differing from fp64-logit routing: {int(d64.sum())} of {T}")
+    assert d64.mean() <= 1e-2
+
+
+def test_router_topk_rejects(m):
+    x = torch.zeros((4, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(m.MoeError):
+        m.moe_router_topk(x, torch.zeros((300, 64), dtype=torch.bfloat16, device="cuda"), 2)
+    with pytest.raises(m.MoeError):
+        m.moe_router_topk(torch.zeros((4, 96), dtype=torch.bfloat16, device="cuda"),
+                          torch.zeros((16, 96), dtype=torch.bfloat16, device="cuda"), 2)
+    with pytest.raises(m.MoeError):
+        m.moe_router_topk(torch.zeros((4, 192), dtype=torch.bfloat16, device="cuda"),
+                          torch.zeros((16, 192), dtype=torch.bfloat16, device="cuda"), 2)
