@@ -77,7 +77,7 @@ def expert_bytes(H, I):
     return 2 * I * H // 2 + 2 * I * H // 32, H * I // 2 + H * I // 32
 
 
-def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True):
+def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True, fused=False):
     import torch
 
     import synth
@@ -89,7 +89,8 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True):
     x = torch.from_numpy(x_np.view(np.int16)).to(dev).view(torch.bfloat16)
     logits = torch.from_numpy(logits_np).to(dev)
     w = tuple(torch.from_numpy(a[: cfg.NE]).to(dev) for a in weights_np)
-    layer = moe.MoELayer(cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.n_shared, fmt, device=dev)
+    layer = moe.MoELayer(cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.n_shared, fmt, device=dev,
+                         fused=fused)
     stream = torch.cuda.current_stream()
 
     for _ in range(warmup):
@@ -135,7 +136,8 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True):
     xb = cfg.T * cfg.H * (1 + 1 / 32)                      # MXFP8 x codes + scales
     hb = A * cfg.I * (1 + 1 / 32)                           # MXFP8 h codes + scales
     gate_up_bytes = touched * w13b + xb + hb
-    down_bytes = touched * w2b + hb + A * cfg.H * 4
+    # down writes fp32 partial rows, or (fused with the combine) the bf16 output
+    down_bytes = touched * w2b + hb + (cfg.T * cfg.H * 2 if layer.fused else A * cfg.H * 4)
     layer_bytes = touched * (w13b + w2b) + cfg.T * cfg.H * 2 * 2 + cfg.T * cfg.E * 4
     gate_up_flops = 4.0 * cfg.H * cfg.I * A
     layer_flops = 6.0 * cfg.H * cfg.I * A
@@ -145,9 +147,36 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True):
     wall = graph_wall if use_g else eager_wall
     return dict(ms_per_step=ms, wall_s=wall, tokens_per_s=cfg.T / (ms * 1e-3), stage_ms=stage_ms,
                 eager_ms_per_step=eager_ms, graph_ms_per_step=graph_ms, graph=use_g,
-                touched=touched, variant=variant, gate_up_bytes=gate_up_bytes,
+                touched=touched, variant=variant, fused=layer.fused, gate_up_bytes=gate_up_bytes,
                 down_bytes=down_bytes, layer_bytes=layer_bytes, gate_up_flops=gate_up_flops,
                 layer_flops=layer_flops)
+
+
+def measure_workload(name, steps, fmt, use_graph, weights_np=None):
+    """One of the other full-size workloads (the Zipf-skewed 32K prefill, the
+    TP-shard shape at I=256): layer time, stage times and both rooflines of
+    the whole layer (algorithmic bytes against HBM, flops against the matrix
+    cores' FP8-rate and FP4 peaks)."""
+    import synth
+    cfg = synth.CONFIGS[name]
+    log(f"measuring {name}")
+    # expert e's weights depend only on (seed, e, H, I): same-dims workloads share them
+    r = measure(cfg, weights_np if weights_np is not None else synth.gen_all_experts(cfg),
+                steps, 2, fmt, use_graph)
+    s = r["ms_per_step"] * 1e-3
+    gb = r["layer_bytes"] / s / 1e9
+    tf = r["layer_flops"] / s / 1e12
+    return {"workload": f"{name}: T={cfg.T} H={cfg.H} E={cfg.E}+{cfg.n_shared} k={cfg.k} "
+                        f"I={cfg.I}, {cfg.routing} routing",
+            "tokens_per_s": r["tokens_per_s"], "ms_per_step": r["ms_per_step"],
+            "eager_ms_per_step": r["eager_ms_per_step"],
+            "graph_ms_per_step": r["graph_ms_per_step"],
+            "launch": "hip_graph" if r["graph"] else "eager", "variant": r["variant"],
+            "experts_touched": r["touched"], "stage_ms": r["stage_ms"],
+            "down_fused_with_combine": r["fused"],
+            "layer_GBps": gb, "layer_hbm_frac": gb / HBM_PEAK_GBS,
+            "layer_TFLOPs": tf, "layer_frac_of_fp8_peak": tf / MFMA_PEAK_FP8_TFLOPS,
+            "layer_frac_of_fp4_peak": tf / MFMA_PEAK_FP4_TFLOPS}
 
 
 def measure_router(cfg, steps):
@@ -229,6 +258,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=4)
     ap.add_argument("--no-router", action="store_true", help="skip the router front-end timing")
+    ap.add_argument("--workloads", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time the skewed 32K prefill and the TP-shard workloads")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager launches only (default: one HIP graph launch per step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -284,6 +315,7 @@ def main():
                                f"k={cfg.k} I={cfg.I}, FP4 e2m1 weights with E8M0 per-32 scales",
                    "global_batch": cfg.T, "act_format": args.fmt,
                    "experts_touched": r["touched"], "variant": r["variant"],
+                   "down_fused_with_combine": r["fused"],
                    "launch": "hip_graph" if r["graph"] else "eager"},
         "eager_ms_per_step": r["eager_ms_per_step"],
         "graph_ms_per_step": r["graph_ms_per_step"],
@@ -306,6 +338,7 @@ def main():
             "graph_ms_per_step": p["graph_ms_per_step"],
             "launch": "hip_graph" if p["graph"] else "eager",
             "stage_ms": p["stage_ms"], "variant": p["variant"],
+            "down_fused_with_combine": p["fused"],
             "roofline": {"kernel": "gate_up (stage 1)", "bound": "mfma", "achieved": tf,
                          "peak": MFMA_PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
                          "frac": tf / MFMA_PEAK_FP8_TFLOPS,
@@ -315,6 +348,20 @@ def main():
             "layer_mfma_frac_of_fp4_peak": p["layer_flops"] / (p["ms_per_step"] * 1e-3) / 1e12
             / MFMA_PEAK_FP4_TFLOPS,
         }
+    from paper_2609_15627_amd import moe as _moe
+    if _moe.moe_fp4_grouped_gemm_combine_supported(cfg.T, cfg.H, cfg.I, cfg.NE, cfg.k_total,
+                                                   args.fmt):
+        log("measuring the down projection fused with the combine")
+        u = measure(cfg, weights_np, args.steps, args.warmup, args.fmt, not args.no_graph,
+                    fused=True)
+        line["fused_down_combine"] = {
+            "ms_per_step": u["ms_per_step"], "eager_ms_per_step": u["eager_ms_per_step"],
+            "graph_ms_per_step": u["graph_ms_per_step"], "stage_ms": u["stage_ms"],
+            "down_combine_GBps": u["down_bytes"] / (u["stage_ms"]["down"] * 1e-3) / 1e9}
+    if args.workloads and cfg.name == "decode":
+        line["workloads"] = {
+            "skew32k": measure_workload("skew32k", 5, args.fmt, not args.no_graph, weights_np),
+            "tpshard": measure_workload("tpshard", 10, args.fmt, not args.no_graph)}
     if not args.no_router and cfg.name == "decode":
         log("measuring the router front-end")
         line["router"] = {"decode": measure_router(cfg, args.steps),

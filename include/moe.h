@@ -257,6 +257,36 @@ moe_status moe_fp4_grouped_gemm_stages(const uint16_t* x, int T, int H, int I,
                                        const uint8_t* w2_s, moe_act_format f, float* partials,
                                        void* ws, size_t ws_bytes, int stages, void* stream);
 
+/* ---- f3: small-M down projection fused with the combine ---------------------
+ * moe_fp4_grouped_gemm followed by moe_combine_fixed_order as one call, for
+ * decode-sized batches: the down projection of every row and the
+ * fixed-order sum over each token's slots run in one kernel, so no fp32
+ * partial row is written to global memory and no combine kernel runs (the
+ * paper's small down consumer, Historical down-consumer pilot, joined to its
+ * fixed-order reducer, Current TP8 native-AR results / Accepted large-prefill
+ * configuration). The output has exactly the bits of the two calls: the same
+ * products in the same order, then acc = fmaf(topk_w[t, j], ., acc) for j =
+ * 0 .. k_total-1 and one bf16 rounding.
+ *   topk_w  fp32 [T, k_total] (from moe_route_topk); out bf16 [T, H]
+ *   other arguments as moe_fp4_grouped_gemm_stages; stages bit 2 = the fused
+ *   down projection + combine (writes out), 7 = the whole call.
+ * An assignment with an invalid expert id contributes 0.
+ * Available when moe_fp4_grouped_gemm_combine_supported() returns 1: the
+ * weight-streaming geometry is chosen (few rows per expert) and the fp32
+ * results of all T * k_total rows for 16 output columns fit one workgroup's
+ * LDS (T * k_total * 64 + 32 * I bytes; T * k_total up to 1536 at
+ * I = 2048). Otherwise (or without a device) MOE_ERR_UNSUPPORTED, and nothing
+ * is enqueued: use the two calls. */
+int moe_fp4_grouped_gemm_combine_supported(int T, int H, int I, int n_experts_total, int k_total,
+                                           moe_act_format f);
+moe_status moe_fp4_grouped_gemm_combine(const uint16_t* x, int T, int H, int I,
+                                        int n_experts_total, int k_total, const int32_t* offsets,
+                                        const int32_t* sorted, const uint8_t* w13,
+                                        const uint8_t* w13_s, const uint8_t* w2,
+                                        const uint8_t* w2_s, moe_act_format f,
+                                        const float* topk_w, uint16_t* out, void* ws,
+                                        size_t ws_bytes, int stages, void* stream);
+
 /* ---- a7: fixed-order combine ------------------------------------------------
  * out[t, :] = bf16_rne(acc), acc = 0; for j = 0 .. k_total-1:
  *   acc = fmaf(topk_w[t, j], partials[t*k_total + j, :], acc)      (fp32)

@@ -174,24 +174,29 @@ moe_status moe_fp4_grouped_gemm_workspace_layout(int T, int H, int I, int n_expe
   return MOE_OK;
 }
 
+// fused: stage 2 writes out through the combine (topk_w, out) instead of
+// partials.
 static moe_status grouped_gemm(const uint16_t* x, int T, int H, int I, int n_experts_total,
                                int k_total, const int32_t* offsets, const int32_t* sorted,
                                const uint8_t* w13, const uint8_t* w13_s, const uint8_t* w2,
-                               const uint8_t* w2_s, moe_act_format f, float* partials, void* ws,
+                               const uint8_t* w2_s, moe_act_format f, float* partials,
+                               bool fused, const float* topk_w, uint16_t* out, void* ws,
                                size_t ws_bytes, int stages, void* stream) {
   const int fc = fmt_code(f);
   if (fc < 0 || !gemm_dims_ok(T, H, I, n_experts_total, k_total)) return MOE_ERR_INVALID_ARG;
   if (stages < 1 || stages > 7) return MOE_ERR_INVALID_ARG;
   if (fc == 2) return MOE_ERR_UNSUPPORTED;
-  if (T > 0 && (!x || !offsets || !sorted || !w13 || !w13_s || !w2 || !w2_s || !partials))
+  if (T > 0 && (!x || !offsets || !sorted || !w13 || !w13_s || !w2 || !w2_s))
     return MOE_ERR_INVALID_ARG;
+  if (T > 0 && (fused ? (!topk_w || !out) : !partials)) return MOE_ERR_INVALID_ARG;
   if (!aligned(x, 16) || !aligned(w13, 16) || !aligned(w2, 16) || !aligned(w13_s, 4) ||
-      !aligned(w2_s, 4) || !aligned(partials, 16))
+      !aligned(w2_s, 4) || !aligned(partials, 16) || !aligned(out, 16) || !aligned(topk_w, 4))
     return MOE_ERR_INVALID_ARG;
   const size_t need = moe::gemm_workspace(T, H, I, n_experts_total, k_total, fc).off[5];
   if (T > 0 && (!ws || ws_bytes < need || !aligned(ws, 256))) return MOE_ERR_WORKSPACE;
   moe::GemmArgs a{x, T, H, I, n_experts_total, k_total, fc, offsets, sorted,
-                  w13, w13_s, w2, w2_s, partials, static_cast<uint8_t*>(ws)};
+                  w13, w13_s, w2, w2_s, partials, static_cast<uint8_t*>(ws), topk_w, out};
+  if (fused && T > 0 && !moe::fused_combine_ok(a)) return MOE_ERR_UNSUPPORTED;
   int variant = MOE_VARIANT_NONE;
   const moe_status st = launched(moe::launch_grouped_gemm(a, stages, as_stream(stream), &variant));
   g_last_variant = variant;
@@ -204,7 +209,7 @@ moe_status moe_fp4_grouped_gemm(const uint16_t* x, int T, int H, int I, int n_ex
                                 const uint8_t* w2_s, moe_act_format f, float* partials, void* ws,
                                 size_t ws_bytes, void* stream) {
   return grouped_gemm(x, T, H, I, n_experts_total, k_total, offsets, sorted, w13, w13_s, w2, w2_s,
-                      f, partials, ws, ws_bytes, 7, stream);
+                      f, partials, false, nullptr, nullptr, ws, ws_bytes, 7, stream);
 }
 
 moe_status moe_fp4_grouped_gemm_stages(const uint16_t* x, int T, int H, int I,
@@ -214,7 +219,27 @@ moe_status moe_fp4_grouped_gemm_stages(const uint16_t* x, int T, int H, int I,
                                        const uint8_t* w2_s, moe_act_format f, float* partials,
                                        void* ws, size_t ws_bytes, int stages, void* stream) {
   return grouped_gemm(x, T, H, I, n_experts_total, k_total, offsets, sorted, w13, w13_s, w2, w2_s,
-                      f, partials, ws, ws_bytes, stages, stream);
+                      f, partials, false, nullptr, nullptr, ws, ws_bytes, stages, stream);
+}
+
+int moe_fp4_grouped_gemm_combine_supported(int T, int H, int I, int n_experts_total, int k_total,
+                                           moe_act_format f) {
+  const int fc = fmt_code(f);
+  if (fc < 0 || fc == 2 || !gemm_dims_ok(T, H, I, n_experts_total, k_total)) return 0;
+  moe::GemmArgs a{nullptr, T, H, I, n_experts_total, k_total, fc, nullptr, nullptr,
+                  nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  return moe::fused_combine_ok(a) ? 1 : 0;
+}
+
+moe_status moe_fp4_grouped_gemm_combine(const uint16_t* x, int T, int H, int I,
+                                        int n_experts_total, int k_total, const int32_t* offsets,
+                                        const int32_t* sorted, const uint8_t* w13,
+                                        const uint8_t* w13_s, const uint8_t* w2,
+                                        const uint8_t* w2_s, moe_act_format f,
+                                        const float* topk_w, uint16_t* out, void* ws,
+                                        size_t ws_bytes, int stages, void* stream) {
+  return grouped_gemm(x, T, H, I, n_experts_total, k_total, offsets, sorted, w13, w13_s, w2, w2_s,
+                      f, nullptr, true, topk_w, out, ws, ws_bytes, stages, stream);
 }
 
 moe_status moe_combine_fixed_order(const float* partials, const float* topk_w, int T, int H,

@@ -121,6 +121,10 @@ static bool use_tiled(const GemmArgs& a) {
          (size_t)max_lds_per_block() >= tiled_lds_bytes(a.fmt);
 }
 
+bool fused_combine_ok(const GemmArgs& a) {
+  return !use_tiled(a) && fused_lds_bytes(a.T, a.k_total, a.I) <= (size_t)max_lds_per_block();
+}
+
 static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int stages,
                                   bool tiled, hipStream_t s) {
   const int BM = tiled ? tiled_rows() : 16;
@@ -165,7 +169,8 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p2.H = a.H;
     p2.I = a.I;
     p2.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks, queue};
-    if (tiled) launch_s2_tiled(p2, mt, a.fmt, s);
+    if (a.out) launch_s2c_stream(S2CArgs{p2, a.topk_w, a.out, a.T, a.k_total}, a.fmt, s);
+    else if (tiled) launch_s2_tiled(p2, mt, a.fmt, s);
     else launch_s2_stream(p2, mt, a.fmt, s);
   }
   return hipGetLastError();
@@ -177,6 +182,7 @@ hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int
   *variant = tiled ? 2 : 1;
   if (a.T == 0) return hipSuccess;
   if (a.fmt != 0 && a.fmt != 4) return hipErrorNotSupported;
+  if (a.out && !fused_combine_ok(a)) return hipErrorNotSupported;
   return launch_geometry(a, w, stages, tiled, s);
 }
 

@@ -94,6 +94,15 @@ struct S2Args {
   TileArgs t;
 };
 
+// Stage 2 fused with the fixed-order combine (few rows): out[t, :] is formed
+// from the topk weights and the down projections of token t's slots.
+struct S2CArgs {
+  S2Args s;                   // partials unused
+  const float* topk_w;        // [T, k_total]
+  uint16_t* out;              // bf16 [T, H]
+  int T, k_total;
+};
+
 // Stage-1 epilogue for one wave holding gate accumulators acc[0..NBW) and up
 // accumulators acc[NBW..2NBW) of 16-column tiles hc0 + 16b: SwiGLU and
 // per-32 quantisation of h. Lane (g, c16) holds rows 4g+i of columns

@@ -12,6 +12,12 @@ namespace moe {
 void launch_s1_stream(const S1Args& p, long mt, int fa, hipStream_t s);
 void launch_s2_stream(const S2Args& p, long mt, int fa, hipStream_t s);
 
+// Stage 2 + combine in one kernel for the streaming geometry: one workgroup
+// per 16 output columns holding every row's fp32 result in LDS.
+// fused_lds_bytes: its LDS need (0 when T * k_total rows are too many).
+size_t fused_lds_bytes(int T, int k_total, int I);
+void launch_s2c_stream(const S2CArgs& p, int fa, hipStream_t s);
+
 // LDS-tiled geometry (many rows per expert): row tiles of tiled_rows() rows.
 int tiled_rows();
 size_t tiled_lds_bytes(int fa);

@@ -95,19 +95,21 @@ struct Frag {
 template <int FA, int J, int NB>
 __device__ __forceinline__ void frag_codes(Frag<FA, J, NB>& f, const uint8_t* a_row,
                                            const uint8_t* const* b_rows, size_t b_off, int step,
-                                           int g) {
+                                           int g, bool av = true) {
   // the step's loads go out as one group, ahead of the products that follow
   // them in program order (the scheduler would otherwise interleave them with
   // those products and leave each load only a few instructions of lead)
   __builtin_amdgcn_sched_barrier(0);
+  if (av) {  // lanes of rows past the tile's end skip their activation loads
 #pragma unroll
-  for (int j = 0; j < J; ++j) {
-    if constexpr (FA == 0) {
-      const uint8_t* base = a_row + (size_t)step * 32 + 128 * j + 16 * g;
-      f.a[2 * j] = ld16<false>(base);
-      f.a[2 * j + 1] = ld16<false>(base + 64);
-    } else {
-      f.a[j] = ld16<false>(a_row + (size_t)(step + 4 * j + g) * 16);
+    for (int j = 0; j < J; ++j) {
+      if constexpr (FA == 0) {
+        const uint8_t* base = a_row + (size_t)step * 32 + 128 * j + 16 * g;
+        f.a[2 * j] = ld16<false>(base);
+        f.a[2 * j + 1] = ld16<false>(base + 64);
+      } else {
+        f.a[j] = ld16<false>(a_row + (size_t)(step + 4 * j + g) * 16);
+      }
     }
   }
 #pragma unroll
@@ -172,25 +174,30 @@ __device__ __forceinline__ void frag_mma(const Frag<FA, J, NB>& f, v4f* acc) {
 // (it stages the scale rows, so both latencies overlap). With nst even
 // (EVEN) the loop runs step pairs with no branch around a load; odd nst
 // (K/32 not a multiple of 8) takes a plain loop.
+// av: this lane's activation row is a row of the tile (lanes past the end
+// skip their activation loads and multiply zeros; rows are independent in
+// the product, and those accumulator rows are never stored).
 template <int FA, int J, int NB, bool EVEN, typename Pro>
 __device__ __forceinline__ void stream_k(const uint8_t* a_row, const uint8_t* const* b_rows,
                                          int nst, uint32_t xa, uint32_t wb, const uint32_t* wo,
-                                         int g, v4f* acc, Pro pro) {
+                                         int g, v4f* acc, Pro pro, bool av = true) {
   constexpr int kc = 4 * J;
   Frag<FA, J, NB> f0, f1;
+#pragma unroll
+  for (int i = 0; i < Frag<FA, J, NB>::kAV; ++i) f0.a[i] = f1.a[i] = v4u{0u, 0u, 0u, 0u};
   if constexpr (EVEN) {
-    frag_codes<FA, J, NB>(f0, a_row, b_rows, 0, 0, g);
+    frag_codes<FA, J, NB>(f0, a_row, b_rows, 0, 0, g, av);
     pro();
     wait_all_vmem();  // the first step and the scale rows are needed next anyway
     for (int c = 0; c + 2 < nst; c += 2) {  // f0 holds step c
-      frag_codes<FA, J, NB>(f1, a_row, b_rows, 0, (c + 1) * kc, g);
+      frag_codes<FA, J, NB>(f1, a_row, b_rows, 0, (c + 1) * kc, g, av);
       frag_scales<FA, J, NB>(f0, xa, wb, wo, c * kc, g);
       frag_mma<FA, J, NB>(f0, acc);
-      frag_codes<FA, J, NB>(f0, a_row, b_rows, 0, (c + 2) * kc, g);
+      frag_codes<FA, J, NB>(f0, a_row, b_rows, 0, (c + 2) * kc, g, av);
       frag_scales<FA, J, NB>(f1, xa, wb, wo, (c + 1) * kc, g);
       frag_mma<FA, J, NB>(f1, acc);
     }
-    frag_codes<FA, J, NB>(f1, a_row, b_rows, 0, (nst - 1) * kc, g);
+    frag_codes<FA, J, NB>(f1, a_row, b_rows, 0, (nst - 1) * kc, g, av);
     frag_scales<FA, J, NB>(f0, xa, wb, wo, (nst - 2) * kc, g);
     frag_mma<FA, J, NB>(f0, acc);
     frag_scales<FA, J, NB>(f1, xa, wb, wo, (nst - 1) * kc, g);
@@ -199,12 +206,19 @@ __device__ __forceinline__ void stream_k(const uint8_t* a_row, const uint8_t* co
     pro();
     wait_all_vmem();
     for (int c = 0; c < nst; ++c) {
-      frag_codes<FA, J, NB>(f0, a_row, b_rows, 0, c * kc, g);
+      frag_codes<FA, J, NB>(f0, a_row, b_rows, 0, c * kc, g, av);
       frag_scales<FA, J, NB>(f0, xa, wb, wo, c * kc, g);
       frag_mma<FA, J, NB>(f0, acc);
     }
   }
 }
+
+#ifndef MOE_MASKA_S1
+#define MOE_MASKA_S1 0
+#endif
+#ifndef MOE_MASKA_S2
+#define MOE_MASKA_S2 0
+#endif
 
 template <int FA, int J, int NBW, bool EVEN>
 __global__ __launch_bounds__(64) void s1_stream_kernel(S1Args p) {
@@ -250,7 +264,7 @@ __global__ __launch_bounds__(64) void s1_stream_kernel(S1Args p) {
         kb, lane);
     dma_rows16(lds + 16 * kb, p.w13s + (ebase + hc0) * kb, half, lane);
     dma_rows16(lds + 16 * kb + half, p.w13s + (ebase + p.I + hc0) * kb, half, lane);
-  });
+  }, !MOE_MASKA_S1 || c16 < nrows);
   s1_epilogue<FA, NBW>(acc, p, row0, nrows, hc0, g, c16);
 }
 
@@ -284,8 +298,270 @@ __global__ __launch_bounds__(64) void s2_stream_kernel(S2Args p) {
     dma_gather16(
         lds, [&](int r) { return p.hs + ((size_t)row0 + (r < nrows ? r : 0)) * kb; }, kb, lane);
     dma_rows16(lds + 16 * kb, p.w2s + rbase * kb, NB * 16 * kb, lane);
-  });
+  }, !MOE_MASKA_S2 || c16 < nrows);
   s2_epilogue<NBW>(acc, p, row0, nrows, nc0, g, c16);
+}
+
+// Stage 2 fused with the fixed-order combine, for few rows (decode): the
+// paper's small down consumer joined to the reducer (Historical down-consumer
+// pilot; Current TP8 native-AR results). A workgroup owns 16 output columns
+// and every row: its waves take the row tiles round-robin, stream those 16
+// W2 rows of the tile's expert once over the whole K extent with the same
+// products in the same order as s2_stream_kernel (so the same fp32 values),
+// and put each row's result into LDS at the row's assignment index. After
+// one barrier the workgroup forms out[t, columns] = bf16(acc), acc =
+// fmaf(topk_w[t, j], P[t*k_total + j], acc) for j = 0, 1, ... -- the combine
+// kernel's arithmetic -- so the output has the bits of s2_stream_kernel +
+// combine_kernel while no fp32 partial row reaches global memory.
+//
+// A wave streams about a dozen tiles one after another, each only a few K
+// steps long, so the start of a tile (its scale rows staged in LDS, its
+// first codes loaded) must not wait for the memory round trip: the next
+// tile's scale rows go out by DMA into the wave's second LDS slot during
+// the current tile's first step, and its first codes are loaded during the
+// current tile's last step. That DMA is written out (sdma4 / sdma16) so the
+// compiler does not turn it into waits for every outstanding load; one
+// explicit wait at each tile's first step covers it (see s2c_tiles).
+//
+// LDS: P [A][16] fp32 (zeroed first, so an assignment whose expert id was
+// invalid contributes 0), then two slots per wave of 16 activation and 16
+// weight scale rows.
+#ifndef MOE_FUSED_WAVES
+#define MOE_FUSED_WAVES 16
+#endif
+constexpr int kFusedWaves = MOE_FUSED_WAVES;
+
+// One 4-byte (sdma4) or 16-byte (sdma16) DMA instruction: lane i's bytes at
+// base + voff go to LDS byte lds_base + 4 i (16 i); base and lds_base are
+// wave-uniform.
+__device__ __forceinline__ void sdma4(const uint8_t* base, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2"
+               :
+               : "s"(lds_base), "v"(voff), "s"(base)
+               : "m0");
+}
+__device__ __forceinline__ void sdma16(const uint8_t* base, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_base), "v"(voff), "s"(base)
+               : "m0");
+}
+
+// Wait until at most N vector memory operations are outstanding.
+template <int N>
+__device__ __forceinline__ void tvmcnt_s() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xf00);
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t* l) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)l;
+}
+
+// Per-tile values of a wave: the tile's activation row of this lane (lane
+// c16 multiplies row c16; rows past the end repeat row 0), its W2 row and
+// the first W2 scale row.
+struct S2CTile {
+  int row0, nrows;
+  size_t rbase;  // first W2 row: expert * H + first column
+};
+
+__device__ __forceinline__ S2CTile s2c_tile(const int4& t, int H, int nc0) {
+  const int e = __builtin_amdgcn_readfirstlane(t.x);  // tile values are wave-uniform
+  return S2CTile{__builtin_amdgcn_readfirstlane(t.y), __builtin_amdgcn_readfirstlane(t.z),
+                 (size_t)e * H + nc0};
+}
+
+// Scale rows of a tile into the LDS slot at byte offset `slot`: the 16
+// activation scale rows gathered 4 bytes a lane, then the 16 consecutive W2
+// scale rows of the workgroup's columns, 16 bytes a lane.
+__device__ __forceinline__ void s2c_scales(uint8_t* lds, uint32_t slot, const S2Args& p,
+                                           const S2CTile& t, int kb, int lane) {
+  const int words = kb / 4;
+  const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr(lds) + slot);
+  for (int o = 0; o < 16 * words; o += 64) {
+    const int q = o + lane;
+    if (q < 16 * words) {
+      const int r = q / words;
+      sdma4(p.hs, (uint32_t)((t.row0 + (r < t.nrows ? r : 0)) * kb + 4 * (q % words)), base + 4 * o);
+    }
+  }
+  const uint8_t* src = p.w2s + t.rbase * kb;
+  for (int o = 0; o < 16 * kb; o += 1024)
+    if (o + 16 * lane < 16 * kb) sdma16(src, (uint32_t)(o + 16 * lane), base + 16 * kb + o);
+}
+
+// The tiles of one wave with the cross-tile prefetch; nst (K steps of 4J
+// blocks per tile) is even. fa holds even steps, fb odd steps.
+// Waits: the compiler waits for the code registers before each product; the
+// scale rows are read from LDS before the products, so the first step of a
+// tile waits explicitly for all but the step-1 codes just issued
+// (vmcnt(kStepLoads)): the tile's scale DMA was issued earlier (during the
+// previous tile, or the prologue, which waits for everything), and the
+// step-1 loads are kStepLoads unconditional instructions issued after it,
+// so the DMA is complete when at most kStepLoads loads are outstanding
+// (loads complete in order).
+template <int FA, int J>
+__device__ __forceinline__ void s2c_tiles(const S2CArgs& c, uint8_t* lds, float* P, int wave,
+                                          int lane, int nc0) {
+  const S2Args& p = c.s;
+  using F = Frag<FA, J, 1>;
+  constexpr int kAB = ActBytes<FA>::kBlock;
+  constexpr int kc = 4 * J;
+  constexpr int kStepLoads = F::kAV + J;  // code load instructions of one step
+  const int g = lane >> 4, c16 = lane & 15;
+  const int kb = p.I / 32, nst = kb / kc;
+  wave = __builtin_amdgcn_readfirstlane(wave);
+  const int ntl = *p.t.ntiles;
+  const int W = kFusedWaves;
+  int tj = wave;
+  if (tj >= ntl) return;
+  const uint32_t slot0 = (uint32_t)(c.T * c.k_total * 64 + wave * 64 * kb);
+  const uint32_t wo[1] = {(uint32_t)(c16 * kb)};
+  auto a_row = [&](const S2CTile& t) {
+    return p.hq + ((size_t)t.row0 + (c16 < t.nrows ? c16 : 0)) * (p.I / 32) * kAB;
+  };
+  auto b_row = [&](const S2CTile& t) { return p.w2 + (t.rbase + c16) * (p.I / 2); };
+
+  S2CTile tc = s2c_tile(p.t.tiles[tj], p.H, nc0);
+  int4 tn4 = p.t.tiles[tj + W < ntl ? tj + W : tj];
+  uint32_t slot = slot0;
+  F fa, fb;
+  {
+    const uint8_t* br = b_row(tc);
+    frag_codes<FA, J, 1>(fa, a_row(tc), &br, 0, 0, g);
+  }
+  s2c_scales(lds, slot, p, tc, kb, lane);
+  wait_all_vmem();
+  for (;;) {
+    const bool has_next = tj + W < ntl;
+    const S2CTile tn = s2c_tile(tn4, p.H, nc0);
+    const int4 tnn4 = p.t.tiles[tj + 2 * W < ntl ? tj + 2 * W : tj];
+    int arow[4];  // assignment index of the lane's accumulator rows 4g + i (-1: past the end)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rl = 4 * g + i;
+      const int a = p.sorted[tc.row0 + (rl < tc.nrows ? rl : tc.nrows - 1)];
+      arow[i] = rl < tc.nrows ? a : -1;
+    }
+    const uint8_t* ar = a_row(tc);
+    const uint8_t* br = b_row(tc);
+    // codes of the step after s + 1: step s + 2 of this tile, else step 0 of
+    // the next tile (of this tile again when there is none: every step issues
+    // the same loads, so the compiler's waits count exactly)
+    const uint8_t* arn = has_next ? a_row(tn) : ar;
+    const uint8_t* brn = has_next ? b_row(tn) : br;
+    const uint32_t xa = slot + c16 * kb, wb = slot + 16 * kb;
+    const uint32_t nslot = slot ^ (slot0 ^ (slot0 + 32 * kb));
+    v4f acc[1] = {v4f{0.f, 0.f, 0.f, 0.f}};
+    auto pair = [&](int s, bool first) {
+      frag_codes<FA, J, 1>(fb, ar, &br, 0, (s + 1) * kc, g);
+      if (first) {
+        tvmcnt_s<kStepLoads>();
+        if (has_next) s2c_scales(lds, nslot, p, tn, kb, lane);
+      }
+      frag_scales<FA, J, 1>(fa, xa, wb, wo, s * kc, g);
+      frag_mma<FA, J, 1>(fa, acc);
+      const bool last = s + 2 >= nst;
+      const uint8_t* a2 = last ? arn : ar;
+      const uint8_t* b2 = last ? brn : br;
+      frag_codes<FA, J, 1>(fa, a2, &b2, 0, last ? 0 : (s + 2) * kc, g);
+      frag_scales<FA, J, 1>(fb, xa, wb, wo, (s + 1) * kc, g);
+      frag_mma<FA, J, 1>(fb, acc);
+    };
+    pair(0, true);
+    for (int s = 2; s < nst; s += 2) pair(s, false);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (arow[i] >= 0) P[arow[i] * 16 + c16] = acc[0][i];
+    if (!has_next) break;
+    tj += W;
+    tc = tn;
+    tn4 = tnn4;
+    slot = nslot;
+  }
+}
+
+template <int FA, int J, bool EVEN>
+__global__ __launch_bounds__(64 * kFusedWaves) void s2c_stream_kernel(S2CArgs c) {
+  const S2Args& p = c.s;
+  constexpr int kAB = ActBytes<FA>::kBlock;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  float* P = reinterpret_cast<float*>(lds);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, c16 = lane & 15;
+  const int kb = p.I / 32, kt = c.k_total;
+  const int A = c.T * kt;
+  const int nc0 = blockIdx.x * 16;  // first output column of the workgroup
+
+  for (int i = threadIdx.x; i < A * 4; i += blockDim.x)
+    reinterpret_cast<v4f*>(P)[i] = v4f{0.f, 0.f, 0.f, 0.f};
+  __syncthreads();
+
+  if constexpr (EVEN) {
+    s2c_tiles<FA, J>(c, lds, P, wave, lane, nc0);
+  } else {  // odd step counts: one tile at a time
+    const uint32_t sb = (uint32_t)(A * 64 + wave * 64 * kb);  // this wave's scale rows
+    const int ntl = *p.t.ntiles;
+    for (int tj = wave; tj < ntl; tj += kFusedWaves) {
+      const int4 tile = p.t.tiles[tj];
+      const int row0 = tile.y, nrows = tile.z;
+      const size_t rbase = (size_t)tile.x * p.H + nc0;
+      int arow[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) arow[i] = 4 * g + i < nrows ? p.sorted[row0 + 4 * g + i] : -1;
+      const size_t ar = (size_t)row0 + (c16 < nrows ? c16 : 0);
+      const uint8_t* a_row = p.hq + ar * (p.I / 32) * kAB;
+      const uint8_t* b_rows[1] = {p.w2 + (rbase + c16) * (p.I / 2)};
+      const uint32_t wo[1] = {(uint32_t)(c16 * kb)};
+      v4f acc[1] = {v4f{0.f, 0.f, 0.f, 0.f}};
+      stream_k<FA, J, 1, false>(
+          a_row, b_rows, kb / (4 * J), sb + c16 * kb, sb + 16 * kb, wo, g, acc, [&]() {
+            dma_gather16(
+                lds + sb,
+                [&](int r) { return p.hs + ((size_t)row0 + (r < nrows ? r : 0)) * kb; }, kb,
+                lane);
+            dma_rows16(lds + sb + 16 * kb, p.w2s + rbase * kb, 16 * kb, lane);
+          });
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (arow[i] >= 0) P[arow[i] * 16 + c16] = acc[0][i];
+    }
+  }
+  __syncthreads();
+
+  // fixed-order combine of the workgroup's 16 columns, two per thread
+  for (int o = threadIdx.x; o < c.T * 8; o += blockDim.x) {
+    const int t = o >> 3, cp = 2 * (o & 7);
+    const float* wrow = c.topk_w + (size_t)t * kt;
+    const float* prow = P + (size_t)t * kt * 16 + cp;
+    float a0 = 0.f, a1 = 0.f;
+    for (int j = 0; j < kt; ++j) {
+      const float wj = wrow[j];
+      a0 = fmaf(wj, prow[16 * j], a0);
+      a1 = fmaf(wj, prow[16 * j + 1], a1);
+    }
+    *reinterpret_cast<uint32_t*>(c.out + (size_t)t * p.H + nc0 + cp) =
+        f32_to_bf16_rne(a0) | (f32_to_bf16_rne(a1) << 16);
+  }
+}
+
+size_t fused_lds_bytes(int T, int k_total, int I) {
+  return (size_t)T * k_total * 64 + (size_t)kFusedWaves * 64 * (I / 32);
+}
+
+template <int FA>
+static void launch_s2c(const S2CArgs& p, hipStream_t s) {
+  const int kb = p.s.I / 32;
+  const size_t lds = fused_lds_bytes(p.T, p.k_total, p.s.I);
+  const dim3 grid(p.s.H / 16), block(64 * kFusedWaves);
+  if (kb % 16 == 0) hipLaunchKernelGGL((s2c_stream_kernel<FA, 2, true>), grid, block, lds, s, p);
+  else if (kb % 8 == 0) hipLaunchKernelGGL((s2c_stream_kernel<FA, 1, true>), grid, block, lds, s, p);
+  else hipLaunchKernelGGL((s2c_stream_kernel<FA, 1, false>), grid, block, lds, s, p);
+}
+
+void launch_s2c_stream(const S2CArgs& p, int fa, hipStream_t s) {
+  if (fa == 0) launch_s2c<0>(p, s);
+  else launch_s2c<4>(p, s);
 }
 
 // Kernel instance: steps of 8 blocks (kb = K/32 a multiple of 16), else of

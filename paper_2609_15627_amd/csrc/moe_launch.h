@@ -50,11 +50,16 @@ struct GemmArgs {
   const uint8_t *w13, *w13_s, *w2, *w2_s;
   float* partials;
   uint8_t* ws;
+  const float* topk_w = nullptr;  // with out: stage 2 fused with the combine
+  uint16_t* out = nullptr;
 };
 // stages: bit 0 = activation quantisation + tile list, bit 1 = gate/up
 // (stage 1), bit 2 = down (stage 2). Writes the geometry variant used
 // (MOE_VARIANT_*) to *variant.
 hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int* variant);
+// Whether stage 2 can run fused with the combine for these dims (streaming
+// geometry chosen and every row's 16-column result fits one workgroup's LDS).
+bool fused_combine_ok(const GemmArgs& a);
 
 hipError_t launch_combine(const float* partials, const float* w, int T, int H, int k_total,
                           uint16_t* out, hipStream_t s);

@@ -39,6 +39,9 @@ _SIGNATURES = {
                                   _SZ, _P]),
     "moe_fp4_grouped_gemm_stages": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P,
                                          _P, _SZ, _I, _P]),
+    "moe_fp4_grouped_gemm_combine_supported": (_I, [_I, _I, _I, _I, _I, _I]),
+    "moe_fp4_grouped_gemm_combine": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P,
+                                          _P, _P, _SZ, _I, _P]),
     "moe_combine_fixed_order": (_I, [_P, _P, _I, _I, _I, _P, _P]),
     "moe_status_string": (ctypes.c_char_p, [_I]),
     "moe_last_variant": (_I, []),
@@ -257,6 +260,42 @@ def moe_fp4_grouped_gemm(x, offsets, sorted_, w13, w13_s, w2, w2_s, k_total, fmt
     return partials
 
 
+def moe_fp4_grouped_gemm_combine_supported(T, H, I, n_experts_total, k_total, fmt="e4m3"):
+    """True when the down projection can run fused with the combine."""
+    return bool(lib.moe_fp4_grouped_gemm_combine_supported(T, H, I, n_experts_total, k_total,
+                                                           ACT_FORMATS[fmt]))
+
+
+def moe_fp4_grouped_gemm_combine(x, offsets, sorted_, w13, w13_s, w2, w2_s, topk_w, fmt="e4m3",
+                                 out=None, ws=None, stream=None, stages=7):
+    """The grouped GEMM with its down projection fused with the fixed-order
+    combine: writes out [T, H] bf16 directly (bit-identical to
+    moe_fp4_grouped_gemm + moe_combine_fixed_order)."""
+    T, H = x.shape
+    NE, two_i, _ = w13.shape
+    I = two_i // 2
+    k_total = topk_w.shape[1]
+    _need(x, torch.bfloat16, (T, H), "x")
+    _need(offsets, torch.int32, (NE + 1,), "offsets")
+    _need(sorted_, torch.int32, (T * k_total,), "sorted")
+    _need(w13, torch.uint8, (NE, 2 * I, H // 2), "w13")
+    _need(w13_s, torch.uint8, (NE, 2 * I, H // 32), "w13_s")
+    _need(w2, torch.uint8, (NE, H, I // 2), "w2")
+    _need(w2_s, torch.uint8, (NE, H, I // 32), "w2_s")
+    _need(topk_w, torch.float32, (T, k_total), "topk_w")
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.bfloat16, device=x.device)
+    _need(out, torch.bfloat16, (T, H), "out")
+    if ws is None:
+        ws = torch.empty(max(moe_fp4_grouped_gemm_workspace_bytes(T, H, I, NE, k_total, fmt), 256),
+                         dtype=torch.uint8, device=x.device)
+    _check(lib.moe_fp4_grouped_gemm_combine(
+        _ptr(x), T, H, I, NE, k_total, _ptr(offsets), _ptr(sorted_), _ptr(w13), _ptr(w13_s),
+        _ptr(w2), _ptr(w2_s), ACT_FORMATS[fmt], _ptr(topk_w), _ptr(out), _ptr(ws), ws.numel(),
+        stages, _stream(stream)), "moe_fp4_grouped_gemm_combine")
+    return out
+
+
 def moe_combine_fixed_order(partials, topk_w, out=None, stream=None):
     T, kt = topk_w.shape
     H = partials.shape[1]
@@ -289,10 +328,18 @@ class MoELayer:
     at construction); ``forward`` enqueues only library kernels.
     """
 
-    def __init__(self, T, H, E, k, I, n_shared=0, fmt="e4m3", device="cuda"):
+    def __init__(self, T, H, E, k, I, n_shared=0, fmt="e4m3", device="cuda", fused=False):
+        """fused: run the down projection fused with the combine (same bits
+        as the two calls; raises MoeError when the dims do not allow it).
+        None picks it whenever the library supports the dims. Off by default:
+        at decode size the two-kernel path measured faster."""
         self.T, self.H, self.E, self.k, self.I, self.S = T, H, E, k, I, n_shared
         self.NE, self.kt = E + n_shared, k + n_shared
         self.fmt = fmt
+        ok = moe_fp4_grouped_gemm_combine_supported(T, H, I, self.NE, self.kt, fmt)
+        if fused and not ok:
+            raise MoeError(MOE_ERR_UNSUPPORTED, "fused down + combine for these dims")
+        self.fused = ok if fused is None else bool(fused)
         dev = torch.device(device)
         A = T * self.kt
         self.logits = torch.empty((T, E), dtype=torch.float32, device=dev)
@@ -304,7 +351,7 @@ class MoELayer:
                      torch.empty(A, dtype=torch.int32, device=dev))
         self.perm_ws = torch.empty(max(moe_permute_workspace_bytes(T, self.NE, self.kt), 256),
                                    dtype=torch.uint8, device=dev)
-        self.partials = torch.empty((A, H), dtype=torch.float32, device=dev)
+        self.partials = None if self.fused else torch.empty((A, H), dtype=torch.float32, device=dev)
         self.gemm_ws = torch.empty(
             max(moe_fp4_grouped_gemm_workspace_bytes(T, H, I, self.NE, self.kt, fmt), 256),
             dtype=torch.uint8, device=dev)
@@ -319,7 +366,8 @@ class MoELayer:
     def forward(self, x, weights, logits=None, w_router=None, stream=None, events=None):
         """Enqueue the layer. ``events``: optional list of 7 torch.cuda.Event
         recorded between the steps (route, permute, quantise, gate/up, down,
-        combine) for per-step timing."""
+        combine) for per-step timing; with the fused path "down" is the fused
+        down projection + combine and "combine" is empty."""
         w13, w13_s, w2, w2_s = weights
         ev = (lambda i: events[i].record(stream)) if events else (lambda i: None)
         ev(0)
@@ -330,6 +378,17 @@ class MoELayer:
         counts, offsets, srt, pos = moe_permute(self.ids, self.NE, out=self.perm, ws=self.perm_ws,
                                                 stream=stream)
         ev(2)
+        if self.fused:
+            g = (x, offsets, srt, w13, w13_s, w2, w2_s, self.w, self.fmt)
+            if events:
+                for i, st in enumerate((1, 2, 4)):
+                    moe_fp4_grouped_gemm_combine(*g, out=self.out, ws=self.gemm_ws, stream=stream,
+                                                 stages=st)
+                    ev(3 + i)
+            else:
+                moe_fp4_grouped_gemm_combine(*g, out=self.out, ws=self.gemm_ws, stream=stream)
+            ev(6)
+            return self.out
         g = (x, offsets, srt, w13, w13_s, w2, w2_s, self.kt, self.fmt)
         if events:
             for i, st in enumerate((1, 2, 4)):
