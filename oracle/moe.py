@@ -32,6 +32,12 @@ in a sum. The steps, in order, each cite what fixes them:
                           FP32 top-k reduction). The oracle sums in fp64 and
                           rounds once to bf16.
 
+The BF16 contract (``fmt='bf16'``, the paper's accepted large-prefill
+arithmetic: Large-M CK and the meaning of the earlier 6.42k result; Accepted
+large-prefill configuration) replaces steps 4 and 5's per-32 quantisation:
+x enters unquantised and h is rounded once to bf16 before the down
+projection; weights, partials and combine are unchanged.
+
 Readings where the paper is silent: softmax scoring
 with renormalisation over the k picks and routed scale 1; SwiGLU
 h = silu(gate) * up; rows 0..I-1 of W13 are gate, I..2I-1 are up; the shared
@@ -167,9 +173,15 @@ def expert_ffn(a, w13_packed, w13_scales, w2_packed, w2_scales, fmt):
     intermediate h is quantised per 32 along I before the down projection;
     ``fmt`` None skips that (the unquantised reading used for reporting only).
 
+    ``fmt`` 'bf16' is the BF16 contract (Large-M CK and the meaning of the
+    earlier 6.42k result; Historical down-consumer pilot): no per-32
+    quantisation; h is rounded once to bf16 (nearest, ties to even) and the
+    down projection consumes that rounded intermediate.
+
     Returns dict(g, u, h, hq, hs, hd, p): gate, up, intermediate, its codes and
-    scale bytes (None without fmt), the dequantised intermediate the down
-    projection consumes, and the partial outputs p [M, H].
+    scale bytes (None without fmt; for 'bf16' hq holds the bf16 bits and hs
+    is None), the intermediate the down projection consumes, and the partial
+    outputs p [M, H].
     """
     w13 = mx.dequant_fp4(w13_packed, w13_scales)
     w2 = mx.dequant_fp4(w2_packed, w2_scales)
@@ -180,6 +192,9 @@ def expert_ffn(a, w13_packed, w13_scales, w2_packed, w2_scales, fmt):
     if fmt is None:
         hq = hs = None
         hd = h
+    elif fmt == "bf16":
+        hq, hs = mx.f64_to_bf16(h), None
+        hd = mx.bf16_to_f64(hq)
     else:
         hq, hs = mx.mx_quantize(h, fmt)
         hd = mx.mx_dequantize(hq, hs, fmt)
@@ -200,8 +215,9 @@ def layer(x_bits, w13, w13s, w2, w2s, *, k, n_shared=0, logits=None, wr_bits=Non
     [NE, ...] or any object whose ``[e]`` returns that expert's arrays), with
     NE = E + n_shared and the shared expert at index E. Give either fp32
     ``logits`` [T, E] or bf16 router weights ``wr_bits`` [E, H].
-    ``fmt``: activation element format ('e4m3', 'e2m3', 'e2m1') or None for no
-    activation quantisation.
+    ``fmt``: activation element format ('e4m3', 'e2m3', 'e2m1'), 'bf16' for
+    the BF16 contract (x exact, h rounded to bf16; see expert_ffn) or None
+    for no activation quantisation.
 
     Returns a dict with ``out`` (bf16 bits [len(tokens), H]), ``out_f64`` and
     the routing and permutation arrays for all T tokens; with ``keep`` also the
@@ -229,7 +245,7 @@ def layer(x_bits, w13, w13s, w2, w2s, *, k, n_shared=0, logits=None, wr_bits=Non
 
     # activations are quantised per token row, so the subset is exact
     x64 = mx.bf16_to_f64(np.asarray(x_bits)[tokens])
-    if fmt is None:
+    if fmt is None or fmt == "bf16":
         xq = xs = None
         xd = x64
     else:

@@ -113,6 +113,15 @@ def quantize_row(vals, fmt):
     return codes, scales, deq
 
 
+def round_bf16(v):
+    """Nearest bf16 value (8 significant bits, ties to the even significand) of
+    a finite float in the normal bf16 range, by Python's round-half-even."""
+    if v == 0:
+        return v
+    m, e = math.frexp(v)                   # v = m * 2**e, 0.5 <= |m| < 1
+    return round(m * 256) * 2.0 ** (e - 8)
+
+
 def dequant_weight(packed_row, scale_row):
     """One weight row: packed bytes (low nibble first) and E8M0 bytes -> values."""
     tab = paper_e2m1_table()
@@ -128,7 +137,8 @@ def layer(x, logits, w13, w13s, w2, w2s, k, n_shared, fmt):
     """The routed layer by explicit loops (lists of Python floats).
 
     x: [T][H] floats; logits: [T][E]; w13[e]: [2I][H/2] bytes, w13s[e]: [2I][H/32],
-    w2[e]: [H][I/2], w2s[e]: [H][I/32]. fmt None: no activation quantisation.
+    w2[e]: [H][I/2], w2s[e]: [H][I/32]. fmt None: no activation quantisation;
+    'bf16': x unquantised, h rounded to bf16.
     Returns out [T][H] (unrounded floats).
     """
     T, H = len(x), len(x[0])
@@ -150,7 +160,7 @@ def layer(x, logits, w13, w13s, w2, w2s, k, n_shared, fmt):
         weights = [v / tot for v in z]
         experts = chosen + ([E] if n_shared else [])
         weights = weights + ([1.0] if n_shared else [])
-        xa = quantize_row(x[t], fmt)[2] if fmt else list(x[t])
+        xa = quantize_row(x[t], fmt)[2] if fmt and fmt != "bf16" else list(x[t])
         acc = [0.0] * H
         for e, wt in zip(experts, weights):
             I = len(w13[e]) // 2
@@ -161,7 +171,10 @@ def layer(x, logits, w13, w13s, w2, w2s, k, n_shared, fmt):
             for n in range(I):
                 sig = 1.0 / (1.0 + math.exp(-g[n])) if g[n] > -700 else 0.0
                 h.append(g[n] * sig * u[n])
-            ha = quantize_row(h, fmt)[2] if fmt else h
+            if fmt == "bf16":
+                ha = [round_bf16(v) for v in h]
+            else:
+                ha = quantize_row(h, fmt)[2] if fmt else h
             for n in range(H):
                 w2d = dequant_weight(w2[e][n], w2s[e][n])
                 acc[n] += wt * sum(ha[i] * w2d[i] for i in range(I))

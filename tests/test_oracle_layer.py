@@ -128,7 +128,7 @@ def _tiny_case(seed, t, h, i, e, k, n_shared):
     return cfg, inp
 
 
-@pytest.mark.parametrize("fmt", ["e4m3", "e2m3", "e2m1", None])
+@pytest.mark.parametrize("fmt", ["e4m3", "e2m3", "e2m1", "bf16", None])
 @pytest.mark.parametrize("shape", [(3, 32, 32, 4, 2, 0), (2, 64, 32, 3, 1, 1), (4, 32, 64, 4, 4, 1)])
 def test_brute_force_layer(fmt, shape):
     """Explicit-loop layer agrees with the numpy oracle to 1e-12 (relative to the row max)."""
