@@ -65,14 +65,22 @@ typedef enum {
 typedef enum {
   MOE_ACT_MXFP8_E4M3 = 0, /* 1 byte per element */
   MOE_ACT_MXFP6_E2M3 = 1, /* reserved: not implemented in this build */
-  MOE_ACT_MXFP4_E2M1 = 2  /* 2 elements per byte, low nibble first */
+  MOE_ACT_MXFP4_E2M1 = 2, /* 2 elements per byte, low nibble first */
+  /* The paper's BF16 contract (Large-M CK and the meaning of the earlier
+   * 6.42k result; Accepted large-prefill configuration): x is not quantised,
+   * FP4 weights are expanded to bf16 (exactly, for scale bytes <= 252), G and
+   * U accumulate in fp32 and h = SwiGLU(G, U) is rounded once to bf16
+   * (nearest, ties to even) before the down projection; partials and the
+   * combine are unchanged. Grouped GEMM only (not moe_quantize_act). */
+  MOE_ACT_BF16 = 3
 } moe_act_format;
 
 /* Geometry variants reported by moe_last_variant(). */
 enum {
   MOE_VARIANT_NONE = 0,
   MOE_VARIANT_STREAM = 1, /* weight-streaming geometry for few rows per expert (decode) */
-  MOE_VARIANT_TILED = 2   /* LDS-tiled MFMA geometry for many rows per expert (prefill) */
+  MOE_VARIANT_TILED = 2,  /* LDS-tiled MFMA geometry for many rows per expert (prefill) */
+  MOE_VARIANT_BF16 = 3    /* MOE_ACT_BF16: LDS-tiled bf16 geometry, any batch size */
 };
 
 /* Limits checked by the validators. */
@@ -231,7 +239,8 @@ size_t moe_fp4_grouped_gemm_workspace_bytes(int T, int H, int I, int n_experts_t
 
 /* Byte offsets of the workspace regions: [0] x codes [T, H*bits/8], [1] x
  * scales [T, H/32], [2] h codes [T*k_total, I*bits/8] in sorted-row order,
- * [3] h scales [T*k_total, I/32], [4] tile list, [5] total bytes. */
+ * [3] h scales [T*k_total, I/32], [4] tile list, [5] total bytes. With
+ * MOE_ACT_BF16 regions 0, 1 and 3 are empty and region 2 holds h as bf16. */
 #define MOE_WS_REGIONS 6
 moe_status moe_fp4_grouped_gemm_workspace_layout(int T, int H, int I, int n_experts_total,
                                                  int k_total, moe_act_format f,

@@ -26,6 +26,7 @@ int fmt_code(moe_act_format f) {
     case MOE_ACT_MXFP8_E4M3: return 0;
     case MOE_ACT_MXFP6_E2M3: return 2;
     case MOE_ACT_MXFP4_E2M1: return 4;
+    case MOE_ACT_BF16: return moe::kFmtBf16;
   }
   return -1;
 }
@@ -146,7 +147,7 @@ moe_status moe_permute(const int32_t* topk_ids, int T, int n_experts_total, int 
 moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f, uint8_t* codes,
                             uint8_t* scales, void* stream) {
   const int fc = fmt_code(f);
-  if (fc < 0 || rows < 0 || K <= 0 || K % 32) return MOE_ERR_INVALID_ARG;
+  if (fc < 0 || fc == moe::kFmtBf16 || rows < 0 || K <= 0 || K % 32) return MOE_ERR_INVALID_ARG;
   if (rows > 0 && (!x || !codes || !scales)) return MOE_ERR_INVALID_ARG;
   if (!aligned(x, 16) || !aligned(codes, 16)) return MOE_ERR_INVALID_ARG;
   return launched(moe::launch_quantize_act(x, rows, K, fc, codes, scales, as_stream(stream)));

@@ -88,10 +88,11 @@ GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt) 
   const size_t bits = act_bits(fmt);
   GemmWorkspace w;
   size_t o = 0;
-  w.off[0] = o;  o += al((size_t)T * H * bits / 8);
-  w.off[1] = o;  o += al((size_t)T * (H / 32));
+  const bool mx = fmt != kFmtBf16;  // the BF16 contract has no x codes and no scales
+  w.off[0] = o;  o += mx ? al((size_t)T * H * bits / 8) : 0;
+  w.off[1] = o;  o += mx ? al((size_t)T * (H / 32)) : 0;
   w.off[2] = o;  o += al(A * I * bits / 8);
-  w.off[3] = o;  o += al(A * (I / 32));
+  w.off[3] = o;  o += mx ? al(A * (I / 32)) : 0;
   // tile list (int4 x bound), its count, the chunk list (int2 x bound), its
   // count, the work queue
   const size_t tb = (size_t)tile_bound((long)A, NE, 16) + 1;
@@ -122,12 +123,14 @@ static bool use_tiled(const GemmArgs& a) {
 }
 
 bool fused_combine_ok(const GemmArgs& a) {
-  return !use_tiled(a) && fused_lds_bytes(a.T, a.k_total, a.I) <= (size_t)max_lds_per_block();
+  return a.fmt != kFmtBf16 && !use_tiled(a) &&
+         fused_lds_bytes(a.T, a.k_total, a.I) <= (size_t)max_lds_per_block();
 }
 
 static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int stages,
                                   bool tiled, hipStream_t s) {
-  const int BM = tiled ? tiled_rows() : 16;
+  const bool bf = a.fmt == kFmtBf16;
+  const int BM = bf ? bf16_rows() : (tiled ? tiled_rows() : 16);
   const long A = (long)a.T * a.k_total;
   const int mt = tile_bound(A, a.NE, BM);
   const int tb = tile_bound(A, a.NE, 16) + 1;
@@ -137,14 +140,16 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
   int* nchunks = reinterpret_cast<int*>(chunks + tb);
   int* queue = nchunks + 4;
   if (stages & 1) {
-    hipError_t err = launch_quantize_act(a.x, a.T, a.H, a.fmt, a.ws + w.off[0], a.ws + w.off[1], s);
-    if (err != hipSuccess) return err;
+    if (!bf) {  // the BF16 contract feeds x to the matrix cores as it is
+      hipError_t err = launch_quantize_act(a.x, a.T, a.H, a.fmt, a.ws + w.off[0], a.ws + w.off[1], s);
+      if (err != hipSuccess) return err;
+    }
     hipLaunchKernelGGL(build_tiles_kernel, dim3(1), dim3(1024), (a.NE + 1) * sizeof(int), s,
                        a.offsets, a.NE, BM, tiles, ntiles, chunks, nchunks, queue);
   }
   if (stages & 2) {
     S1Args p1;
-    p1.xq = a.ws + w.off[0];
+    p1.xq = bf ? reinterpret_cast<const uint8_t*>(a.x) : a.ws + w.off[0];
     p1.xs = a.ws + w.off[1];
     p1.sorted = a.sorted;
     p1.w13 = a.w13;
@@ -155,7 +160,8 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p1.I = a.I;
     p1.k_total = a.k_total;
     p1.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks, queue};
-    if (tiled) launch_s1_tiled(p1, mt, a.fmt, s);
+    if (bf) launch_s1_bf16(p1, mt, s);
+    else if (tiled) launch_s1_tiled(p1, mt, a.fmt, s);
     else launch_s1_stream(p1, mt, a.fmt, s);
   }
   if (stages & 4) {
@@ -170,6 +176,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p2.I = a.I;
     p2.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks, queue};
     if (a.out) launch_s2c_stream(S2CArgs{p2, a.topk_w, a.out, a.T, a.k_total}, a.fmt, s);
+    else if (bf) launch_s2_bf16(p2, mt, s);
     else if (tiled) launch_s2_tiled(p2, mt, a.fmt, s);
     else launch_s2_stream(p2, mt, a.fmt, s);
   }
@@ -179,9 +186,9 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
 hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int* variant) {
   const GemmWorkspace w = gemm_workspace(a.T, a.H, a.I, a.NE, a.k_total, a.fmt);
   const bool tiled = use_tiled(a);
-  *variant = tiled ? 2 : 1;
+  *variant = a.fmt == kFmtBf16 ? 3 : (tiled ? 2 : 1);
   if (a.T == 0) return hipSuccess;
-  if (a.fmt != 0 && a.fmt != 4) return hipErrorNotSupported;
+  if (a.fmt != 0 && a.fmt != 4 && a.fmt != kFmtBf16) return hipErrorNotSupported;
   if (a.out && !fused_combine_ok(a)) return hipErrorNotSupported;
   return launch_geometry(a, w, stages, tiled, s);
 }

@@ -1,0 +1,254 @@
+// f2: the grouped expert GEMM under the paper's BF16 contract (Large-M CK and
+// the meaning of the earlier 6.42k result; Accepted large-prefill
+// configuration): activations are not quantised, FP4 weights are expanded to
+// BF16, products accumulate in fp32, the intermediate h is rounded once to
+// bf16 before the down projection (Historical down-consumer pilot: the down
+// consumer reads the already-rounded BF16 intermediate), and stage 2 keeps
+// unique-slot fp32 partials for the fixed-order combine.
+//
+// The paper materialised the expert shard in BF16 in HBM; here the expansion
+// happens in registers at operand-read time (v_cvt_scalef32_pk_bf16_fp4:
+// two FP4 codes times the block's E8M0 scale to two bf16, exact), so weights
+// still stream as 4.5 bits per value.
+//
+// One geometry for every batch size: workgroup tile 128 sorted rows x 128
+// weight rows (stage 1: 64 gate rows and the matching 64 up rows, so SwiGLU
+// stays in the workgroup), K in steps of 32 (one scale block); 4 waves of
+// 64 x 64, each 2 x 2 products of 32x32x16 bf16 per 16 K elements. The
+// product is transposed (weights are the row operand), so a lane's
+// accumulator holds 16 weight-row values of one activation row.
+//
+// Data movement: activation rows (64 bytes a step) and weight rows (16 bytes
+// of FP4 a step) go global -> LDS by DMA through a ring of 4 steps; every
+// wave issues exactly 3 DMA instructions per step (rows past the tile's end
+// repeat its first row; a stage past the last step reloads the last one), so
+// one explicit vmcnt wait per step counts exactly. The tile's weight scale
+// rows (K/32 bytes each) are staged once. Activation rows are chunk-swizzled
+// (16-byte chunk c of row r at c ^ ((r >> 2) & 3)) so the operand reads do
+// not collide in LDS banks.
+#include "gemm_common.h"
+#include "gemm_launch.h"
+
+namespace moe {
+
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+constexpr int kBM = 128;              // sorted rows per tile
+constexpr int kBN = 128;              // weight rows per tile
+constexpr int kBK = 32;               // K elements per step
+constexpr int kRingN = 4;             // steps in the LDS ring
+constexpr int kAS = kBM * kBK * 2;    // activation bytes per step (8 KiB)
+constexpr int kBS = kBN * kBK / 2;    // weight bytes per step (2 KiB)
+constexpr int kSlot = kAS + kBS;
+constexpr int kRingBytes = kRingN * kSlot;
+constexpr int kDmaPerStep = 3;        // DMA instructions per wave per step
+
+struct BfArgs {
+  const uint8_t* act;       // stage 1: x bf16 [T, K]; stage 2: h bf16 [A, K] in sorted-row order
+  const int32_t* sorted;
+  const uint8_t *w, *ws;    // FP4 codes [NE, N, K/2], E8M0 scales [NE, N, K/32]
+  uint8_t* hout;            // stage 1: h bf16 [A, I] in sorted-row order
+  float* partials;          // stage 2: [A, H] indexed by assignment
+  int K, N, I, H, k_total;  // N: weight rows per expert (2I or H)
+  TileArgs t;
+};
+
+size_t bf16_lds_bytes(int K) { return kRingBytes + (size_t)kBN * (K / 32); }
+
+// E8M0 byte -> 2^(b - 127) as fp32 (b = 0: the subnormal 2^-127; 255: NaN).
+__device__ __forceinline__ float e8m0_f32(uint32_t b) {
+  uint32_t bits = b << 23;
+  bits = b == 0 ? 0x00400000u : bits;
+  bits = b == 255 ? 0x7fc00000u : bits;
+  return __uint_as_float(bits);
+}
+
+// 8 FP4 codes (one dword, element 2i in the low nibble of byte i) times the
+// scale -> 8 bf16 in K order.
+__device__ __forceinline__ v8bf fp4x8_bf16(uint32_t d, float s) {
+  const v2bf p0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(d, s, 0);
+  const v2bf p1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(d, s, 1);
+  const v2bf p2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(d, s, 2);
+  const v2bf p3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(d, s, 3);
+  return v8bf{p0[0], p0[1], p1[0], p1[1], p2[0], p2[1], p3[0], p3[1]};
+}
+
+__device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
+  return f32_to_bf16_rne(a) | (f32_to_bf16_rne(b) << 16);
+}
+
+// ST = 1: gate/up + SwiGLU + bf16 h; ST = 2: down -> fp32 partials.
+template <int ST>
+__global__ __launch_bounds__(256) void bf16_gemm_kernel(BfArgs p) {
+  int4 tile;
+  int nt;
+  if (!tile_of_block(p.t, &tile, &nt)) return;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int e = __builtin_amdgcn_readfirstlane(tile.x);
+  const int row0 = __builtin_amdgcn_readfirstlane(tile.y);
+  const int nrows = __builtin_amdgcn_readfirstlane(tile.z);
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int lane = threadIdx.x & 63, l32 = lane & 31, h = lane >> 5;
+  const int kb = p.K / 32, nk = kb;
+  const uint32_t ring = __builtin_amdgcn_readfirstlane(lds_addr(lds));
+  uint8_t* sc_lds = lds + kRingBytes;  // [kBN][kb] weight scale bytes
+
+  // tile weight row r -> expert weight row
+  auto wrow = [&](int r) {
+    return ST == 1 ? (r < 64 ? 64 * nt + r : p.I + 64 * nt + r - 64) : kBN * nt + r;
+  };
+  const uint8_t* wbase = p.w + (size_t)e * p.N * (p.K / 2);
+  const uint8_t* sbase = p.ws + (size_t)e * p.N * kb;
+
+  // DMA sources of this lane: activation instructions i = 0, 1 cover tile
+  // rows 32 w + 16 i + lane / 4, chunk slot lane % 4 (global chunk slot ^
+  // f(row)); the weight instruction covers tile row 32 w + lane (lanes < 32).
+  uint32_t aoff[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = 32 * w + 16 * i + (lane >> 2);
+    const int rr = row0 + (r < nrows ? r : 0);
+    const int src = ST == 1 ? p.sorted[rr] / p.k_total : rr;
+    const int c = (lane & 3) ^ ((r >> 2) & 3);
+    aoff[i] = (uint32_t)src * (uint32_t)(p.K * 2) + 16 * c;
+  }
+  const uint32_t boff = (uint32_t)wrow(32 * w + l32) * (uint32_t)(p.K / 2);
+  // step s's slot; past the last step the slot gets the last step again
+  auto issue = [&](int s) {
+    const uint32_t slot = ring + (uint32_t)((s % kRingN) * kSlot);
+    const int step = s < nk ? s : nk - 1;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      sdma16(p.act, aoff[i] + (uint32_t)step * 64, slot + (32 * w + 16 * i) * 64);
+    if (lane < 32) sdma16(wbase, boff + (uint32_t)step * 16, slot + kAS + 32 * w * 16);
+  };
+
+  // weight scale rows of the tile (stage 1: the 64 gate rows, then the 64 up rows)
+  {
+    const int nblk = ST == 1 ? 2 : 1, rows = kBN / nblk, bytes = rows * kb;
+    const uint32_t sl = ring + kRingBytes;
+    for (int b = 0; b < nblk; ++b) {
+      const uint8_t* src = sbase + (size_t)wrow(b * rows) * kb;
+      for (int o = 1024 * w; o < bytes; o += 4096)
+        if (o + 16 * lane < bytes) sdma16(src, (uint32_t)(o + 16 * lane), sl + b * bytes + o);
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < kRingN - 1; ++s) issue(s);
+  // every wave's share of the scale rows and of the first stages has landed
+  // before any wave reads LDS
+  tvmcnt_s<0>();
+  asm volatile("s_barrier" ::: "memory");
+
+  // operand rows of this lane: weight blocks nb (tile rows), activation blocks mb
+  const int wn = w >> 1, wm = w & 1;
+  int brow[2], arow[2];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+    brow[nb] = ST == 1 ? 64 * nb + 32 * wn + l32 : 64 * wn + 32 * nb + l32;
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) arow[mb] = 64 * wm + 32 * mb + l32;
+
+  v16f acc[2][2];
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = v16f{};
+
+  uint32_t scb[2];  // scale bytes of the next step (read one step ahead)
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) scb[nb] = sc_lds[brow[nb] * kb];
+  for (int k = 0; k < nk; ++k) {
+    // this wave's DMA of step k landed (steps k+1, k+2 may be in flight), and
+    // after the barrier every wave's has, and every wave is done with step k-1
+    tvmcnt_s<(kRingN - 2) * kDmaPerStep>();
+    asm volatile("s_barrier" ::: "memory");
+    issue(k + kRingN - 1);  // into the slot of step k - 1
+    const uint8_t* as = lds + (k % kRingN) * kSlot;
+    const uint8_t* bs = as + kAS;
+    float sc[2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      sc[nb] = e8m0_f32(scb[nb]);
+      scb[nb] = sc_lds[brow[nb] * kb + (k + 1 < nk ? k + 1 : k)];
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      v8bf wa[2], xb[2];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        wa[nb] = fp4x8_bf16(*reinterpret_cast<const uint32_t*>(bs + brow[nb] * 16 + 8 * ks + 4 * h),
+                            sc[nb]);
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+        const int r = arow[mb];
+        xb[mb] = *reinterpret_cast<const v8bf*>(as + r * 64 + 16 * ((2 * ks + h) ^ ((r >> 2) & 3)));
+      }
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[nb], xb[mb], acc[mb][nb], 0, 0, 0);
+    }
+  }
+  tvmcnt_s<0>();  // the ring's last (repeated) loads
+
+  // D: lane l, element i = weight row 8 (i / 4) + 4 h + i % 4 of the block,
+  // activation row l % 32 of the block.
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+    const int m = arow[mb];
+    if (m >= nrows) continue;
+    if constexpr (ST == 1) {
+      uint8_t* dst = p.hout + ((size_t)(row0 + m) * p.I + 64 * nt + 32 * wn + 4 * h) * 2;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float hv[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float G = acc[mb][0][4 * q + j], U = acc[mb][1][4 * q + j];
+          hv[j] = G * U / (1.0f + expf(-G));
+        }
+        *reinterpret_cast<uint2*>(dst + 16 * q) =
+            make_uint2(bf16_pair(hv[0], hv[1]), bf16_pair(hv[2], hv[3]));
+      }
+    } else {
+      const size_t a = (size_t)p.sorted[row0 + m];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        float* dst = p.partials + a * p.H + kBN * nt + 64 * wn + 32 * nb + 4 * h;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<v4f*>(dst + 8 * q) =
+              v4f{acc[mb][nb][4 * q], acc[mb][nb][4 * q + 1], acc[mb][nb][4 * q + 2],
+                  acc[mb][nb][4 * q + 3]};
+      }
+    }
+  }
+}
+
+int bf16_rows() { return kBM; }
+
+template <int ST>
+static void launch_bf(const BfArgs& p0, long mt, int n_ntiles, hipStream_t s) {
+  BfArgs p = p0;
+  p.t.n_ntiles = n_ntiles;
+  p.t.ngroup = n_group_of(n_ntiles);
+  const long n = mt * n_ntiles;
+  hipLaunchKernelGGL((bf16_gemm_kernel<ST>), dim3((int)((n + 7) / 8 * 8)), dim3(256),
+                     bf16_lds_bytes(p.K), s, p);
+}
+
+void launch_s1_bf16(const S1Args& a, long mt, hipStream_t s) {
+  BfArgs p{a.xq, a.sorted, a.w13, a.w13s, a.hq, nullptr, a.H, 2 * a.I, a.I, a.H, a.k_total, a.t};
+  launch_bf<1>(p, mt, a.I / 64, s);
+}
+
+void launch_s2_bf16(const S2Args& a, long mt, hipStream_t s) {
+  BfArgs p{a.hq, a.sorted, a.w2, a.w2s, nullptr, a.partials, a.I, a.H, a.I, a.H, 1, a.t};
+  launch_bf<2>(p, mt, a.H / kBN, s);
+}
+
+}  // namespace moe

@@ -30,6 +30,43 @@ __device__ __forceinline__ v4u ld16(const uint8_t* p) {
   return *q;
 }
 
+// LDS DMA written out so that the compiler neither waits for it nor orders
+// LDS reads behind it: the caller's explicit vmcnt waits (loads complete in
+// order) and barriers cover it.
+// One 4-byte (sdma4) or 16-byte (sdma16) DMA instruction: lane i's bytes at
+// base + voff go to LDS byte lds_base + 4 i (16 i); base and lds_base are
+// wave-uniform.
+// A wave-uniform pointer held in scalar registers.
+__device__ __forceinline__ const uint8_t* sptr(const uint8_t* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const uint8_t*>(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ void sdma4(const uint8_t* base, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2"
+               :
+               : "s"(lds_base), "v"(voff), "s"(sptr(base))
+               : "m0");
+}
+__device__ __forceinline__ void sdma16(const uint8_t* base, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_base), "v"(voff), "s"(sptr(base))
+               : "m0");
+}
+
+// Wait until at most N vector memory operations are outstanding.
+template <int N>
+__device__ __forceinline__ void tvmcnt_s() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xf00);
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t* l) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)l;
+}
+
 // Scale bytes of the step's 4J blocks starting at p (4-byte aligned); lane
 // group g takes block 4j + g for product j: byte g of word j goes to byte j.
 template <int J>

@@ -18,6 +18,13 @@ void launch_s2_stream(const S2Args& p, long mt, int fa, hipStream_t s);
 size_t fused_lds_bytes(int T, int k_total, int I);
 void launch_s2c_stream(const S2CArgs& p, int fa, hipStream_t s);
 
+// BF16 contract (bf16 activations, FP4 weights expanded to bf16 in
+// registers, bf16 intermediate): one LDS-tiled geometry of bf16_rows() rows.
+int bf16_rows();
+size_t bf16_lds_bytes(int K);
+void launch_s1_bf16(const S1Args& p, long mt, hipStream_t s);
+void launch_s2_bf16(const S2Args& p, long mt, hipStream_t s);
+
 // LDS-tiled geometry (many rows per expert): row tiles of tiled_rows() rows.
 int tiled_rows();
 size_t tiled_lds_bytes(int fa);

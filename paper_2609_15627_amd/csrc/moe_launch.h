@@ -33,6 +33,9 @@ hipError_t launch_permute(const int32_t* ids, int T, int NE, int k_total, int32_
                           hipStream_t s);
 
 // fmt: 0 = e4m3, 2 = e2m3, 4 = e2m1 (matrix-core operand codes)
+// Internal activation format codes: 0 MXFP8 e4m3, 2 MXFP6 e2m3, 4 MXFP4
+// e2m1, kFmtBf16 the BF16 contract (bf16 activations, no scales).
+constexpr int kFmtBf16 = 16;
 int act_bits(int fmt);
 hipError_t launch_quantize_act(const uint16_t* x, long rows, int K, int fmt, uint8_t* codes,
                                uint8_t* scales, hipStream_t s);
