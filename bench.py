@@ -133,8 +133,9 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True, fused=False):
     touched = int((counts > 0).sum())
     A = cfg.A
     w13b, w2b = expert_bytes(cfg.H, cfg.I)
-    xb = cfg.T * cfg.H * (1 + 1 / 32)                      # MXFP8 x codes + scales
-    hb = A * cfg.I * (1 + 1 / 32)                           # MXFP8 h codes + scales
+    eb = {"e4m3": 1 + 1 / 32, "e2m1": 0.5 + 1 / 32, "bf16": 2.0}[fmt]  # bytes per activation
+    xb = cfg.T * cfg.H * eb                                 # x codes + scales (bf16: x itself)
+    hb = A * cfg.I * eb                                     # h codes + scales (bf16: h)
     gate_up_bytes = touched * w13b + xb + hb
     # down writes fp32 partial rows, or (fused with the combine) the bf16 output
     down_bytes = touched * w2b + hb + (cfg.T * cfg.H * 2 if layer.fused else A * cfg.H * 4)
@@ -177,6 +178,31 @@ def measure_workload(name, steps, fmt, use_graph, weights_np=None):
             "layer_GBps": gb, "layer_hbm_frac": gb / HBM_PEAK_GBS,
             "layer_TFLOPs": tf, "layer_frac_of_fp8_peak": tf / MFMA_PEAK_FP8_TFLOPS,
             "layer_frac_of_fp4_peak": tf / MFMA_PEAK_FP4_TFLOPS}
+
+
+MFMA_PEAK_BF16_TFLOPS = 2500.0  # dense bf16
+
+
+def measure_bf16_contract(weights_np, steps, use_graph):
+    """The BF16 contract (bf16 activations, FP4 weights expanded to bf16 in
+    registers, bf16 intermediate) on the decode and 8K prefill workloads:
+    layer time, and stage 1 against the HBM roofline (decode) and the dense
+    bf16 matrix-core peak (prefill)."""
+    import synth
+    out = {}
+    for name, n in (("decode", steps), ("prefill8k", max(3, steps // 10))):
+        cfg = synth.CONFIGS[name]
+        log(f"measuring the BF16 contract on {name}")
+        r = measure(cfg, weights_np, n, 2, "bf16", use_graph)
+        gu = r["stage_ms"]["gate_up"] * 1e-3
+        out[name] = {"ms_per_step": r["ms_per_step"], "tokens_per_s": r["tokens_per_s"],
+                     "stage_ms": r["stage_ms"], "variant": r["variant"],
+                     "gate_up_GBps": r["gate_up_bytes"] / gu / 1e9,
+                     "gate_up_hbm_frac": r["gate_up_bytes"] / gu / 1e9 / HBM_PEAK_GBS,
+                     "gate_up_TFLOPs": r["gate_up_flops"] / gu / 1e12,
+                     "gate_up_frac_of_bf16_peak": r["gate_up_flops"] / gu / 1e12
+                     / MFMA_PEAK_BF16_TFLOPS}
+    return out
 
 
 def measure_router(cfg, steps):
@@ -253,13 +279,15 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="decode")
-    ap.add_argument("--fmt", default="e4m3", choices=["e4m3", "e2m1"])
+    ap.add_argument("--fmt", default="e4m3", choices=["e4m3", "e2m1", "bf16"])
     ap.add_argument("--no-prefill", action="store_true", help="skip the 8K prefill measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=4)
     ap.add_argument("--no-router", action="store_true", help="skip the router front-end timing")
     ap.add_argument("--workloads", action=argparse.BooleanOptionalAction, default=True,
                     help="also time the skewed 32K prefill and the TP-shard workloads")
+    ap.add_argument("--bf16-contract", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time the BF16 contract (bf16 activations and intermediate)")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager launches only (default: one HIP graph launch per step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -309,7 +337,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": f"mx{'fp8' if args.fmt == 'e4m3' else 'fp4'}x{'fp4'} (fp32 accumulate)",
+        "dtype": {"e4m3": "mxfp8 x mxfp4 (fp32 accumulate)", "e2m1": "mxfp4 x mxfp4 (fp32 accumulate)",
+                  "bf16": "bf16 x fp4-expanded-to-bf16 (fp32 accumulate)"}[args.fmt],
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: T={cfg.T} H={cfg.H} E={cfg.E}+{cfg.n_shared} "
                                f"k={cfg.k} I={cfg.I}, FP4 e2m1 weights with E8M0 per-32 scales",
@@ -358,6 +387,8 @@ def main():
             "ms_per_step": u["ms_per_step"], "eager_ms_per_step": u["eager_ms_per_step"],
             "graph_ms_per_step": u["graph_ms_per_step"], "stage_ms": u["stage_ms"],
             "down_combine_GBps": u["down_bytes"] / (u["stage_ms"]["down"] * 1e-3) / 1e9}
+    if args.bf16_contract and cfg.name == "decode":
+        line["bf16_contract"] = measure_bf16_contract(weights_np, args.steps, not args.no_graph)
     if args.workloads and cfg.name == "decode":
         line["workloads"] = {
             "skew32k": measure_workload("skew32k", 5, args.fmt, not args.no_graph, weights_np),

@@ -11,16 +11,22 @@
 // two FP4 codes times the block's E8M0 scale to two bf16, exact), so weights
 // still stream as 4.5 bits per value.
 //
-// One geometry for every batch size: workgroup tile 128 sorted rows x 128
-// weight rows (stage 1: 64 gate rows and the matching 64 up rows, so SwiGLU
-// stays in the workgroup), K in steps of 32 (one scale block); 4 waves of
-// 64 x 64, each 2 x 2 products of 32x32x16 bf16 per 16 K elements. The
+// One geometry for every batch size: workgroup tile 128 sorted rows x 256
+// weight rows (stage 1: 128 gate rows and the matching 128 up rows, so
+// SwiGLU stays in the workgroup), K in steps of 32 (one scale block); 8
+// waves, each one 32-row weight block x all 128 rows = 4 products of
+// 32x32x16 bf16 per 16 K elements. Measured facts behind the shape: the
+// FP4 -> bf16 conversion instruction costs about 16 clocks a wave, as much
+// per step as the products, so no two waves convert the same codes (each
+// wave's weight block is the one it moves by DMA); and a 128-row weight
+// tile re-read the bf16 activation rows twice as often as this one. The
 // product is transposed (weights are the row operand), so a lane's
-// accumulator holds 16 weight-row values of one activation row.
+// accumulator holds 16 weight-row values of one activation row; stage 1's
+// up waves hand their accumulators to the gate waves through LDS.
 //
 // Data movement: activation rows (64 bytes a step) and weight rows (16 bytes
-// of FP4 a step) go global -> LDS by DMA through a ring of 4 steps; every
-// wave issues exactly 3 DMA instructions per step (rows past the tile's end
+// of FP4 a step) go global -> LDS by DMA through a ring of steps; every
+// wave issues exactly 2 DMA instructions per step (rows past the tile's end
 // repeat its first row; a stage past the last step reloads the last one), so
 // one explicit vmcnt wait per step counts exactly. The tile's weight scale
 // rows (K/32 bytes each) are staged once. Activation rows are chunk-swizzled
@@ -36,14 +42,18 @@ typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int kBM = 128;              // sorted rows per tile
-constexpr int kBN = 128;              // weight rows per tile
+constexpr int kBN = 256;              // weight rows per tile
+constexpr int kWaves = 8;
 constexpr int kBK = 32;               // K elements per step
-constexpr int kRingN = 4;             // steps in the LDS ring
+#ifndef MOE_BF16_RING
+#define MOE_BF16_RING 4
+#endif
+constexpr int kRingN = MOE_BF16_RING;  // steps in the LDS ring
 constexpr int kAS = kBM * kBK * 2;    // activation bytes per step (8 KiB)
-constexpr int kBS = kBN * kBK / 2;    // weight bytes per step (2 KiB)
+constexpr int kBS = kBN * kBK / 2;    // weight bytes per step (4 KiB)
 constexpr int kSlot = kAS + kBS;
 constexpr int kRingBytes = kRingN * kSlot;
-constexpr int kDmaPerStep = 3;        // DMA instructions per wave per step
+constexpr int kDmaPerStep = 2;        // DMA instructions per wave per step
 
 struct BfArgs {
   const uint8_t* act;       // stage 1: x bf16 [T, K]; stage 2: h bf16 [A, K] in sorted-row order
@@ -55,7 +65,15 @@ struct BfArgs {
   TileArgs t;
 };
 
-size_t bf16_lds_bytes(int K) { return kRingBytes + (size_t)kBN * (K / 32); }
+// Stage 1 passes the up accumulators [128 rows][128 columns] through LDS
+// after the K loop, rows padded to kExStride floats (no bank collisions).
+constexpr int kExStride = 132;
+constexpr size_t kExBytes = (size_t)kBM * kExStride * 4;
+
+size_t bf16_lds_bytes(int K) {
+  const size_t loop = kRingBytes + (size_t)kBN * (K / 32);
+  return loop > kExBytes ? loop : kExBytes;
+}
 
 // E8M0 byte -> 2^(b - 127) as fp32 (b = 0: the subnormal 2^-127; 255: NaN).
 __device__ __forceinline__ float e8m0_f32(uint32_t b) {
@@ -81,7 +99,7 @@ __device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
 
 // ST = 1: gate/up + SwiGLU + bf16 h; ST = 2: down -> fp32 partials.
 template <int ST>
-__global__ __launch_bounds__(256) void bf16_gemm_kernel(BfArgs p) {
+__global__ __launch_bounds__(64 * kWaves) void bf16_gemm_kernel(BfArgs p) {
   int4 tile;
   int nt;
   if (!tile_of_block(p.t, &tile, &nt)) return;
@@ -95,44 +113,46 @@ __global__ __launch_bounds__(256) void bf16_gemm_kernel(BfArgs p) {
   const uint32_t ring = __builtin_amdgcn_readfirstlane(lds_addr(lds));
   uint8_t* sc_lds = lds + kRingBytes;  // [kBN][kb] weight scale bytes
 
-  // tile weight row r -> expert weight row
+  // tile weight row r -> expert weight row (stage 2: rows past H repeat row
+  // H - 1; their columns are not stored)
   auto wrow = [&](int r) {
-    return ST == 1 ? (r < 64 ? 64 * nt + r : p.I + 64 * nt + r - 64) : kBN * nt + r;
+    return ST == 1 ? (r < 128 ? 128 * nt + r : p.I + 128 * nt + r - 128)
+                   : (kBN * nt + r < p.H ? kBN * nt + r : p.H - 1);
   };
   const uint8_t* wbase = p.w + (size_t)e * p.N * (p.K / 2);
   const uint8_t* sbase = p.ws + (size_t)e * p.N * kb;
 
-  // DMA sources of this lane: activation instructions i = 0, 1 cover tile
-  // rows 32 w + 16 i + lane / 4, chunk slot lane % 4 (global chunk slot ^
-  // f(row)); the weight instruction covers tile row 32 w + lane (lanes < 32).
-  uint32_t aoff[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int r = 32 * w + 16 * i + (lane >> 2);
+  // DMA sources of this lane: the activation instruction covers tile rows
+  // 16 w + lane / 4, chunk slot lane % 4 (global chunk slot ^ f(row)); the
+  // weight instruction covers tile row 32 w + lane (lanes < 32).
+  uint32_t aoff;
+  {
+    const int r = 16 * w + (lane >> 2);
     const int rr = row0 + (r < nrows ? r : 0);
     const int src = ST == 1 ? p.sorted[rr] / p.k_total : rr;
     const int c = (lane & 3) ^ ((r >> 2) & 3);
-    aoff[i] = (uint32_t)src * (uint32_t)(p.K * 2) + 16 * c;
+    aoff = (uint32_t)src * (uint32_t)(p.K * 2) + 16 * c;
   }
   const uint32_t boff = (uint32_t)wrow(32 * w + l32) * (uint32_t)(p.K / 2);
   // step s's slot; past the last step the slot gets the last step again
   auto issue = [&](int s) {
     const uint32_t slot = ring + (uint32_t)((s % kRingN) * kSlot);
     const int step = s < nk ? s : nk - 1;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      sdma16(p.act, aoff[i] + (uint32_t)step * 64, slot + (32 * w + 16 * i) * 64);
+    sdma16(p.act, aoff + (uint32_t)step * 64, slot + 16 * w * 64);
     if (lane < 32) sdma16(wbase, boff + (uint32_t)step * 16, slot + kAS + 32 * w * 16);
   };
 
-  // weight scale rows of the tile (stage 1: the 64 gate rows, then the 64 up rows)
+  // weight scale rows of the tile (stage 1: the 128 gate rows, then the 128
+  // up rows; stage 2: the rows below H)
   {
-    const int nblk = ST == 1 ? 2 : 1, rows = kBN / nblk, bytes = rows * kb;
+    const int nblk = ST == 1 ? 2 : 1, rows = kBN / nblk;
+    const int vrows = ST == 1 ? rows : (p.H - kBN * nt < rows ? p.H - kBN * nt : rows);
+    const int bytes = vrows * kb;
     const uint32_t sl = ring + kRingBytes;
     for (int b = 0; b < nblk; ++b) {
       const uint8_t* src = sbase + (size_t)wrow(b * rows) * kb;
-      for (int o = 1024 * w; o < bytes; o += 4096)
-        if (o + 16 * lane < bytes) sdma16(src, (uint32_t)(o + 16 * lane), sl + b * bytes + o);
+      for (int o = 1024 * w; o < bytes; o += 1024 * kWaves)
+        if (o + 16 * lane < bytes) sdma16(src, (uint32_t)(o + 16 * lane), sl + b * rows * kb + o);
     }
   }
 #pragma unroll
@@ -142,88 +162,92 @@ __global__ __launch_bounds__(256) void bf16_gemm_kernel(BfArgs p) {
   tvmcnt_s<0>();
   asm volatile("s_barrier" ::: "memory");
 
-  // operand rows of this lane: weight blocks nb (tile rows), activation blocks mb
-  const int wn = w >> 1, wm = w & 1;
-  int brow[2], arow[2];
+  // operand rows of this lane: the wave's one weight block (tile rows
+  // 32 w .. 32 w + 31, the rows it moves itself, so no two waves convert the
+  // same codes) against all four activation blocks
+  const int brow = 32 * w + l32;
+  int arow[4];
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb)
-    brow[nb] = ST == 1 ? 64 * nb + 32 * wn + l32 : 64 * wn + 32 * nb + l32;
+  for (int mb = 0; mb < 4; ++mb) arow[mb] = 32 * mb + l32;
+  v16f acc[4];
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb) arow[mb] = 64 * wm + 32 * mb + l32;
+  for (int mb = 0; mb < 4; ++mb) acc[mb] = v16f{};
 
-  v16f acc[2][2];
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = v16f{};
-
-  uint32_t scb[2];  // scale bytes of the next step (read one step ahead)
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb) scb[nb] = sc_lds[brow[nb] * kb];
+  uint32_t scb = sc_lds[brow * kb];  // scale byte of the next step (read one step ahead)
   for (int k = 0; k < nk; ++k) {
-    // this wave's DMA of step k landed (steps k+1, k+2 may be in flight), and
+    // this wave's DMA of step k landed (later steps may be in flight), and
     // after the barrier every wave's has, and every wave is done with step k-1
     tvmcnt_s<(kRingN - 2) * kDmaPerStep>();
     asm volatile("s_barrier" ::: "memory");
     issue(k + kRingN - 1);  // into the slot of step k - 1
     const uint8_t* as = lds + (k % kRingN) * kSlot;
     const uint8_t* bs = as + kAS;
-    float sc[2];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      sc[nb] = e8m0_f32(scb[nb]);
-      scb[nb] = sc_lds[brow[nb] * kb + (k + 1 < nk ? k + 1 : k)];
-    }
+    const float sc = e8m0_f32(scb);
+    scb = sc_lds[brow * kb + (k + 1 < nk ? k + 1 : k)];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      v8bf wa[2], xb[2];
+      const v8bf wa = fp4x8_bf16(*reinterpret_cast<const uint32_t*>(bs + brow * 16 + 8 * ks + 4 * h), sc);
+      v8bf xb[4];
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-        wa[nb] = fp4x8_bf16(*reinterpret_cast<const uint32_t*>(bs + brow[nb] * 16 + 8 * ks + 4 * h),
-                            sc[nb]);
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
+      for (int mb = 0; mb < 4; ++mb) {
         const int r = arow[mb];
         xb[mb] = *reinterpret_cast<const v8bf*>(as + r * 64 + 16 * ((2 * ks + h) ^ ((r >> 2) & 3)));
       }
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[nb], xb[mb], acc[mb][nb], 0, 0, 0);
+      for (int mb = 0; mb < 4; ++mb)
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa, xb[mb], acc[mb], 0, 0, 0);
     }
   }
   tvmcnt_s<0>();  // the ring's last (repeated) loads
 
   // D: lane l, element i = weight row 8 (i / 4) + 4 h + i % 4 of the block,
   // activation row l % 32 of the block.
+  if constexpr (ST == 1) {
+    // waves 0-3 hold gate columns 32 w + .., waves 4-7 the matching up
+    // columns: the up waves pass theirs through LDS (the ring is free now)
+    asm volatile("s_barrier" ::: "memory");
+    float* ex = reinterpret_cast<float*>(lds);  // [128 rows][kExStride]
+    if (w >= 4) {
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb) {
-    const int m = arow[mb];
-    if (m >= nrows) continue;
-    if constexpr (ST == 1) {
-      uint8_t* dst = p.hout + ((size_t)(row0 + m) * p.I + 64 * nt + 32 * wn + 4 * h) * 2;
+      for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float hv[4];
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<v4f*>(ex + arow[mb] * kExStride + 32 * (w - 4) + 8 * q + 4 * h) =
+              v4f{acc[mb][4 * q], acc[mb][4 * q + 1], acc[mb][4 * q + 2], acc[mb][4 * q + 3]};
+    }
+    asm volatile("s_barrier" ::: "memory");
+    if (w < 4) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float G = acc[mb][0][4 * q + j], U = acc[mb][1][4 * q + j];
-          hv[j] = G * U / (1.0f + expf(-G));
+      for (int mb = 0; mb < 4; ++mb) {
+        const int m = arow[mb];
+        if (m >= nrows) continue;
+        uint8_t* dst = p.hout + ((size_t)(row0 + m) * p.I + 128 * nt + 32 * w + 4 * h) * 2;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const v4f U = *reinterpret_cast<const v4f*>(ex + m * kExStride + 32 * w + 8 * q + 4 * h);
+          float hv[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float G = acc[mb][4 * q + j];
+            hv[j] = G * U[j] / (1.0f + expf(-G));
+          }
+          *reinterpret_cast<uint2*>(dst + 16 * q) =
+              make_uint2(bf16_pair(hv[0], hv[1]), bf16_pair(hv[2], hv[3]));
         }
-        *reinterpret_cast<uint2*>(dst + 16 * q) =
-            make_uint2(bf16_pair(hv[0], hv[1]), bf16_pair(hv[2], hv[3]));
       }
-    } else {
-      const size_t a = (size_t)p.sorted[row0 + m];
+    }
+  } else {
+    if (kBN * nt + 32 * w < p.H) {  // columns past H (H % 256 == 128) are not stored
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        float* dst = p.partials + a * p.H + kBN * nt + 64 * wn + 32 * nb + 4 * h;
+      for (int mb = 0; mb < 4; ++mb) {
+        const int m = arow[mb];
+        if (m >= nrows) continue;
+        const size_t a = (size_t)p.sorted[row0 + m];
+        float* dst = p.partials + a * p.H + kBN * nt + 32 * w + 4 * h;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           *reinterpret_cast<v4f*>(dst + 8 * q) =
-              v4f{acc[mb][nb][4 * q], acc[mb][nb][4 * q + 1], acc[mb][nb][4 * q + 2],
-                  acc[mb][nb][4 * q + 3]};
+              v4f{acc[mb][4 * q], acc[mb][4 * q + 1], acc[mb][4 * q + 2], acc[mb][4 * q + 3]};
       }
     }
   }
@@ -237,18 +261,18 @@ static void launch_bf(const BfArgs& p0, long mt, int n_ntiles, hipStream_t s) {
   p.t.n_ntiles = n_ntiles;
   p.t.ngroup = n_group_of(n_ntiles);
   const long n = mt * n_ntiles;
-  hipLaunchKernelGGL((bf16_gemm_kernel<ST>), dim3((int)((n + 7) / 8 * 8)), dim3(256),
+  hipLaunchKernelGGL((bf16_gemm_kernel<ST>), dim3((int)((n + 7) / 8 * 8)), dim3(64 * kWaves),
                      bf16_lds_bytes(p.K), s, p);
 }
 
 void launch_s1_bf16(const S1Args& a, long mt, hipStream_t s) {
   BfArgs p{a.xq, a.sorted, a.w13, a.w13s, a.hq, nullptr, a.H, 2 * a.I, a.I, a.H, a.k_total, a.t};
-  launch_bf<1>(p, mt, a.I / 64, s);
+  launch_bf<1>(p, mt, a.I / 128, s);
 }
 
 void launch_s2_bf16(const S2Args& a, long mt, hipStream_t s) {
   BfArgs p{a.hq, a.sorted, a.w2, a.w2s, nullptr, a.partials, a.I, a.H, a.I, a.H, 1, a.t};
-  launch_bf<2>(p, mt, a.H / kBN, s);
+  launch_bf<2>(p, mt, (a.H + kBN - 1) / kBN, s);
 }
 
 }  // namespace moe
