@@ -286,6 +286,8 @@ def main():
     ap.add_argument("--no-router", action="store_true", help="skip the router front-end timing")
     ap.add_argument("--workloads", action=argparse.BooleanOptionalAction, default=True,
                     help="also time the skewed 32K prefill and the TP-shard workloads")
+    ap.add_argument("--fused", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time the down projection fused with the combine")
     ap.add_argument("--bf16-contract", action=argparse.BooleanOptionalAction, default=True,
                     help="also time the BF16 contract (bf16 activations and intermediate)")
     ap.add_argument("--no-graph", action="store_true",
@@ -378,8 +380,8 @@ def main():
             / MFMA_PEAK_FP4_TFLOPS,
         }
     from paper_2609_15627_amd import moe as _moe
-    if _moe.moe_fp4_grouped_gemm_combine_supported(cfg.T, cfg.H, cfg.I, cfg.NE, cfg.k_total,
-                                                   args.fmt):
+    if args.fused and _moe.moe_fp4_grouped_gemm_combine_supported(cfg.T, cfg.H, cfg.I, cfg.NE,
+                                                                  cfg.k_total, args.fmt):
         log("measuring the down projection fused with the combine")
         u = measure(cfg, weights_np, args.steps, args.warmup, args.fmt, not args.no_graph,
                     fused=True)
