@@ -80,7 +80,8 @@ enum {
   MOE_VARIANT_NONE = 0,
   MOE_VARIANT_STREAM = 1, /* weight-streaming geometry for few rows per expert (decode) */
   MOE_VARIANT_TILED = 2,  /* LDS-tiled MFMA geometry for many rows per expert (prefill) */
-  MOE_VARIANT_BF16 = 3    /* MOE_ACT_BF16: LDS-tiled bf16 geometry, any batch size */
+  MOE_VARIANT_BF16 = 3,   /* MOE_ACT_BF16: LDS-tiled bf16 geometry, any batch size */
+  MOE_VARIANT_MIXED = 4   /* tiled stage 1, streaming stage 2 (I not a multiple of 512) */
 };
 
 /* Limits checked by the validators. */
@@ -232,7 +233,8 @@ moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f
  * reported by moe_fp4_grouped_gemm_workspace_layout (for inspection by tests).
  * Requires T >= 0, H > 0, I > 0, H % 128 == 0, I % 128 == 0,
  * 1 <= NE <= MOE_MAX_EXPERTS_TOTAL, 1 <= k_total <= MOE_MAX_K_TOTAL.
- * The geometry (MOE_VARIANT_*) is chosen from T * k_total / NE and reported
+ * The geometry (MOE_VARIANT_*) is chosen per stage from T * k_total / NE and
+ * the stage's K extent (the tiled K loop takes multiples of 512) and reported
  * by moe_last_variant(). */
 size_t moe_fp4_grouped_gemm_workspace_bytes(int T, int H, int I, int n_experts_total, int k_total,
                                             moe_act_format f);

@@ -82,6 +82,22 @@ static int tile_bound(long A, int NE, int BM) {
   return (int)((A + nonempty * (BM - 1)) / BM);
 }
 
+// Bytes of one tile list (sized for the smallest row tile, 16 rows).
+static size_t tile_list_bytes(long A, int NE) {
+  const size_t tb = (size_t)tile_bound(A, NE, 16) + 1;
+  return sizeof(int4) * tb + 16 + sizeof(int2) * tb + 16 + 4 * kQueueInts;
+}
+
+// The tile list at `base` for row tiles of BM rows.
+static TileArgs tile_list(uint8_t* base, long A, int NE, int BM) {
+  const int tb = tile_bound(A, NE, 16) + 1;
+  int4* tiles = reinterpret_cast<int4*>(base);
+  int* ntiles = reinterpret_cast<int*>(tiles + tb);
+  int2* chunks = reinterpret_cast<int2*>(ntiles + 4);
+  int* nchunks = reinterpret_cast<int*>(chunks + tb);
+  return TileArgs{tiles, ntiles, tile_bound(A, NE, BM), 0, 1, chunks, nchunks, nchunks + 4};
+}
+
 GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt) {
   auto al = [](size_t v) { return (v + 255) / 256 * 256; };
   const size_t A = (size_t)T * k_total;
@@ -93,10 +109,10 @@ GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt) 
   w.off[1] = o;  o += mx ? al((size_t)T * (H / 32)) : 0;
   w.off[2] = o;  o += al(A * I * bits / 8);
   w.off[3] = o;  o += mx ? al(A * (I / 32)) : 0;
-  // tile list (int4 x bound), its count, the chunk list (int2 x bound), its
-  // count, the work queue
-  const size_t tb = (size_t)tile_bound((long)A, NE, 16) + 1;
-  w.off[4] = o;  o += al(sizeof(int4) * tb + 16 + sizeof(int2) * tb + 16 + 4 * kQueueInts);
+  // two tile lists (stage 1's and, when stage 2 runs another geometry,
+  // stage 2's), each: tiles (int4 x bound), count, chunks (int2 x bound),
+  // count, work queue
+  w.off[4] = o;  o += 2 * al(tile_list_bytes((long)A, NE));
   w.off[5] = o;
   return w;
 }
@@ -112,40 +128,52 @@ static int max_lds_per_block() {
   return v;
 }
 
-// Geometry rule (runtime M): the LDS-tiled geometry when experts average at
-// least kTiledMinRows rows, the weight-streaming geometry otherwise.
+// Geometry rule (runtime M), per stage: the LDS-tiled geometry when experts
+// average at least kTiledMinRows rows and the stage's K is a multiple of the
+// tiled K loop's 512 (stage 1: K = H, N tiles of 128 h columns; stage 2:
+// K = I, N tiles of 256 output columns); the weight-streaming geometry
+// otherwise. So a shape like the TP8 expert shard (I = 256) runs stage 1
+// tiled and stage 2 streaming.
 constexpr int kTiledMinRows = 64;
 
-static bool use_tiled(const GemmArgs& a) {
+struct Geometry {
+  bool s1_tiled, s2_tiled;
+};
+
+static Geometry geometry(const GemmArgs& a) {
   const long A = (long)a.T * a.k_total;
-  return A >= (long)kTiledMinRows * a.NE && tiled_ok(a.H, a.I) &&
-         (size_t)max_lds_per_block() >= tiled_lds_bytes(a.fmt);
+  const bool many = A >= (long)kTiledMinRows * a.NE &&
+                    (size_t)max_lds_per_block() >= tiled_lds_bytes(a.fmt);
+  return Geometry{many && tiled_k_ok(a.H) && a.I % 128 == 0, many && tiled_ok(a.H, a.I)};
 }
 
 bool fused_combine_ok(const GemmArgs& a) {
-  return a.fmt != kFmtBf16 && !use_tiled(a) &&
+  const Geometry g = geometry(a);
+  return a.fmt != kFmtBf16 && !g.s1_tiled && !g.s2_tiled &&
          fused_lds_bytes(a.T, a.k_total, a.I) <= (size_t)max_lds_per_block();
 }
 
 static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int stages,
-                                  bool tiled, hipStream_t s) {
+                                  Geometry g, hipStream_t s) {
   const bool bf = a.fmt == kFmtBf16;
-  const int BM = bf ? bf16_rows() : (tiled ? tiled_rows() : 16);
+  const int BM1 = bf ? bf16_rows() : (g.s1_tiled ? tiled_rows() : 16);
+  const int BM2 = bf ? bf16_rows() : (g.s2_tiled ? tiled_rows() : 16);
   const long A = (long)a.T * a.k_total;
-  const int mt = tile_bound(A, a.NE, BM);
-  const int tb = tile_bound(A, a.NE, 16) + 1;
-  int4* tiles = reinterpret_cast<int4*>(a.ws + w.off[4]);
-  int* ntiles = reinterpret_cast<int*>(tiles + tb);
-  int2* chunks = reinterpret_cast<int2*>(ntiles + 4);
-  int* nchunks = reinterpret_cast<int*>(chunks + tb);
-  int* queue = nchunks + 4;
+  uint8_t* lists = a.ws + w.off[4];
+  const TileArgs t1 = tile_list(lists, A, a.NE, BM1);
+  const TileArgs t2 = BM2 == BM1 ? t1 : tile_list(lists + (w.off[5] - w.off[4]) / 2, A, a.NE, BM2);
   if (stages & 1) {
     if (!bf) {  // the BF16 contract feeds x to the matrix cores as it is
       hipError_t err = launch_quantize_act(a.x, a.T, a.H, a.fmt, a.ws + w.off[0], a.ws + w.off[1], s);
       if (err != hipSuccess) return err;
     }
-    hipLaunchKernelGGL(build_tiles_kernel, dim3(1), dim3(1024), (a.NE + 1) * sizeof(int), s,
-                       a.offsets, a.NE, BM, tiles, ntiles, chunks, nchunks, queue);
+    for (const TileArgs* t : {&t1, &t2}) {
+      hipLaunchKernelGGL(build_tiles_kernel, dim3(1), dim3(1024), (a.NE + 1) * sizeof(int), s,
+                         a.offsets, a.NE, t == &t1 ? BM1 : BM2, const_cast<int4*>(t->tiles),
+                         const_cast<int*>(t->ntiles), const_cast<int2*>(t->chunks),
+                         const_cast<int*>(t->nchunks), t->queue);
+      if (BM2 == BM1) break;
+    }
   }
   if (stages & 2) {
     S1Args p1;
@@ -159,10 +187,10 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p1.H = a.H;
     p1.I = a.I;
     p1.k_total = a.k_total;
-    p1.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks, queue};
-    if (bf) launch_s1_bf16(p1, mt, s);
-    else if (tiled) launch_s1_tiled(p1, mt, a.fmt, s);
-    else launch_s1_stream(p1, mt, a.fmt, s);
+    p1.t = t1;
+    if (bf) launch_s1_bf16(p1, t1.mt_bound, s);
+    else if (g.s1_tiled) launch_s1_tiled(p1, t1.mt_bound, a.fmt, s);
+    else launch_s1_stream(p1, t1.mt_bound, a.fmt, s);
   }
   if (stages & 4) {
     S2Args p2;
@@ -174,23 +202,23 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p2.partials = a.partials;
     p2.H = a.H;
     p2.I = a.I;
-    p2.t = TileArgs{tiles, ntiles, mt, 0, 1, chunks, nchunks, queue};
+    p2.t = t2;
     if (a.out) launch_s2c_stream(S2CArgs{p2, a.topk_w, a.out, a.T, a.k_total}, a.fmt, s);
-    else if (bf) launch_s2_bf16(p2, mt, s);
-    else if (tiled) launch_s2_tiled(p2, mt, a.fmt, s);
-    else launch_s2_stream(p2, mt, a.fmt, s);
+    else if (bf) launch_s2_bf16(p2, t2.mt_bound, s);
+    else if (g.s2_tiled) launch_s2_tiled(p2, t2.mt_bound, a.fmt, s);
+    else launch_s2_stream(p2, t2.mt_bound, a.fmt, s);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int* variant) {
   const GemmWorkspace w = gemm_workspace(a.T, a.H, a.I, a.NE, a.k_total, a.fmt);
-  const bool tiled = use_tiled(a);
-  *variant = a.fmt == kFmtBf16 ? 3 : (tiled ? 2 : 1);
+  const Geometry g = geometry(a);
+  *variant = a.fmt == kFmtBf16 ? 3 : (g.s2_tiled ? 2 : (g.s1_tiled ? 4 : 1));
   if (a.T == 0) return hipSuccess;
   if (a.fmt != 0 && a.fmt != 4 && a.fmt != kFmtBf16) return hipErrorNotSupported;
   if (a.out && !fused_combine_ok(a)) return hipErrorNotSupported;
-  return launch_geometry(a, w, stages, tiled, s);
+  return launch_geometry(a, w, stages, g, s);
 }
 
 }  // namespace moe

@@ -28,7 +28,8 @@ void launch_s2_bf16(const S2Args& p, long mt, hipStream_t s);
 // LDS-tiled geometry (many rows per expert): row tiles of tiled_rows() rows.
 int tiled_rows();
 size_t tiled_lds_bytes(int fa);
-bool tiled_ok(int H, int I);
+bool tiled_ok(int H, int I);  // both stages (K = H and K = I) fit the tiled K loop
+bool tiled_k_ok(int K);       // a K extent fits the tiled K loop
 void launch_s1_tiled(const S1Args& p, long mt, int fa, hipStream_t s);
 void launch_s2_tiled(const S2Args& p, long mt, int fa, hipStream_t s);
 

@@ -860,6 +860,7 @@ size_t tiled_lds_bytes(int fa) {
 // Scale groups cover 512 K elements in both stages; N tiles are 128 h
 // columns (stage 1) and 256 output columns (stage 2).
 bool tiled_ok(int H, int I) { return H % (128 * kSG) == 0 && I % (128 * kSG) == 0; }
+bool tiled_k_ok(int K) { return K % (128 * kSG) == 0; }
 
 // One workgroup per CU (each holds a CU's LDS), never more than the items.
 static int persistent_grid(long mt, int n_ntiles) {

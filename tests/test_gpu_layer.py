@@ -131,6 +131,8 @@ def small_case(T, H, I, E, k, S, seed, routing="normal"):
     (300, 1024, 512, 4, 2, 1),    # tiled geometry: ~150-300 rows per expert, ragged tiles
     (600, 512, 1024, 2, 1, 0),    # tiled geometry: a full 256-row tile plus a ragged one
     (130, 512, 512, 2, 1, 0),     # tiled geometry: ~65 rows per expert, partial row blocks
+    (400, 512, 256, 4, 2, 0),     # tiled stage 1, streaming stage 2 (I = 256, like the TP shard)
+    (300, 1024, 384, 4, 2, 1),    # the same with I = 384 and a shared expert
 ])
 def test_small_layers(m, shape, fmt):
     cfg, inp = small_case(*shape, seed=sum(shape))
@@ -243,7 +245,8 @@ def test_full_size_configs(m, name, ntok):
     log(f"full {name}: forward")
     layer, out = run_layer(m, cfg, x, weights, logits=inp.logits)
     variant = m.moe_last_variant()
-    assert variant == (m.VARIANT_TILED if name in ("prefill8k", "skew32k") else m.VARIANT_STREAM)
+    assert variant == {"decode": m.VARIANT_STREAM, "tpshard": m.VARIANT_MIXED}.get(
+        name, m.VARIANT_TILED)
     ids_ref, w_ref = omoe.route_topk(inp.logits, cfg.k, cfg.n_shared)
     assert np.array_equal(layer.ids.cpu().numpy(), ids_ref)
     perm_ref = omoe.permute(ids_ref, cfg.NE)
