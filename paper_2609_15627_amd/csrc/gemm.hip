@@ -3,6 +3,7 @@
 #include "gemm_common.h"
 #include "gemm_launch.h"
 #include "moe_launch.h"
+#include "quant_dev.h"
 
 namespace moe {
 
@@ -20,12 +21,10 @@ namespace moe {
 // tile left over by an expert pairs with the next expert's leftover. Chunk
 // order: all within-expert pairs (expert order), then the leftover pairs.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void build_tiles_kernel(const int32_t* __restrict__ offsets,
-                                                           int NE, int BM, int4* __restrict__ tiles,
-                                                           int* __restrict__ ntiles,
-                                                           int2* __restrict__ chunks,
-                                                           int* __restrict__ nchunks,
-                                                           int* __restrict__ queue) {
+__device__ __forceinline__ void build_tiles(const int32_t* __restrict__ offsets, int NE, int BM,
+                                            int4* __restrict__ tiles, int* __restrict__ ntiles,
+                                            int2* __restrict__ chunks, int* __restrict__ nchunks,
+                                            int* __restrict__ queue) {
   extern __shared__ int start[];  // [NE + 1]
   int m[2], tot[3][2];
 #pragma unroll
@@ -75,6 +74,28 @@ __global__ __launch_bounds__(1024) void build_tiles_kernel(const int32_t* __rest
     const int r0 = offsets[lo] + j * BM;
     tiles[i] = make_int4(lo, r0, min(BM, offsets[lo + 1] - r0), 0);
   }
+}
+
+// The preparation launch: blocks [0, nqb) quantise x (1024 blocks of 32
+// elements each), then one block per tile list builds it (the two jobs are
+// independent, so they run side by side).
+template <int FMT>
+__global__ __launch_bounds__(1024) void prep_kernel(const uint16_t* __restrict__ x, long nblk,
+                                                    uint8_t* __restrict__ codes,
+                                                    uint8_t* __restrict__ scales, int nqb,
+                                                    const int32_t* __restrict__ offsets, int NE,
+                                                    int BM1, TileArgs t1, int BM2, TileArgs t2) {
+  if ((int)blockIdx.x < nqb) {
+    if constexpr (FMT >= 0) {
+      const long b = (long)blockIdx.x * 1024 + threadIdx.x;
+      if (b < nblk) quant_block<FMT>(x, b, codes, scales);
+    }
+    return;
+  }
+  const bool first = (int)blockIdx.x == nqb;
+  const TileArgs& t = first ? t1 : t2;
+  build_tiles(offsets, NE, first ? BM1 : BM2, const_cast<int4*>(t.tiles), const_cast<int*>(t.ntiles),
+              const_cast<int2*>(t.chunks), const_cast<int*>(t.nchunks), t.queue);
 }
 
 static int tile_bound(long A, int NE, int BM) {
@@ -163,17 +184,21 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
   const TileArgs t1 = tile_list(lists, A, a.NE, BM1);
   const TileArgs t2 = BM2 == BM1 ? t1 : tile_list(lists + (w.off[5] - w.off[4]) / 2, A, a.NE, BM2);
   if (stages & 1) {
-    if (!bf) {  // the BF16 contract feeds x to the matrix cores as it is
-      hipError_t err = launch_quantize_act(a.x, a.T, a.H, a.fmt, a.ws + w.off[0], a.ws + w.off[1], s);
-      if (err != hipSuccess) return err;
-    }
-    for (const TileArgs* t : {&t1, &t2}) {
-      hipLaunchKernelGGL(build_tiles_kernel, dim3(1), dim3(1024), (a.NE + 1) * sizeof(int), s,
-                         a.offsets, a.NE, t == &t1 ? BM1 : BM2, const_cast<int4*>(t->tiles),
-                         const_cast<int*>(t->ntiles), const_cast<int2*>(t->chunks),
-                         const_cast<int*>(t->nchunks), t->queue);
-      if (BM2 == BM1) break;
-    }
+    // quantisation of x (none under the BF16 contract) and the tile list(s)
+    const long nblk = bf ? 0 : (long)a.T * (a.H / 32);
+    const int nqb = (int)((nblk + 1023) / 1024);
+    const dim3 grid(nqb + (BM2 == BM1 ? 1 : 2));
+    const size_t lds = (a.NE + 1) * sizeof(int);
+    uint8_t *codes = a.ws + w.off[0], *scales = a.ws + w.off[1];
+    if (bf)
+      hipLaunchKernelGGL(prep_kernel<-1>, grid, dim3(1024), lds, s, a.x, nblk, codes, scales, nqb,
+                         a.offsets, a.NE, BM1, t1, BM2, t2);
+    else if (a.fmt == 0)
+      hipLaunchKernelGGL(prep_kernel<0>, grid, dim3(1024), lds, s, a.x, nblk, codes, scales, nqb,
+                         a.offsets, a.NE, BM1, t1, BM2, t2);
+    else
+      hipLaunchKernelGGL(prep_kernel<4>, grid, dim3(1024), lds, s, a.x, nblk, codes, scales, nqb,
+                         a.offsets, a.NE, BM1, t1, BM2, t2);
   }
   if (stages & 2) {
     S1Args p1;

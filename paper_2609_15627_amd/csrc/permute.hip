@@ -9,7 +9,8 @@
 //                    with ballots over the id bits; a lane's rank among its
 //                    lower-numbered peers plus the running per-expert cursor
 //                    in LDS is its slot, which keeps the sort stable.
-// Small inputs (one chunk) run all three steps in one workgroup.
+// Small inputs (one chunk) run all three steps in one workgroup, spread over
+// its 16 waves when the experts' per-wave counts fit LDS.
 // Integer counting only, so the result is exact and run-to-run identical.
 #include "moe_dev.h"
 #include "moe_launch.h"
@@ -143,6 +144,61 @@ __global__ __launch_bounds__(1024) void perm_small(const int32_t* __restrict__ i
   if (threadIdx.x < kWave) scatter_chunk(ids, 0, A, NE, nbits, cursor, sorted, pos);
 }
 
+// Small inputs (A <= 1024, NE <= kSmallNE) in one workgroup where wave w
+// places assignments [64 w, 64 w + 64): ballot ranks inside the wave, the
+// per-wave count of every expert in LDS, and their exclusive prefix over the
+// waves give each assignment its slot with no serial pass (stable: wave w's
+// assignments precede wave w + 1's, lanes in order).
+constexpr int kSmallNE = 512;
+
+__global__ __launch_bounds__(1024) void perm_small16(const int32_t* __restrict__ ids, int A, int NE,
+                                                     int nbits, int32_t* __restrict__ counts,
+                                                     int32_t* __restrict__ offsets,
+                                                     int32_t* __restrict__ sorted,
+                                                     int32_t* __restrict__ pos) {
+  extern __shared__ int32_t sh[];
+  int32_t* cnt = sh;             // [16][NE]: per-wave counts, then their prefix over waves
+  int32_t* off = sh + 16 * NE;   // [NE]: expert offsets
+  const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  for (int i = threadIdx.x; i < 16 * NE; i += blockDim.x) cnt[i] = 0;
+  const int a = 64 * w + lane;
+  const int e = a < A ? ids[a] : -1;
+  const bool ok = (unsigned)e < (unsigned)NE;
+  uint64_t peers = __ballot(ok);
+  for (int b = 0; b < nbits; ++b) {
+    const bool bit = ok && ((e >> b) & 1);
+    const uint64_t m = __ballot(bit);
+    peers &= bit ? m : ~m;
+  }
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+  const int rank = __popcll(peers & lt);
+  __syncthreads();
+  if (ok && (peers >> lane) == 1ull) cnt[w * NE + e] = rank + 1;  // the group's highest lane
+  __syncthreads();
+  int c = 0;
+  if ((int)threadIdx.x < NE) {
+    for (int v = 0; v < 16; ++v) {
+      const int n = cnt[v * NE + threadIdx.x];
+      cnt[v * NE + threadIdx.x] = c;
+      c += n;
+    }
+  }
+  int total;
+  const int p0 = block_exclusive_scan_1024(c, &total);
+  if ((int)threadIdx.x < NE) {
+    counts[threadIdx.x] = c;
+    offsets[threadIdx.x] = p0;
+    off[threadIdx.x] = p0;
+  }
+  if (threadIdx.x == 0) offsets[NE] = total;
+  __syncthreads();
+  if (ok) {
+    const int dest = off[e] + cnt[w * NE + e] + rank;
+    sorted[dest] = a;
+    pos[a] = dest;
+  }
+}
+
 size_t permute_workspace_bytes(int T, int NE, int k_total) {
   const long A = (long)T * k_total;
   const long nchunks = (A + kChunk - 1) / kChunk;
@@ -156,6 +212,11 @@ hipError_t launch_permute(const int32_t* ids, int T, int NE, int k_total, int32_
   int nbits = 0;
   while ((1 << nbits) < NE) ++nbits;
   const size_t lds = (size_t)NE * sizeof(int32_t);
+  if (A <= kChunk && NE <= kSmallNE) {
+    hipLaunchKernelGGL(perm_small16, dim3(1), dim3(1024), 17 * lds, s, ids, A, NE, nbits, counts,
+                       offsets, sorted, pos);
+    return hipGetLastError();
+  }
   if (A <= kChunk) {
     hipLaunchKernelGGL(perm_small, dim3(1), dim3(1024), lds, s, ids, A, NE, nbits, counts, offsets,
                        sorted, pos);

@@ -137,7 +137,10 @@ def test_permute_configs(m, name):
 
 
 @pytest.mark.parametrize("T,kt,ne", [(0, 3, 5), (1, 1, 1), (7, 3, 5), (341, 3, 2048), (342, 3, 7),
-                                     (1000, 9, 257), (5000, 2, 1), (3000, 32, 1100)])
+                                     (1000, 9, 257), (5000, 2, 1), (3000, 32, 1100),
+                                     # one workgroup, 16 waves: up to 1024 assignments, 512 experts
+                                     (341, 3, 512), (113, 9, 257), (64, 16, 300), (1, 32, 512),
+                                     (32, 32, 2)])
 def test_permute_shapes(m, T, kt, ne):
     log(f"permute T={T} kt={kt} ne={ne}")
     rng = np.random.default_rng(T + ne)
