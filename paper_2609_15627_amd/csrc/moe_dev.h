@@ -127,6 +127,49 @@ __device__ __forceinline__ v4f mfma_scaled_16x16x128(const v8i& a, const v8i& b,
 __device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, kWave); }
 __device__ __forceinline__ int shfl_xor_i(int v, int m) { return __shfl_xor(v, m, kWave); }
 
+// Value of the exchange partner at butterfly level L of a wave-wide
+// reduction, by VALU lane moves (no LDS round trip): L = 0, 1 swap lanes
+// inside each quad (xor 1, xor 2), L = 2, 3 rotate each row of 16 by 4 and 8
+// (for a commutative reduction this covers the row like xor 4, xor 8), L = 4
+// swaps rows 0 <-> 1 and 2 <-> 3, L = 5 the two halves of the wave.
+template <int L>
+__device__ __forceinline__ int wave_partner(int v) {
+  if constexpr (L == 0) return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+  if constexpr (L == 1) return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+  if constexpr (L == 2) return __builtin_amdgcn_update_dpp(0, v, 0x124, 0xF, 0xF, false);
+  if constexpr (L == 3) return __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false);
+  const int lane = (int)(threadIdx.x % kWave);
+  if constexpr (L == 4) {
+    const auto r = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+    return (int)(((lane >> 4) & 1) ? r[0] : r[1]);
+  }
+  const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+  return (int)((lane >> 5) ? r[0] : r[1]);
+}
+
+// Wave-wide arg-max of (value, index) pairs: the largest value, ties to the
+// lower index; every lane ends with the result (a unique answer, so the
+// reduction order does not matter).
+__device__ __forceinline__ void wave_argmax(float& bv, int& bi) {
+  auto step = [&](float ov, int oi) {
+    if (ov > bv || (ov == bv && oi < bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  };
+  step(__int_as_float(wave_partner<0>(__float_as_int(bv))), wave_partner<0>(bi));
+  step(__int_as_float(wave_partner<1>(__float_as_int(bv))), wave_partner<1>(bi));
+  step(__int_as_float(wave_partner<2>(__float_as_int(bv))), wave_partner<2>(bi));
+  step(__int_as_float(wave_partner<3>(__float_as_int(bv))), wave_partner<3>(bi));
+  step(__int_as_float(wave_partner<4>(__float_as_int(bv))), wave_partner<4>(bi));
+  step(__int_as_float(wave_partner<5>(__float_as_int(bv))), wave_partner<5>(bi));
+}
+
+// Lane j's value (j wave-uniform), read through a scalar register.
+__device__ __forceinline__ float lane_value(float v, int j) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), j));
+}
+
 // Map a linear workgroup id to a logical tile id so that consecutive logical
 // ids run on the same XCD: the dispatcher sends workgroup b to XCD b % 8.
 // n must be a multiple of 8.

@@ -73,15 +73,7 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
         bi = e;
       }
     }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      const float ov = shfl_xor_f(bv, m);
-      const int oi = shfl_xor_i(bi, m);
-      if (ov > bv || (ov == bv && oi < bi)) {
-        bv = ov;
-        bi = oi;
-      }
-    }
+    wave_argmax(bv, bi);
     // every lane now holds the same (bv, bi); retire the pick
 #pragma unroll
     for (int j = 0; j < EPL; ++j)
@@ -91,10 +83,10 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
       my_id = bi;
     }
   }
-  const float l0 = __shfl(my_val, 0, kWave);
+  const float l0 = lane_value(my_val, 0);
   const float ex = lane < k ? expf(my_val - l0) : 0.0f;
   float den = 0.0f;
-  for (int j = 0; j < k; ++j) den += __shfl(ex, j, kWave);
+  for (int j = 0; j < k; ++j) den += lane_value(ex, j);
   const int kt = k + n_shared;
   int32_t* id_row = ids + (size_t)t * kt;
   float* w_row = wts + (size_t)t * kt;
@@ -139,8 +131,9 @@ __device__ __forceinline__ void route_token(const float* row, int E, int k, int 
     l[j] = (x != x) ? -INFINITY : x;  // NaN reads as -inf
     lmax = fmaxf(lmax, l[j]);
   }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) lmax = fmaxf(lmax, shfl_xor_f(lmax, m));
+  static_for<6>([&](auto L) {
+    lmax = fmaxf(lmax, __int_as_float(wave_partner<decltype(L)::value>(__float_as_int(lmax))));
+  });
   // softmax denominator, summed in a fixed order (lane order j, then butterfly)
   float den = 0.0f;
   if (!o.sigmoid) {
@@ -172,11 +165,12 @@ __device__ __forceinline__ void route_token(const float* row, int E, int k, int 
           top2_merge(a1, a2, v, -INFINITY);
         }
       }
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        const float b1 = shfl_xor_f(a1, m), b2 = shfl_xor_f(a2, m);
+      static_for<6>([&](auto L) {  // the two largest over the wave (a multiset union)
+        constexpr int l = decltype(L)::value;
+        const float b1 = __int_as_float(wave_partner<l>(__float_as_int(a1)));
+        const float b2 = __int_as_float(wave_partner<l>(__float_as_int(a2)));
         top2_merge(a1, a2, b1, b2);
-      }
+      });
       if (lane == g) my_gs = gs == 1 ? a1 : a1 + a2;
     }
     // keep topk_group groups: arg-max rounds over (score descending, group ascending)
@@ -184,15 +178,7 @@ __device__ __forceinline__ void route_token(const float* row, int E, int k, int 
     for (int r = 0; r < o.topk_group; ++r) {
       float bv = (lane < o.n_group && !kept) ? my_gs : -INFINITY;
       int bi = (lane < o.n_group && !kept) ? lane : 0x7fffffff;
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        const float ov = shfl_xor_f(bv, m);
-        const int oi = shfl_xor_i(bi, m);
-        if (ov > bv || (ov == bv && oi < bi)) {
-          bv = ov;
-          bi = oi;
-        }
-      }
+      wave_argmax(bv, bi);
       if (lane == bi) kept = true;
     }
     const uint64_t mask = __ballot(kept);
@@ -216,16 +202,17 @@ __device__ __forceinline__ void route_token(const float* row, int E, int k, int 
         bl = l[j];
       }
     }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      const float ov = shfl_xor_f(bv, m), ol = shfl_xor_f(bl, m);
-      const int oi = shfl_xor_i(bi, m);
+    static_for<6>([&](auto L) {  // arg-max carrying the pick's logit
+      constexpr int q = decltype(L)::value;
+      const float ov = __int_as_float(wave_partner<q>(__float_as_int(bv)));
+      const float ol = __int_as_float(wave_partner<q>(__float_as_int(bl)));
+      const int oi = wave_partner<q>(bi);
       if (ov > bv || (ov == bv && oi < bi)) {
         bv = ov;
         bi = oi;
         bl = ol;
       }
-    }
+    });
 #pragma unroll
     for (int j = 0; j < EPL; ++j)
       if (lane + kWave * j == bi) live[j] = false;
@@ -239,14 +226,14 @@ __device__ __forceinline__ void route_token(const float* row, int E, int k, int 
   float wv;
   if (!o.sigmoid && o.renorm) {
     // exactly moe_route_topk's weights: exp(l_j - l_0) / sum over the picks
-    const float l0 = __shfl(my_l, 0, kWave);
+    const float l0 = lane_value(my_l, 0);
     wv = lane < k ? expf(my_l - l0) : 0.0f;
   } else {
     wv = lane < k ? score(my_l) : 0.0f;
   }
   if (o.renorm) {
     float sum = 0.0f;
-    for (int j = 0; j < k; ++j) sum += __shfl(wv, j, kWave);
+    for (int j = 0; j < k; ++j) sum += lane_value(wv, j);
     wv = wv / sum;
   }
   wv *= o.scale;
