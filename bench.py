@@ -286,6 +286,8 @@ def main():
     ap.add_argument("--no-router", action="store_true", help="skip the router front-end timing")
     ap.add_argument("--workloads", action=argparse.BooleanOptionalAction, default=True,
                     help="also time the skewed 32K prefill and the TP-shard workloads")
+    ap.add_argument("--fp4-prefill", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time the 8K prefill with MXFP4 activations (the FP4-rate run)")
     ap.add_argument("--fused", action=argparse.BooleanOptionalAction, default=True,
                     help="also time the down projection fused with the combine")
     ap.add_argument("--bf16-contract", action=argparse.BooleanOptionalAction, default=True,
@@ -379,6 +381,19 @@ def main():
             "layer_mfma_frac_of_fp4_peak": p["layer_flops"] / (p["ms_per_step"] * 1e-3) / 1e12
             / MFMA_PEAK_FP4_TFLOPS,
         }
+        if args.fmt == "e4m3" and args.fp4_prefill:
+            # the FP4-peak run with MXFP4 activations (both operands at the FP4 rate;
+            # parity-tested against the oracle with the same activation format)
+            log("measuring prefill8k with MXFP4 activations")
+            q = measure(pcfg, weights_np, max(3, args.steps // 10), 2, "e2m1", not args.no_graph)
+            gq = q["stage_ms"]["gate_up"]
+            tq = q["gate_up_flops"] / (gq * 1e-3) / 1e12
+            line["prefill"]["mxfp4_activations"] = {
+                "act_format": "e2m1", "ms_per_step": q["ms_per_step"],
+                "tokens_per_s": q["tokens_per_s"], "stage_ms": q["stage_ms"],
+                "gate_up_TFLOPs": tq, "gate_up_frac_of_fp4_peak": tq / MFMA_PEAK_FP4_TFLOPS,
+                "layer_frac_of_fp4_peak": q["layer_flops"] / (q["ms_per_step"] * 1e-3) / 1e12
+                / MFMA_PEAK_FP4_TFLOPS}
     from paper_2609_15627_amd import moe as _moe
     if args.fused and _moe.moe_fp4_grouped_gemm_combine_supported(cfg.T, cfg.H, cfg.I, cfg.NE,
                                                                   cfg.k_total, args.fmt):
