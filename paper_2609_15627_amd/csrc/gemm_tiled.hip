@@ -784,14 +784,21 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
     t_sync_lds();
 
     const int r = lane & 31, g = lane >> 5;
+    float* const col = p.partials + c.nc0 + 128 * wn + r;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) {
       if (mb < nmb) {
+        // the block's 16 slot numbers first, in a few wide LDS reads (rows
+        // past nrows read the zero stored for them and are not written)
+        int slot16[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          slot16[i] = sidx[128 * wm + 32 * mb + 8 * (i / 4) + 4 * g + (i % 4)];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int row = 128 * wm + 32 * mb + 8 * (i / 4) + 4 * g + (i % 4);
           if (row < nrows) {
-            float* dst = p.partials + (size_t)sidx[row] * p.H + c.nc0 + 128 * wn + r;
+            float* dst = col + (size_t)slot16[i] * p.H;
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) dst[32 * nb] = acc[mb][nb][i];
           }
