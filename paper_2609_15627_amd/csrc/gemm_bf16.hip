@@ -19,7 +19,10 @@
 // FP4 -> bf16 conversion instruction costs about 16 clocks a wave, as much
 // per step as the products, so no two waves convert the same codes (each
 // wave's weight block is the one it moves by DMA); and a 128-row weight
-// tile re-read the bf16 activation rows twice as often as this one. The
+// tile re-read the bf16 activation rows twice as often as this one. A tile
+// of fewer than 128 rows (decode: a few rows per expert) skips the operand
+// reads and products of its empty 32-row blocks; full tiles run a loop
+// without those tests (the tests cost full tiles ~10%). The
 // product is transposed (weights are the row operand), so a lane's
 // accumulator holds 16 weight-row values of one activation row; stage 1's
 // up waves hand their accumulators to the gate waves through LDS.
@@ -95,6 +98,40 @@ __device__ __forceinline__ v8bf fp4x8_bf16(uint32_t d, float s) {
 
 __device__ __forceinline__ uint32_t bf16_pair(float a, float b) {
   return f32_to_bf16_rne(a) | (f32_to_bf16_rne(b) << 16);
+}
+
+// The K loop over steps of 32: ALL runs the four row blocks; otherwise only
+// the first nmb (their reads and products).
+template <bool ALL, typename Issue>
+__device__ __forceinline__ void bf16_kloop(const uint8_t* lds, const uint8_t* sc_lds, int brow,
+                                           const int* arow, int nk, int kb, int h, Issue& issue,
+                                           v16f* acc, int nmb) {
+  uint32_t scb = sc_lds[brow * kb];  // scale byte of the next step (read one step ahead)
+  for (int k = 0; k < nk; ++k) {
+    // this wave's DMA of step k landed (later steps may be in flight), and
+    // after the barrier every wave's has, and every wave is done with step k-1
+    tvmcnt_s<(kRingN - 2) * kDmaPerStep>();
+    asm volatile("s_barrier" ::: "memory");
+    issue(k + kRingN - 1);  // into the slot of step k - 1
+    const uint8_t* as = lds + (k % kRingN) * kSlot;
+    const uint8_t* bs = as + kAS;
+    const float sc = e8m0_f32(scb);
+    scb = sc_lds[brow * kb + (k + 1 < nk ? k + 1 : k)];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const v8bf wa = fp4x8_bf16(*reinterpret_cast<const uint32_t*>(bs + brow * 16 + 8 * ks + 4 * h), sc);
+      v8bf xb[4];
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        const int r = arow[mb];
+        if (ALL || mb < nmb)
+          xb[mb] = *reinterpret_cast<const v8bf*>(as + r * 64 + 16 * ((2 * ks + h) ^ ((r >> 2) & 3)));
+      }
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+        if (ALL || mb < nmb) acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa, xb[mb], acc[mb], 0, 0, 0);
+    }
+  }
 }
 
 // ST = 1: gate/up + SwiGLU + bf16 h; ST = 2: down -> fp32 partials.
@@ -173,31 +210,12 @@ __global__ __launch_bounds__(64 * kWaves) void bf16_gemm_kernel(BfArgs p) {
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) acc[mb] = v16f{};
 
-  uint32_t scb = sc_lds[brow * kb];  // scale byte of the next step (read one step ahead)
-  for (int k = 0; k < nk; ++k) {
-    // this wave's DMA of step k landed (later steps may be in flight), and
-    // after the barrier every wave's has, and every wave is done with step k-1
-    tvmcnt_s<(kRingN - 2) * kDmaPerStep>();
-    asm volatile("s_barrier" ::: "memory");
-    issue(k + kRingN - 1);  // into the slot of step k - 1
-    const uint8_t* as = lds + (k % kRingN) * kSlot;
-    const uint8_t* bs = as + kAS;
-    const float sc = e8m0_f32(scb);
-    scb = sc_lds[brow * kb + (k + 1 < nk ? k + 1 : k)];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const v8bf wa = fp4x8_bf16(*reinterpret_cast<const uint32_t*>(bs + brow * 16 + 8 * ks + 4 * h), sc);
-      v8bf xb[4];
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
-        const int r = arow[mb];
-        xb[mb] = *reinterpret_cast<const v8bf*>(as + r * 64 + 16 * ((2 * ks + h) ^ ((r >> 2) & 3)));
-      }
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa, xb[mb], acc[mb], 0, 0, 0);
-    }
-  }
+  // row blocks holding tile rows: a tile short of 128 rows skips the reads
+  // and products of the others (they stay zero and are not stored); full
+  // tiles run the loop without the per-block tests
+  const int nmb = __builtin_amdgcn_readfirstlane((nrows + 31) / 32);
+  if (nmb >= 4) bf16_kloop<true>(lds, sc_lds, brow, arow, nk, kb, h, issue, acc, 4);
+  else bf16_kloop<false>(lds, sc_lds, brow, arow, nk, kb, h, issue, acc, nmb);
   tvmcnt_s<0>();  // the ring's last (repeated) loads
 
   // D: lane l, element i = weight row 8 (i / 4) + 4 h + i % 4 of the block,
