@@ -119,3 +119,52 @@ def test_combine_quant_logits_reject(m):
     assert L.moe_router_logits(FAKE, FAKE, 4, 100, 8, FAKE, NUL) == 1         # H % 8
     assert L.moe_router_logits(FAKE, FAKE, 4, 128, 0, FAKE, NUL) == 1
     assert L.moe_probe_scaled_mfma(NUL, FAKE, 0, FAKE, FAKE, FAKE, NUL) == 1
+
+
+def test_route_ex_and_router_reject(m):
+    L = m.lib
+    ref = ctypes.byref
+
+    def opts(score=0, ng=1, tg=1):
+        return m._RouteOpts(score, None, ng, tg, 1, 1.0)
+    ok = opts()
+    assert L.moe_route_topk_ex(FAKE, 4, 8, 2, 0, None, FAKE, FAKE, NUL) == 1    # opts NULL
+    assert L.moe_route_topk_ex(FAKE, 4, 8, 2, 0, ref(opts(score=2)), FAKE, FAKE, NUL) == 1
+    assert L.moe_route_topk_ex(FAKE, 4, 8, 2, 0, ref(opts(ng=3)), FAKE, FAKE, NUL) == 1  # 3 !| 8
+    assert L.moe_route_topk_ex(FAKE, 4, 8, 2, 0, ref(opts(ng=0)), FAKE, FAKE, NUL) == 1
+    assert L.moe_route_topk_ex(FAKE, 4, 8, 2, 0, ref(opts(ng=4, tg=5)), FAKE, FAKE, NUL) == 1
+    # k larger than the experts of the kept groups (1 group of 2)
+    assert L.moe_route_topk_ex(FAKE, 4, 8, 3, 0, ref(opts(ng=4, tg=1)), FAKE, FAKE, NUL) == 1
+    assert L.moe_route_topk_ex(NUL, 4, 8, 2, 0, ref(ok), FAKE, FAKE, NUL) == 1     # null logits
+    assert L.moe_router_topk(FAKE, FAKE, 4, 100, 8, 2, 0, None, NUL, FAKE, FAKE, NUL) == 1  # H % 128
+    assert L.moe_router_topk(FAKE, FAKE, 4, 128, 8, 9, 0, None, NUL, FAKE, FAKE, NUL) == 1  # k > E
+    assert L.moe_router_topk(FAKE, FAKE, 4, 128, 512, 8, 0, None, NUL, FAKE, FAKE, NUL) == \
+        m.MOE_ERR_UNSUPPORTED                                                            # E > 256
+    assert L.moe_router_topk(NUL, FAKE, 4, 128, 8, 2, 0, None, NUL, FAKE, FAKE, NUL) == 1   # null x
+
+
+def test_gemm_stages_combine_and_formats_reject(m):
+    L = m.lib
+
+    def stages(st, f=0, ws=FAKE):
+        return L.moe_fp4_grouped_gemm_stages(FAKE, 8, 256, 128, 4, 2, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                             FAKE, f, FAKE, ws, 1 << 30, st, NUL)
+    assert stages(0) == 1 and stages(8) == 1          # stage mask outside 1..7
+    assert stages(7, f=9) == 1                        # format
+    assert stages(7, ws=NUL) == m.MOE_ERR_WORKSPACE
+
+    def comb(f=0, T=8, H=256, topk_w=FAKE, out=FAKE):
+        return L.moe_fp4_grouped_gemm_combine(FAKE, T, H, 128, 4, 2, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                              FAKE, f, topk_w, out, FAKE, 1 << 30, 7, NUL)
+    assert comb(H=200) == 1
+    assert comb(topk_w=NUL) == 1 and comb(out=NUL) == 1
+    assert comb(f=1) == m.MOE_ERR_UNSUPPORTED          # MXFP6
+    assert L.moe_fp4_grouped_gemm_combine_supported(8, 200, 128, 4, 2, 0) == 0
+    assert L.moe_fp4_grouped_gemm_combine_supported(8, 256, 128, 4, 2, 1) == 0
+    assert L.moe_fp4_grouped_gemm_combine_supported(8, 256, 128, 4, 2, 3) == 0   # BF16 contract
+    # the BF16 contract has no standalone activation quantisation
+    assert L.moe_quantize_act(FAKE, 4, 128, m.ACT_FORMATS["bf16"], FAKE, FAKE, NUL) == 1
+    # BF16 workspace: no x codes, no scales
+    off = m.moe_fp4_grouped_gemm_workspace_layout(64, 4096, 2048, 257, 9, "bf16")
+    assert off[0] == off[1] == off[2] and off[3] == off[4]
+    assert off[3] - off[2] >= 64 * 9 * 2048 * 2
