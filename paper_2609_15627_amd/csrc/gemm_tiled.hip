@@ -9,8 +9,9 @@
 //
 // Data movement, chosen from measurements on gfx950:
 //  - operands travel global -> LDS by DMA (global_load_lds, 16 bytes a lane,
-//    1 KiB of contiguous LDS per instruction) through a ring of three K-step
-//    stages; every instruction reads whole 64- or 128-byte row segments;
+//    1 KiB of contiguous LDS per instruction) through a ring of NS K-step
+//    stages (3 with FP8 activations, 4 with FP4 ones, whose stages are
+//    smaller); every instruction reads whole 64- or 128-byte row segments;
 //  - E8M0 scales move in 16-byte row pieces covering four K steps (a
 //    separate ring of two scale groups), not one word per row per step: a
 //    4-byte gather costs a cache line per lane;
@@ -51,7 +52,6 @@ typedef __attribute__((address_space(3))) void lds_ptr_t;
 
 constexpr int TBM = 256;       // sorted rows per tile
 constexpr int TBN = 256;       // weight rows per tile
-constexpr int kNStage = 3;     // K-step stages in the LDS ring
 constexpr int kSG = 4;         // K steps per scale group (16 scale bytes per row)
 
 template <int FA>
@@ -59,7 +59,11 @@ struct TL {
   static constexpr int kARow = FA == 0 ? 128 : 64;  // activation bytes per row per K step
   static constexpr int kB = TBM * kARow;             // weight rows follow the activation rows
   static constexpr int kStage = kB + TBN * 64;
-  static constexpr int kS = kNStage * kStage;        // two scale buffers follow the stages
+  // K-step stages in the LDS ring: 3 of 48 KiB with FP8 activations, 4 of
+  // 32 KiB with FP4 ones (one more step of DMA lead in the same LDS, and the
+  // ring slot of step 4q + J is J)
+  static constexpr int kNS = FA == 0 ? 3 : 4;
+  static constexpr int kS = kNS * kStage;            // two scale buffers follow the stages
   static constexpr int kSBuf = (TBM + TBN) * 16;
   static constexpr int kLoop = kS + 2 * kSBuf;
   static constexpr int kAInstr = TBM * kARow / 4096;  // DMA instructions per wave per step
@@ -142,7 +146,7 @@ __device__ __forceinline__ int t_aci(int w, int i) {
 template <int FA, bool AON>
 __device__ __forceinline__ void t_issue_stage(uint8_t* lds, const TSrc<FA>& S, int w, int k) {
   using L = TL<FA>;
-  uint8_t* st = lds + (k % kNStage) * L::kStage;
+  uint8_t* st = lds + (k % L::kNS) * L::kStage;
   const size_t ka = (size_t)k * L::kARow, kb = (size_t)k * 64;
   if constexpr (AON) {
 #pragma unroll
@@ -279,15 +283,15 @@ __device__ __forceinline__ void t_sched_b() {
 
 // One K step k = 4q + J (J compile-time) of a wave that owns NMB row blocks
 // (0..4, uniform per wave; a wave without rows still moves data and takes
-// part in the barriers). Stage k lives in ring slot k % 3, scale group q in
+// part in the barriers). Stage k lives in ring slot k % NS, scale group q in
 // buffer q % 2. X holds the step's sub-step-0 operands and sa/sb its scales
 // on entry; on exit they hold those of step k + 1.
 //   1. sub-step-0 products on X while sub-step-1 operands are read into Y;
 //   2. one row of sub-step-1 products, then: this wave's loads of stage k + 1
 //      landed, workgroup barrier (every wave has left stage k, stage k + 1 is
 //      visible);
-//   3. reads of step k + 1's operands and scales, then the DMA of stage k + 3
-//      into slot k % 3 (at J == 0 also scale group q + 1, into the buffer
+//   3. reads of step k + 1's operands and scales, then the DMA of stage
+//      k + NS into slot k % NS (at J == 0 also scale group q + 1, into the buffer
 //      group q - 1 used), interleaved with the remaining sub-step-1 products.
 // LAST marks the final group (k = nk - 4 + J), where the ring drains.
 #ifndef MOE_TILED_PRE
@@ -301,12 +305,15 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
                                        int k, int w, v16f (*acc)[4], TOps& X, TOps& Y,
                                        uint32_t* sa, uint32_t* sb) {
   using Lo = TL<FA>;
+  constexpr int NS = Lo::kNS;
   constexpr bool kNext = !LAST || J < 3;  // step k + 1 exists
-  constexpr bool kIssue = !LAST || J == 0;  // stage k + 3 exists
+  constexpr bool kIssue = !LAST || J + NS < 4;  // stage k + NS exists
   constexpr bool kScales = !LAST && J == 0;  // scale group q + 1 exists
-  // Loads issued after stage k + 1's: stage k + 2 and, when J == 1 outside
-  // the last group, the scale group issued just before it.
-  constexpr int kWait = !LAST ? (J == 1 ? 2 : 1) : (J < 2 ? 1 : (J == 2 ? 0 : -1));
+  // Loads this wave issued after stage k + 1's: stages k + 2 .. k + NS - 1
+  // (those that exist in the last group) and the scale group issued at the
+  // group's first step when that came after stage k + 1 (1 <= J <= NS - 2).
+  constexpr int kOutStages = !LAST ? NS - 2 : (NS - 2 < 2 - J ? NS - 2 : 2 - J);
+  constexpr int kOutScales = (!LAST && J >= 1 && J <= NS - 2) ? 1 : 0;
   constexpr int kAPieces = FA == 0 ? 2 : 1;
   constexpr int kOpReads = NMB > 0 ? 4 + kAPieces * NMB : 0;
   constexpr int kScaleReads = NMB > 0 ? 4 + NMB : 0;
@@ -314,7 +321,9 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   constexpr bool kAOn = NMB > 0;  // this wave moves activation rows
   constexpr int kStageLoads = (kAOn ? Lo::kAInstr : 0) + Lo::kBInstr;
   constexpr int kScaleLoads = kAOn ? 2 : 1;
-  const uint8_t* st = lds + (k % kNStage) * Lo::kStage;
+  // ring slot of step k (compile-time with 4 stages: k = 4q + J)
+  const int slot = NS == 4 ? J : k % NS;
+  const uint8_t* st = lds + slot * Lo::kStage;
 
   __builtin_amdgcn_sched_barrier(0);
   t_read_ops<FA, ST, 1, NMB>(st, L, Y);
@@ -325,9 +334,7 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
 #pragma unroll
   for (int f = 0; f < kPreN; ++f)
     acc[f / 4][f % 4] = t_mfma<FA, ST, 1>(Y.a[f / 4], Y.b[f % 4], acc[f / 4][f % 4], sa[f / 4], sb[f % 4]);
-  if constexpr (kWait == 2) tvmcnt<kStageLoads + kScaleLoads>();
-  else if constexpr (kWait == 1) tvmcnt<kStageLoads>();
-  else if constexpr (kWait == 0) tvmcnt<0>();
+  if constexpr (kNext) tvmcnt<kOutStages * kStageLoads + kOutScales * kScaleLoads>();
   tbarrier();
   __builtin_amdgcn_sched_barrier(0);
   // Second half, in explicit order: after each remaining sub-step-1 product
@@ -337,9 +344,9 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   v4u blo[4], alo[4], ahi[4];
   const int k1 = k + 1;
   const uint8_t* sbuf1 = lds + Lo::kS + ((k1 / kSG) & 1) * Lo::kSBuf;
-  const uint8_t* st1 = lds + (k1 % kNStage) * Lo::kStage;
-  uint8_t* dst = lds + (k % kNStage) * Lo::kStage;  // stage k + 3 reuses slot k % 3
-  const size_t ka = (size_t)(k + kNStage) * Lo::kARow, kb = (size_t)(k + kNStage) * 64;
+  const uint8_t* st1 = lds + (NS == 4 ? (J + 1) % 4 : k1 % NS) * Lo::kStage;
+  uint8_t* dst = lds + slot * Lo::kStage;  // stage k + NS reuses the slot of step k
+  const size_t ka = (size_t)(k + NS) * Lo::kARow, kb = (size_t)(k + NS) * 64;
   uint8_t* sdst = lds + Lo::kS + ((k / kSG + 1) & 1) * Lo::kSBuf;
   constexpr int kR = kNext ? kOpReads + kScaleReads : 0;
   constexpr int kDS = kScales ? kScaleLoads : 0;
@@ -422,12 +429,12 @@ __device__ __forceinline__ void t_group(uint8_t* lds, const TSrc<FA>& src, const
 }
 
 // The K loop shared by both stages: nk = K / 128 steps, a multiple of 4.
-// Scale group 0 and stages 0-2 are in flight before the first step.
+// Scale group 0 and stages 0 .. NS-1 are in flight before the first step.
 template <int FA, bool AON>
 __device__ __forceinline__ void t_prologue_n(uint8_t* lds, const TSrc<FA>& src, int w) {
   t_issue_scales<FA, AON>(lds, src, w, 0);
 #pragma unroll
-  for (int s = 0; s < kNStage; ++s) t_issue_stage<FA, AON>(lds, src, w, s);
+  for (int s = 0; s < TL<FA>::kNS; ++s) t_issue_stage<FA, AON>(lds, src, w, s);
 }
 
 // nmb: the row blocks this wave will multiply in the tile.
@@ -445,7 +452,7 @@ __device__ __forceinline__ void t_kloop_n(uint8_t* lds, const TSrc<FA>& src, con
                                        int w, v16f (*acc)[4]) {
   using Lo = TL<FA>;
   if constexpr (PRO) t_prologue_n<FA, (NMB > 0)>(lds, src, w);
-  tvmcnt<2 * ((NMB > 0 ? Lo::kAInstr : 0) + Lo::kBInstr)>();
+  tvmcnt<(Lo::kNS - 1) * ((NMB > 0 ? Lo::kAInstr : 0) + Lo::kBInstr)>();
   tbarrier();
 
   TOps X, Y;

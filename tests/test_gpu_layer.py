@@ -133,6 +133,7 @@ def small_case(T, H, I, E, k, S, seed, routing="normal"):
     (130, 512, 512, 2, 1, 0),     # tiled geometry: ~65 rows per expert, partial row blocks
     (400, 512, 256, 4, 2, 0),     # tiled stage 1, streaming stage 2 (I = 256, like the TP shard)
     (300, 1024, 384, 4, 2, 1),    # the same with I = 384 and a shared expert
+    (300, 2048, 512, 4, 2, 0),    # tiled stage 1 with K = 2048: middle groups of the K loop
 ])
 def test_small_layers(m, shape, fmt):
     cfg, inp = small_case(*shape, seed=sum(shape))
