@@ -80,8 +80,9 @@ enum {
   MOE_VARIANT_NONE = 0,
   MOE_VARIANT_STREAM = 1, /* weight-streaming geometry for few rows per expert (decode) */
   MOE_VARIANT_TILED = 2,  /* LDS-tiled MFMA geometry for many rows per expert (prefill) */
-  MOE_VARIANT_BF16 = 3,   /* MOE_ACT_BF16: LDS-tiled bf16 geometry, any batch size */
-  MOE_VARIANT_MIXED = 4   /* tiled stage 1, streaming stage 2 (I not a multiple of 512) */
+  MOE_VARIANT_BF16 = 3,   /* MOE_ACT_BF16: LDS-tiled bf16 geometry (many rows per expert) */
+  MOE_VARIANT_MIXED = 4,  /* tiled stage 1, streaming stage 2 (I not a multiple of 512) */
+  MOE_VARIANT_BF16_STREAM = 5 /* MOE_ACT_BF16: weight-streaming bf16 geometry (few rows) */
 };
 
 /* Limits checked by the validators. */
@@ -235,7 +236,11 @@ moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f
  * 1 <= NE <= MOE_MAX_EXPERTS_TOTAL, 1 <= k_total <= MOE_MAX_K_TOTAL.
  * The geometry (MOE_VARIANT_*) is chosen per stage from T * k_total / NE and
  * the stage's K extent (the tiled K loop takes multiples of 512) and reported
- * by moe_last_variant(). */
+ * by moe_last_variant(); under MOE_ACT_BF16 from T * k_total / NE alone
+ * (tiled from 64 rows per expert on average, both stages alike).
+ * The kernels address activation rows and one expert's weights with 32-bit
+ * byte offsets: shapes where x [T, H] or h [T * k_total, I] in the activation
+ * format, or H * I bytes, reach 4 GiB return MOE_ERR_UNSUPPORTED. */
 size_t moe_fp4_grouped_gemm_workspace_bytes(int T, int H, int I, int n_experts_total, int k_total,
                                             moe_act_format f);
 

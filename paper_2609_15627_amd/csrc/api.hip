@@ -153,6 +153,15 @@ moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f
   return launched(moe::launch_quantize_act(x, rows, K, fc, codes, scales, as_stream(stream)));
 }
 
+// The GEMM kernels address activation rows (x, h) and one expert's weights
+// with 32-bit byte offsets from a base: each must stay below 4 GiB.
+static bool offsets_fit(int T, int H, int I, int k_total, int fc) {
+  const double bits = moe::act_bits(fc);
+  const double lim = 4294967296.0;
+  return (double)T * H * bits / 8 < lim && (double)T * k_total * I * bits / 8 < lim &&
+         (double)H * I < lim;
+}
+
 static bool gemm_dims_ok(int T, int H, int I, int NE, int k_total) {
   return T >= 0 && H > 0 && I > 0 && H % 128 == 0 && I % 128 == 0 && NE >= 1 &&
          NE <= MOE_MAX_EXPERTS_TOTAL && k_total >= 1 && k_total <= MOE_MAX_K_TOTAL &&
@@ -193,6 +202,7 @@ static moe_status grouped_gemm(const uint16_t* x, int T, int H, int I, int n_exp
   if (!aligned(x, 16) || !aligned(w13, 16) || !aligned(w2, 16) || !aligned(w13_s, 4) ||
       !aligned(w2_s, 4) || !aligned(partials, 16) || !aligned(out, 16) || !aligned(topk_w, 4))
     return MOE_ERR_INVALID_ARG;
+  if (!offsets_fit(T, H, I, k_total, fc)) return MOE_ERR_UNSUPPORTED;
   const size_t need = moe::gemm_workspace(T, H, I, n_experts_total, k_total, fc).off[5];
   if (T > 0 && (!ws || ws_bytes < need || !aligned(ws, 256))) return MOE_ERR_WORKSPACE;
   moe::GemmArgs a{x, T, H, I, n_experts_total, k_total, fc, offsets, sorted,

@@ -163,6 +163,11 @@ struct Geometry {
 
 static Geometry geometry(const GemmArgs& a) {
   const long A = (long)a.T * a.k_total;
+  // the BF16 contract: its LDS-tiled kernel takes any K (a multiple of 128)
+  if (a.fmt == kFmtBf16) {
+    const bool many_bf = A >= (long)kTiledMinRows * a.NE;
+    return Geometry{many_bf, many_bf};
+  }
   const bool many = A >= (long)kTiledMinRows * a.NE &&
                     (size_t)max_lds_per_block() >= tiled_lds_bytes(a.fmt);
   return Geometry{many && tiled_k_ok(a.H) && a.I % 128 == 0, many && tiled_ok(a.H, a.I)};
@@ -177,8 +182,8 @@ bool fused_combine_ok(const GemmArgs& a) {
 static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int stages,
                                   Geometry g, hipStream_t s) {
   const bool bf = a.fmt == kFmtBf16;
-  const int BM1 = bf ? bf16_rows() : (g.s1_tiled ? tiled_rows() : 16);
-  const int BM2 = bf ? bf16_rows() : (g.s2_tiled ? tiled_rows() : 16);
+  const int BM1 = g.s1_tiled ? (bf ? bf16_rows() : tiled_rows()) : (bf ? bf16_stream_rows() : 16);
+  const int BM2 = g.s2_tiled ? (bf ? bf16_rows() : tiled_rows()) : (bf ? bf16_stream_rows() : 16);
   const long A = (long)a.T * a.k_total;
   uint8_t* lists = a.ws + w.off[4];
   const TileArgs t1 = tile_list(lists, A, a.NE, BM1);
@@ -213,7 +218,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p1.I = a.I;
     p1.k_total = a.k_total;
     p1.t = t1;
-    if (bf) launch_s1_bf16(p1, t1.mt_bound, s);
+    if (bf) (g.s1_tiled ? launch_s1_bf16 : launch_s1_bf16_stream)(p1, t1.mt_bound, s);
     else if (g.s1_tiled) launch_s1_tiled(p1, t1.mt_bound, a.fmt, s);
     else launch_s1_stream(p1, t1.mt_bound, a.fmt, s);
   }
@@ -229,7 +234,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p2.I = a.I;
     p2.t = t2;
     if (a.out) launch_s2c_stream(S2CArgs{p2, a.topk_w, a.out, a.T, a.k_total}, a.fmt, s);
-    else if (bf) launch_s2_bf16(p2, t2.mt_bound, s);
+    else if (bf) (g.s2_tiled ? launch_s2_bf16 : launch_s2_bf16_stream)(p2, t2.mt_bound, s);
     else if (g.s2_tiled) launch_s2_tiled(p2, t2.mt_bound, a.fmt, s);
     else launch_s2_stream(p2, t2.mt_bound, a.fmt, s);
   }
@@ -239,7 +244,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
 hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int* variant) {
   const GemmWorkspace w = gemm_workspace(a.T, a.H, a.I, a.NE, a.k_total, a.fmt);
   const Geometry g = geometry(a);
-  *variant = a.fmt == kFmtBf16 ? 3 : (g.s2_tiled ? 2 : (g.s1_tiled ? 4 : 1));
+  *variant = a.fmt == kFmtBf16 ? (g.s1_tiled ? 3 : 5) : (g.s2_tiled ? 2 : (g.s1_tiled ? 4 : 1));
   if (a.T == 0) return hipSuccess;
   if (a.fmt != 0 && a.fmt != 4 && a.fmt != kFmtBf16) return hipErrorNotSupported;
   if (a.out && !fused_combine_ok(a)) return hipErrorNotSupported;

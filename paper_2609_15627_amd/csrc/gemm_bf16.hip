@@ -271,6 +271,132 @@ __global__ __launch_bounds__(64 * kWaves) void bf16_gemm_kernel(BfArgs p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Weight-streaming geometry of the BF16 contract, for few rows per expert
+// (decode): one wave per workgroup takes a tile of up to 16 sorted rows and
+// NBW blocks of 16 weight rows (stage 1: NBW gate blocks and the matching up
+// blocks), so every weight byte is read once, straight into registers, and
+// expanded there. 16x16x32 bf16 products with the weights as the row
+// operand: lane l supplies weight row l % 16 and activation row l % 16, and
+// its accumulator holds weight rows 4 (l / 16) .. +3 of activation row l % 16.
+// K order: in each K step of 128, lane group g = l / 16 takes the physical
+// elements [32 g, 32 g + 32) of the step, one scale block, so its 16 bytes of
+// FP4 codes expand (with that block's scale) to the four 8-element pieces of
+// the step's four products, and its 64 bytes of bf16 activations are the
+// matching pieces. Loads run one step ahead in registers, issued without
+// branches (the last step is loaded again past the end), so the compiler's
+// waits count exactly; the tile's weight scale rows are staged in LDS once.
+// ---------------------------------------------------------------------------
+template <int NB>
+struct BfStep {
+  v4u a[4];   // 32 bf16 activations: K [32 g, 32 g + 32) of the step
+  v4u b[NB];  // 32 FP4 codes of each weight row, same K
+};
+
+template <int ST, int NBW>
+__global__ __launch_bounds__(64) void bf16_stream_kernel(BfArgs p) {
+  constexpr int NB = ST == 1 ? 2 * NBW : NBW;
+  int4 tile;
+  int nt;
+  if (!tile_of_block(p.t, &tile, &nt)) return;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int e = tile.x, row0 = tile.y, nrows = tile.z;
+  const int lane = threadIdx.x, g = lane >> 4, c16 = lane & 15;
+  const int kb = p.K / 32, nst = p.K / 128;
+  const int c0 = nt * NBW * 16;  // first h column (stage 1) or output column (stage 2)
+
+  // this lane's activation row (rows past the tile's end read its first
+  // row; their results are not stored); loads address a wave-uniform base
+  // plus a 32-bit lane offset (the host checks that the offsets fit)
+  const int rr = row0 + (c16 < nrows ? c16 : 0);
+  const uint32_t arow = ST == 1 ? (uint32_t)(p.sorted[rr] / p.k_total) : (uint32_t)rr;
+  const uint8_t* abase = p.act;
+  const uint32_t aoff = arow * (uint32_t)(p.K * 2) + 64 * g;
+  // weight rows (expert-relative): stage 1 gate block n < NBW is h columns
+  // c0 + 16 n .., its up block n + NBW the rows I + c0 + 16 n ..
+  auto wrow = [&](int n) {
+    return ST == 1 ? (n < NBW ? c0 + 16 * n : p.I + c0 + 16 * (n - NBW)) : c0 + 16 * n;
+  };
+  const uint8_t* wbase = p.w + (size_t)e * p.N * (p.K / 2);
+  uint32_t boff[NB];  // this lane's byte of step 0 in weight row wrow(n) + c16
+  uint32_t so[NB];    // LDS byte of this lane's scale of step 0
+#pragma unroll
+  for (int n = 0; n < NB; ++n) {
+    boff[n] = (uint32_t)(wrow(n) + c16) * (uint32_t)(p.K / 2) + 16 * g;
+    so[n] = (uint32_t)((16 * n + c16) * kb + g);
+  }
+
+  // (lanes of rows past the tile's end all load the tile's first row, so
+  // their loads coalesce with that lane's; no branch around the loads)
+  // a step's loads go out as one group ahead of the products that follow
+  // them in program order (interleaved with those products by the scheduler
+  // they would have only a few instructions of lead)
+  auto load = [&](BfStep<NB>& f, int s) {
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f.a[i] = ld16<false>(abase + (aoff + 256 * (uint32_t)s + 16 * i));
+#pragma unroll
+    for (int n = 0; n < NB; ++n) f.b[n] = ld16<false>(wbase + (boff[n] + 64 * (uint32_t)s));
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  BfStep<NB> f0, f1;
+  load(f0, 0);
+  // weight scale rows of the tile: [NB * 16 rows][kb bytes] (stage 1: the gate
+  // rows, then the up rows)
+  const uint8_t* sbase = p.ws + (size_t)e * p.N * kb;
+  if constexpr (ST == 1) {
+    dma_rows16(lds, sbase + (size_t)wrow(0) * kb, NBW * 16 * kb, lane);
+    dma_rows16(lds + NBW * 16 * kb, sbase + (size_t)wrow(NBW) * kb, NBW * 16 * kb, lane);
+  } else {
+    dma_rows16(lds, sbase + (size_t)wrow(0) * kb, NB * 16 * kb, lane);
+  }
+  wait_all_vmem();
+
+  v4f acc[NB];
+#pragma unroll
+  for (int n = 0; n < NB; ++n) acc[n] = v4f{0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](const BfStep<NB>& f, int s) {
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+      const float sc = e8m0_f32(lds[so[n] + 4 * s]);
+      const uint32_t w4[4] = {f.b[n].x, f.b[n].y, f.b[n].z, f.b[n].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const v8bf wb = fp4x8_bf16(w4[i], sc);
+        const v8bf xa = __builtin_bit_cast(v8bf, f.a[i]);
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, xa, acc[n], 0, 0, 0);
+      }
+    }
+  };
+  for (int s = 0; s < nst; s += 2) {
+    load(f1, s + 1 < nst ? s + 1 : nst - 1);
+    mma(f0, s);
+    load(f0, s + 2 < nst ? s + 2 : nst - 1);
+    if (s + 1 < nst) mma(f1, s + 1);
+  }
+
+  if (c16 >= nrows) return;
+  if constexpr (ST == 1) {
+    // h = G * U * sigmoid(G), rounded once to bf16: 4 consecutive h columns
+    uint8_t* dst = p.hout + ((size_t)(row0 + c16) * p.I + c0 + 4 * g) * 2;
+#pragma unroll
+    for (int n = 0; n < NBW; ++n) {
+      float hv[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float G = acc[n][j], U = acc[n + NBW][j];
+        hv[j] = G * U / (1.0f + expf(-G));
+      }
+      *reinterpret_cast<uint2*>(dst + 32 * n) =
+          make_uint2(bf16_pair(hv[0], hv[1]), bf16_pair(hv[2], hv[3]));
+    }
+  } else {
+    float* dst = p.partials + (size_t)p.sorted[row0 + c16] * p.H + c0 + 4 * g;
+#pragma unroll
+    for (int n = 0; n < NB; ++n) *reinterpret_cast<v4f*>(dst + 16 * n) = acc[n];
+  }
+}
+
 int bf16_rows() { return kBM; }
 
 template <int ST>
@@ -291,6 +417,32 @@ void launch_s1_bf16(const S1Args& a, long mt, hipStream_t s) {
 void launch_s2_bf16(const S2Args& a, long mt, hipStream_t s) {
   BfArgs p{a.hq, a.sorted, a.w2, a.w2s, nullptr, a.partials, a.I, a.H, a.I, a.H, 1, a.t};
   launch_bf<2>(p, mt, (a.H + kBN - 1) / kBN, s);
+}
+
+// Streaming geometry: 32 h columns per wave in stage 1 (2 gate + 2 up
+// blocks), 64 output columns in stage 2; tiles of up to 16 rows.
+constexpr int kBfS1 = 2, kBfS2 = 4;
+
+int bf16_stream_rows() { return 16; }
+
+void launch_s1_bf16_stream(const S1Args& a, long mt, hipStream_t s) {
+  BfArgs p{a.xq, a.sorted, a.w13, a.w13s, a.hq, nullptr, a.H, 2 * a.I, a.I, a.H, a.k_total, a.t};
+  const int ntl = a.I / (kBfS1 * 16);
+  p.t.n_ntiles = ntl;
+  p.t.ngroup = n_group_of(ntl);
+  const long n = mt * ntl;
+  hipLaunchKernelGGL((bf16_stream_kernel<1, kBfS1>), dim3((int)((n + 7) / 8 * 8)), dim3(64),
+                     (size_t)2 * kBfS1 * 16 * (a.H / 32), s, p);
+}
+
+void launch_s2_bf16_stream(const S2Args& a, long mt, hipStream_t s) {
+  BfArgs p{a.hq, a.sorted, a.w2, a.w2s, nullptr, a.partials, a.I, a.H, a.I, a.H, 1, a.t};
+  const int ntl = a.H / (kBfS2 * 16);
+  p.t.n_ntiles = ntl;
+  p.t.ngroup = n_group_of(ntl);
+  const long n = mt * ntl;
+  hipLaunchKernelGGL((bf16_stream_kernel<2, kBfS2>), dim3((int)((n + 7) / 8 * 8)), dim3(64),
+                     (size_t)kBfS2 * 16 * (a.I / 32), s, p);
 }
 
 }  // namespace moe

@@ -36,6 +36,21 @@ __device__ __forceinline__ v4u ld16(const uint8_t* p) {
 // One 4-byte (sdma4) or 16-byte (sdma16) DMA instruction: lane i's bytes at
 // base + voff go to LDS byte lds_base + 4 i (16 i); base and lds_base are
 // wave-uniform.
+typedef __attribute__((address_space(3))) void lds_ptr_t;
+
+// nbytes (a multiple of 16) of contiguous global memory to LDS by 16-byte
+// DMA: 1 KiB of contiguous bytes per instruction (lane = 0 .. 63).
+__device__ __forceinline__ void dma_rows16(uint8_t* dst, const uint8_t* src, int nbytes, int lane) {
+  for (int o = 0; o < nbytes; o += 1024)
+    if (o + 16 * lane < nbytes)
+      __builtin_amdgcn_global_load_lds(src + o + 16 * lane, (lds_ptr_t*)(dst + o), 16, 0, 0);
+}
+
+// Wait for every outstanding vector memory operation: after a prologue's
+// DMA the compiler can no longer count the loads exactly; one explicit wait
+// restores exact waits for the step loop that follows.
+__device__ __forceinline__ void wait_all_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
 // A wave-uniform pointer held in scalar registers.
 __device__ __forceinline__ const uint8_t* sptr(const uint8_t* p) {
   const uint64_t v = reinterpret_cast<uint64_t>(p);

@@ -24,6 +24,11 @@ int bf16_rows();
 size_t bf16_lds_bytes(int K);
 void launch_s1_bf16(const S1Args& p, long mt, hipStream_t s);
 void launch_s2_bf16(const S2Args& p, long mt, hipStream_t s);
+// ... and its weight-streaming geometry for few rows per expert (tiles of
+// bf16_stream_rows() rows).
+int bf16_stream_rows();
+void launch_s1_bf16_stream(const S1Args& p, long mt, hipStream_t s);
+void launch_s2_bf16_stream(const S2Args& p, long mt, hipStream_t s);
 
 // LDS-tiled geometry (many rows per expert): row tiles of tiled_rows() rows.
 int tiled_rows();

@@ -44,16 +44,6 @@ namespace moe {
 
 
 
-typedef __attribute__((address_space(3))) void lds_ptr_t;
-
-// nbytes (a multiple of 16) of contiguous global memory to LDS by 16-byte
-// DMA: 1 KiB of contiguous bytes per instruction.
-__device__ __forceinline__ void dma_rows16(uint8_t* dst, const uint8_t* src, int nbytes, int lane) {
-  for (int o = 0; o < nbytes; o += 1024)
-    if (o + 16 * lane < nbytes)
-      __builtin_amdgcn_global_load_lds(src + o + 16 * lane, (lds_ptr_t*)(dst + o), 16, 0, 0);
-}
-
 // 16 gathered rows of kb bytes each (kb a multiple of 4) to LDS as a dense
 // [16][kb] block by 4-byte DMA; rows(r) gives row r's address.
 template <typename RowFn>
@@ -66,11 +56,6 @@ __device__ __forceinline__ void dma_gather16(uint8_t* dst, RowFn rows, int kb, i
                                        (lds_ptr_t*)(dst + 4 * o), 4, 0, 0);
   }
 }
-
-// Wait for every outstanding vector memory operation: after the prologue's
-// DMA the compiler can no longer count the loads exactly; one explicit wait
-// restores exact waits for the step loop.
-__device__ __forceinline__ void wait_all_vmem() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
 // Registers of one K step: activation pieces + scales, NB weight rows + scales.
 template <int FA, int J, int NB>

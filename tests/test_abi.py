@@ -168,3 +168,17 @@ def test_gemm_stages_combine_and_formats_reject(m):
     off = m.moe_fp4_grouped_gemm_workspace_layout(64, 4096, 2048, 257, 9, "bf16")
     assert off[0] == off[1] == off[2] and off[3] == off[4]
     assert off[3] - off[2] >= 64 * 9 * 2048 * 2
+
+
+def test_gemm_rejects_shapes_past_32_bit_offsets(m):
+    """x of 4 GiB (2^20 tokens x 4096 FP8 codes) is refused before anything
+    is enqueued; one token fewer still passes the check (then fails on the
+    fake workspace size instead)."""
+    L = m.lib
+
+    def call(T, f=0):
+        return L.moe_fp4_grouped_gemm(FAKE, T, 4096, 128, 4, 1, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                      FAKE, f, FAKE, FAKE, 16, NUL)
+    assert call(1 << 20) == m.MOE_ERR_UNSUPPORTED
+    assert call((1 << 20) - 1) == m.MOE_ERR_WORKSPACE
+    assert call(1 << 19, f=m.ACT_FORMATS["bf16"]) == m.MOE_ERR_UNSUPPORTED   # 2 bytes an element
