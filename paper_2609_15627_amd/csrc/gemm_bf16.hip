@@ -283,9 +283,10 @@ __global__ __launch_bounds__(64 * kWaves) void bf16_gemm_kernel(BfArgs p) {
 // elements [32 g, 32 g + 32) of the step, one scale block, so its 16 bytes of
 // FP4 codes expand (with that block's scale) to the four 8-element pieces of
 // the step's four products, and its 64 bytes of bf16 activations are the
-// matching pieces. Loads run one step ahead in registers, issued without
-// branches (the last step is loaded again past the end), so the compiler's
-// waits count exactly; the tile's weight scale rows are staged in LDS once.
+// matching pieces. Loads run one step ahead in registers, with no branch
+// around them inside the loop (the last one or two steps are peeled), so the
+// compiler's waits count exactly; the tile's weight scale rows are staged in
+// LDS once.
 // ---------------------------------------------------------------------------
 template <int NB>
 struct BfStep {
@@ -331,16 +332,25 @@ __global__ __launch_bounds__(64) void bf16_stream_kernel(BfArgs p) {
   // a step's loads go out as one group ahead of the products that follow
   // them in program order (interleaved with those products by the scheduler
   // they would have only a few instructions of lead)
-  auto load = [&](BfStep<NB>& f, int s) {
+  // running lane offsets of the next step to load (advanced in place, so
+  // no address register is also a load target)
+  uint32_t ao = aoff;
+  uint32_t bo[NB];
+#pragma unroll
+  for (int n = 0; n < NB; ++n) bo[n] = boff[n];
+  auto load = [&](BfStep<NB>& f) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) f.a[i] = ld16<false>(abase + (aoff + 256 * (uint32_t)s + 16 * i));
+    for (int i = 0; i < 4; ++i) f.a[i] = ld16<false>(abase + ao + 16 * i);
 #pragma unroll
-    for (int n = 0; n < NB; ++n) f.b[n] = ld16<false>(wbase + (boff[n] + 64 * (uint32_t)s));
+    for (int n = 0; n < NB; ++n) f.b[n] = ld16<false>(wbase + bo[n]);
+    ao += 256;
+#pragma unroll
+    for (int n = 0; n < NB; ++n) bo[n] += 64;
     __builtin_amdgcn_sched_barrier(0);
   };
   BfStep<NB> f0, f1;
-  load(f0, 0);
+  load(f0);
   // weight scale rows of the tile: [NB * 16 rows][kb bytes] (stage 1: the gate
   // rows, then the up rows)
   const uint8_t* sbase = p.ws + (size_t)e * p.N * kb;
@@ -368,11 +378,20 @@ __global__ __launch_bounds__(64) void bf16_stream_kernel(BfArgs p) {
       }
     }
   };
-  for (int s = 0; s < nst; s += 2) {
-    load(f1, s + 1 < nst ? s + 1 : nst - 1);
+  // f0 holds step s on entry; steps s + 1 and s + 2 exist inside the loop
+  int s = 0;
+  for (; s + 2 < nst; s += 2) {
+    load(f1);
     mma(f0, s);
-    load(f0, s + 2 < nst ? s + 2 : nst - 1);
-    if (s + 1 < nst) mma(f1, s + 1);
+    load(f0);
+    mma(f1, s + 1);
+  }
+  if (s + 1 < nst) {
+    load(f1);
+    mma(f0, s);
+    mma(f1, s + 1);
+  } else {
+    mma(f0, s);
   }
 
   if (c16 >= nrows) return;
