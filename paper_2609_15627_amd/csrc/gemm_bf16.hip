@@ -11,8 +11,10 @@
 // two FP4 codes times the block's E8M0 scale to two bf16, exact), so weights
 // still stream as 4.5 bits per value.
 //
-// One geometry for every batch size: workgroup tile 128 sorted rows x 256
-// weight rows (stage 1: 128 gate rows and the matching 128 up rows, so
+// Two geometries, chosen by rows per expert. The LDS-tiled one (below; the
+// weight-streaming one for few rows per expert follows it): workgroup tile
+// 128 sorted rows x 256 weight rows (stage 1: 128 gate rows and the matching
+// 128 up rows, so
 // SwiGLU stays in the workgroup), K in steps of 32 (one scale block); 8
 // waves, each one 32-row weight block x all 128 rows = 4 products of
 // 32x32x16 bf16 per 16 K elements. Measured facts behind the shape: the
