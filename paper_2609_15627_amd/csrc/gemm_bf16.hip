@@ -14,10 +14,9 @@
 // Two geometries, chosen by rows per expert. The LDS-tiled one (below; the
 // weight-streaming one for few rows per expert follows it): workgroup tile
 // 128 sorted rows x 256 weight rows (stage 1: 128 gate rows and the matching
-// 128 up rows, so
-// SwiGLU stays in the workgroup), K in steps of 32 (one scale block); 8
-// waves, each one 32-row weight block x all 128 rows = 4 products of
-// 32x32x16 bf16 per 16 K elements. Measured facts behind the shape: the
+// 128 up rows, so SwiGLU stays in the workgroup), K in steps of 32 (one
+// scale block); 8 waves, each one 32-row weight block x all 128 rows = 4
+// products of 32x32x16 bf16 per 16 K elements. Measured facts behind the shape: the
 // FP4 -> bf16 conversion instruction costs about 16 clocks a wave, as much
 // per step as the products, so no two waves convert the same codes (each
 // wave's weight block is the one it moves by DMA); and a 128-row weight
