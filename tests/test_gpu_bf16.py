@@ -155,3 +155,21 @@ def test_bf16_full_size(m, name, ntok):
         torch.cuda.synchronize()
         assert np.array_equal(gc.bf16_bits(o2), first)
     assert ids.shape == (cfg.T, cfg.k_total)
+
+
+def test_bf16_streaming_skewed(m):
+    """Zipf-skewed routing through the BF16 streaming geometry: empty
+    experts, experts of one row and experts of several 16-row tiles."""
+    cfg = synth.LayerConfig("bf16skew", 48, 512, 32, 4, 384, 1, "zipf", 9, zipf_empty=6)
+    inp = synth.make_inputs(cfg)
+    log("bf16 streaming skewed")
+    layer, out = run(m, cfg, inp)
+    assert m.moe_last_variant() == m.VARIANT_BF16_STREAM
+    ref, _ = check(cfg, inp, layer, out, np.arange(cfg.T))
+    counts = np.bincount(ref["ids"].ravel(), minlength=cfg.NE)
+    assert (counts == 0).any() and counts.max() > 16, counts
+    first = gc.bf16_bits(out).copy()
+    o2 = layer.forward(gc.to_dev_bf16(inp.x), tuple(gc.to_dev_u8(a) for a in inp.weights),
+                       logits=torch.from_numpy(inp.logits).cuda())
+    torch.cuda.synchronize()
+    assert np.array_equal(gc.bf16_bits(o2), first)
