@@ -286,3 +286,26 @@ def test_metamorphic_w2_scale_doubles_output(m):
     w[3] = w[3] - 1
     _, out3 = run_layer(m, cfg, gc.to_dev_bf16(inp.x[perm]), tuple(w), logits=inp.logits[perm])
     assert np.array_equal(gc.bf16_bits(out3), gc.bf16_bits(out)[perm])
+
+
+def test_full_size_prefill_mxfp4_activations(m):
+    """The 8K prefill with MXFP4 activations (the FP4-rate run of the bench):
+    routing exact, sampled tokens against the oracle in the same format,
+    three runs bit-identical."""
+    cfg = synth.CONFIGS["prefill8k"]
+    inp = synth.make_inputs(cfg, lazy=True)
+    weights = gc.dev_weights(cfg)
+    x = gc.to_dev_bf16(inp.x)
+    log("full prefill8k e2m1: forward")
+    layer, out = run_layer(m, cfg, x, weights, logits=inp.logits, fmt="e2m1")
+    assert m.moe_last_variant() == m.VARIANT_TILED
+    ids_ref, _ = omoe.route_topk(inp.logits, cfg.k, cfg.n_shared)
+    assert np.array_equal(layer.ids.cpu().numpy(), ids_ref)
+    tokens = _sample_tokens(cfg, ids_ref, 2)
+    log(f"full prefill8k e2m1: oracle on tokens {tokens.tolist()}")
+    check_against_oracle(cfg, inp, layer, out, tokens, "e2m1")
+    first = gc.bf16_bits(out).copy()
+    for _ in range(2):
+        out2 = layer.forward(x, weights, logits=torch.from_numpy(inp.logits).cuda())
+        torch.cuda.synchronize()
+        assert np.array_equal(gc.bf16_bits(out2), first)
