@@ -218,3 +218,23 @@ def test_combine_fixed_order(m):
     ref = (w.astype(np.float64)[:, :, None] * P.reshape(T, kt, H).astype(np.float64)).sum(1)
     gotf = mx.bf16_to_f64(got)
     assert np.all(np.abs(gotf - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-3)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "bf16"])
+def test_layer_empty_batch(m, fmt):
+    """T = 0 through every call of the layer: empty outputs, status OK, no
+    kernel launched that could touch memory."""
+    H, I, E, k, S = 256, 128, 8, 2, 1
+    cfg = synth.LayerConfig("empty", 4, H, E, k, I, S, "normal", 1)
+    inp = synth.make_inputs(cfg)
+    w = tuple(torch.from_numpy(a).cuda() for a in inp.weights)
+    lg = torch.empty((0, E), dtype=torch.float32, device="cuda")
+    ids, tw = m.moe_route_topk(lg, k, S)
+    counts, offsets, sorted_, pos = m.moe_permute(ids, cfg.NE)
+    x = torch.empty((0, H), dtype=torch.bfloat16, device="cuda")
+    partials = m.moe_fp4_grouped_gemm(x, offsets, sorted_, *w, cfg.k_total, fmt=fmt)
+    out = m.moe_combine_fixed_order(partials, tw)
+    torch.cuda.synchronize()
+    assert ids.shape == (0, k + S) and sorted_.numel() == 0
+    assert int(counts.sum().item()) == 0 and int(offsets[-1].item()) == 0
+    assert partials.shape == (0, H) and out.shape == (0, H)
