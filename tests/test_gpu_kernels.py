@@ -96,7 +96,8 @@ def test_route_configs(m, name):
 
 
 @pytest.mark.parametrize("T,E,k,S", [(1, 1, 1, 0), (5, 8, 8, 1), (33, 64, 6, 0), (70, 65, 7, 1),
-                                     (9, 1000, 32, 0), (100, 130, 31, 1)])
+                                     (9, 1000, 32, 0), (100, 130, 31, 1),
+                                     (3, 1024, 8, 1)])    # E = MOE_MAX_EXPERTS: every lane slot full
 def test_route_shapes_and_ties(m, T, E, k, S):
     log(f"route T={T} E={E} k={k} S={S}")
     rng = np.random.default_rng(T * 1000 + E)
