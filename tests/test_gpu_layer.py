@@ -309,3 +309,17 @@ def test_full_size_prefill_mxfp4_activations(m):
         out2 = layer.forward(x, weights, logits=torch.from_numpy(inp.logits).cuda())
         torch.cuda.synchronize()
         assert np.array_equal(gc.bf16_bits(out2), first)
+
+
+def test_layer_at_expert_and_k_limits(m):
+    """1024 routed experts (MOE_MAX_EXPERTS) + the shared one, so the tile
+    list's threads handle a second group, and k_total = 32 (MOE_MAX_K_TOTAL):
+    most experts empty, the rest with a row or two."""
+    cfg = synth.LayerConfig("limits", 8, 256, 1024, 31, 128, 1, "normal", 11)
+    inp = synth.make_inputs(cfg)
+    log("layer at the expert and k limits")
+    weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, logits=inp.logits)
+    ref, _ = check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T))
+    assert np.array_equal(layer.ids.cpu().numpy(), ref["ids"])
+    assert np.array_equal(layer.perm[2].cpu().numpy(), ref["sorted"])
