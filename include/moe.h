@@ -52,7 +52,7 @@ extern "C" {
 typedef enum {
   MOE_OK = 0,
   MOE_ERR_INVALID_ARG = 1, /* null pointer, bad size, unsupported shape */
-  MOE_ERR_UNSUPPORTED = 2, /* valid request that this build does not implement */
+  MOE_ERR_UNSUPPORTED = 2, /* valid request that the library does not implement */
   MOE_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the query said */
   MOE_ERR_LAUNCH = 4       /* a kernel launch failed (HIP error) */
 } moe_status;
@@ -64,7 +64,7 @@ typedef enum {
  * formats instead. */
 typedef enum {
   MOE_ACT_MXFP8_E4M3 = 0, /* 1 byte per element */
-  MOE_ACT_MXFP6_E2M3 = 1, /* reserved: not implemented in this build */
+  MOE_ACT_MXFP6_E2M3 = 1, /* reserved: not implemented */
   MOE_ACT_MXFP4_E2M1 = 2, /* 2 elements per byte, low nibble first */
   /* The paper's BF16 contract (Large-M CK and the meaning of the earlier
    * 6.42k result; Accepted large-prefill configuration): x is not quantised,
