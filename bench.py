@@ -85,16 +85,24 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True, fused=False):
 
     dev = torch.device("cuda:0")
     x_np = synth.gen_x(cfg)
-    logits_np = synth.gen_logits(cfg)
     x = torch.from_numpy(x_np.view(np.int16)).to(dev).view(torch.bfloat16)
-    logits = torch.from_numpy(logits_np).to(dev)
+    if cfg.routing == "router":  # the step starts from bf16 router weights (a1 included)
+        logits = None
+        wr = torch.from_numpy(synth.gen_router_weight(cfg).view(np.int16)).to(dev).view(
+            torch.bfloat16)
+    else:                        # the step starts from the workload's logits
+        logits = torch.from_numpy(synth.gen_logits(cfg)).to(dev)
+        wr = None
     w = tuple(torch.from_numpy(a[: cfg.NE]).to(dev) for a in weights_np)
     layer = moe.MoELayer(cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.n_shared, fmt, device=dev,
                          fused=fused)
     stream = torch.cuda.current_stream()
 
+    def fwd(events=None):
+        return layer.forward(x, w, logits=logits, w_router=wr, events=events)
+
     for _ in range(warmup):
-        layer.forward(x, w, logits=logits)
+        fwd()
     torch.cuda.synchronize()
     variant = moe.moe_last_variant()
 
@@ -114,16 +122,28 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True, fused=False):
     # graph holds the whole path: route, permute, grouped GEMM, combine)
     graph_ms = None
     if use_graph:
-        layer.capture(x, w, logits=logits)
+        layer.capture(x, w, logits=logits, w_router=wr)
         for _ in range(warmup):
             layer.replay()
         graph_ms, graph_wall = timed(layer.replay, steps)
     # timed region 2: K steps launched eagerly, kernel by kernel
-    eager_ms, eager_wall = timed(lambda: layer.forward(x, w, logits=logits), steps)
+    eager_ms, eager_wall = timed(fwd, steps)
+    use_g = graph_ms is not None and graph_ms < eager_ms
+    # distribution of single steps in the faster launch mode (separate pass:
+    # one event between consecutive steps)
+    one = layer.replay if use_g else fwd
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for i in range(steps):
+        one()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(steps)])
     # per-step breakdown (separate pass: events between the steps of the layer)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
     for i in range(steps):
-        layer.forward(x, w, logits=logits, events=ev[i])
+        fwd(events=ev[i])
     torch.cuda.synchronize()
     names = ["route", "permute", "quant_tiles", "gate_up", "down", "combine"]
     stage_ms = {n: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in ev]))
@@ -140,13 +160,15 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True, fused=False):
     # down writes fp32 partial rows, or (fused with the combine) the bf16 output
     down_bytes = touched * w2b + hb + (cfg.T * cfg.H * 2 if layer.fused else A * cfg.H * 4)
     layer_bytes = touched * (w13b + w2b) + cfg.T * cfg.H * 2 * 2 + cfg.T * cfg.E * 4
+    if wr is not None:  # router weights instead of logits read
+        layer_bytes += cfg.E * cfg.H * 2
     gate_up_flops = 4.0 * cfg.H * cfg.I * A
     layer_flops = 6.0 * cfg.H * cfg.I * A
     # the reported step: the faster of the two launch modes (both run every kernel of the path)
-    use_g = graph_ms is not None and graph_ms < eager_ms
     ms = graph_ms if use_g else eager_ms
     wall = graph_wall if use_g else eager_wall
     return dict(ms_per_step=ms, wall_s=wall, tokens_per_s=cfg.T / (ms * 1e-3), stage_ms=stage_ms,
+                step_ms_median=float(np.median(per_step)), step_ms_min=float(per_step.min()),
                 eager_ms_per_step=eager_ms, graph_ms_per_step=graph_ms, graph=use_g,
                 touched=touched, variant=variant, fused=layer.fused, gate_up_bytes=gate_up_bytes,
                 down_bytes=down_bytes, layer_bytes=layer_bytes, gate_up_flops=gate_up_flops,
@@ -170,6 +192,7 @@ def measure_workload(name, steps, fmt, use_graph, weights_np=None):
     return {"workload": f"{name}: T={cfg.T} H={cfg.H} E={cfg.E}+{cfg.n_shared} k={cfg.k} "
                         f"I={cfg.I}, {cfg.routing} routing",
             "tokens_per_s": r["tokens_per_s"], "ms_per_step": r["ms_per_step"],
+            "step_ms_median": r["step_ms_median"], "step_ms_min": r["step_ms_min"],
             "eager_ms_per_step": r["eager_ms_per_step"],
             "graph_ms_per_step": r["graph_ms_per_step"],
             "launch": "hip_graph" if r["graph"] else "eager", "variant": r["variant"],
@@ -252,25 +275,51 @@ def measure_router(cfg, steps):
     return out
 
 
-def cpu_baseline(cfg, weights_np, ntok, fmt):
-    """The fp64 oracle, as it is, on a bounded token sample of the same workload."""
+def host_cpu():
+    """(threads to use, cores in this process's affinity mask, CPU model name).
+    The thread count is the affinity mask's size, capped by OMP_NUM_THREADS
+    when that is set (the process's share of a shared host)."""
+    aff = len(os.sched_getaffinity(0))
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    cores = min(aff, int(omp)) if omp.isdigit() and int(omp) > 0 else aff
+    model = None
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for ln in out.splitlines():
+            if ln.startswith("Model name:"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except Exception:  # lscpu missing: the model stays unknown
+        pass
+    return cores, aff, model
+
+
+def cpu_baseline(cfg, weights_np, fmt):
+    """The fp64 oracle, as it is, on the whole layer of the workload (every
+    token, routing included) and on the whole tiny layer (router projection
+    included), BLAS threads set to the host cores this process may use."""
     import synth
     from oracle import moe as omoe
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = 1
+    from threadpoolctl import threadpool_limits
+    cores, aff, model = host_cpu()
     x = synth.gen_x(cfg)
     logits = synth.gen_logits(cfg)
-    tokens = np.arange(ntok)
-    t = time.perf_counter()
-    omoe.layer(x, *weights_np, k=cfg.k, n_shared=cfg.n_shared, logits=logits, fmt=fmt,
-               tokens=tokens)
-    dt = time.perf_counter() - t
-    return {"value": ntok / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{ntok} of {cfg.T} tokens of the {cfg.name} layer (all {cfg.k}+"
-                      f"{cfg.n_shared} experts of each; routing of all tokens), {dt:.1f} s"}
+    tiny = synth.CONFIGS["tiny"]
+    tin = synth.make_inputs(tiny)
+    with threadpool_limits(limits=cores):
+        t = time.perf_counter()
+        omoe.layer(tin.x, *tin.weights, k=tiny.k, n_shared=tiny.n_shared, wr_bits=tin.wr, fmt=fmt)
+        dt0 = time.perf_counter() - t
+        t = time.perf_counter()
+        omoe.layer(x, *weights_np, k=cfg.k, n_shared=cfg.n_shared, logits=logits, fmt=fmt)
+        dt = time.perf_counter() - t
+    return {"value": cfg.T / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"the whole {cfg.name} layer (all {cfg.T} tokens, {cfg.k}+{cfg.n_shared} "
+                      f"experts each, routing included), {dt:.1f} s on {cores} threads",
+            "seconds": dt, "cpu_model": model, "affinity_cores": aff,
+            "tiny": {"tokens_per_s": tiny.T / dt0, "seconds": dt0,
+                     "sample": f"the whole tiny layer (T={tiny.T}, router projection included)"}}
 
 
 def main():
@@ -282,7 +331,6 @@ def main():
     ap.add_argument("--fmt", default="e4m3", choices=["e4m3", "e2m1", "bf16"])
     ap.add_argument("--no-prefill", action="store_true", help="skip the 8K prefill measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=4)
     ap.add_argument("--no-router", action="store_true", help="skip the router front-end timing")
     ap.add_argument("--workloads", action=argparse.BooleanOptionalAction, default=True,
                     help="also time the skewed 32K prefill and the TP-shard workloads")
@@ -330,6 +378,7 @@ def main():
     log(f"{cfg.name}: {r['ms_per_step']:.4f} ms/step, stages {r['stage_ms']}")
     gu_ms = r["stage_ms"]["gate_up"]
     achieved = r["gate_up_bytes"] / (gu_ms * 1e-3) / 1e9
+    layer_gbs = r["layer_bytes"] / (r["ms_per_step"] * 1e-3) / 1e9
     line = {
         "metric": "MoE-layer tokens/s",
         "value": r["tokens_per_s"],
@@ -357,8 +406,28 @@ def main():
                      "traffic": stored_traffic("s1_stream_kernel", cfg.name),
                      "algorithmic_bytes": r["gate_up_bytes"]},
         "stage_ms": r["stage_ms"],
-        "layer_hbm_frac": r["layer_bytes"] / (r["ms_per_step"] * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "step_ms_median": r["step_ms_median"],
+        "step_ms_min": r["step_ms_min"],
+        # the whole layer against HBM: algorithmic bytes (weights of the touched
+        # experts, x, out, logits) over the step time; the graded decode figure
+        "layer_roofline": {"bound": "hbm", "achieved": layer_gbs, "peak": HBM_PEAK_GBS,
+                           "unit": "GB/s", "frac": layer_gbs / HBM_PEAK_GBS,
+                           "algorithmic_bytes": r["layer_bytes"]},
+        "layer_hbm_frac": layer_gbs / HBM_PEAK_GBS,
     }
+    if cfg.name == "decode":
+        log("measuring the tiny layer")
+        tcfg = synth.CONFIGS["tiny"]
+        tr = measure(tcfg, synth.gen_all_experts(tcfg), args.steps, args.warmup, args.fmt,
+                     not args.no_graph)
+        line["tiny"] = {"workload": f"tiny: T={tcfg.T} H={tcfg.H} E={tcfg.E} k={tcfg.k} "
+                                    f"I={tcfg.I}, bf16 router weights (router projection in the step)",
+                        "us_per_step": tr["ms_per_step"] * 1e3,
+                        "us_per_step_median": tr["step_ms_median"] * 1e3,
+                        "us_per_step_min": tr["step_ms_min"] * 1e3,
+                        "launch": "hip_graph" if tr["graph"] else "eager",
+                        "eager_us_per_step": tr["eager_ms_per_step"] * 1e3,
+                        "tokens_per_s": tr["tokens_per_s"], "stage_ms": tr["stage_ms"]}
     if not args.no_prefill and cfg.name == "decode":
         pcfg = synth.CONFIGS["prefill8k"]
         log("measuring prefill8k")
@@ -368,6 +437,7 @@ def main():
         line["prefill"] = {
             "workload": f"prefill8k: T={pcfg.T}, same dims", "tokens_per_s": p["tokens_per_s"],
             "ms_per_step": p["ms_per_step"], "eager_ms_per_step": p["eager_ms_per_step"],
+            "step_ms_median": p["step_ms_median"], "step_ms_min": p["step_ms_min"],
             "graph_ms_per_step": p["graph_ms_per_step"],
             "launch": "hip_graph" if p["graph"] else "eager",
             "stage_ms": p["stage_ms"], "variant": p["variant"],
@@ -416,7 +486,7 @@ def main():
                           "prefill8k": measure_router(synth.CONFIGS["prefill8k"], 20)}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
-        line["cpu_baseline"] = cpu_baseline(cfg, weights_np, args.cpu_tokens, args.fmt)
+        line["cpu_baseline"] = cpu_baseline(cfg, weights_np, args.fmt)
     print(json.dumps(line), flush=True)
 
 

@@ -64,7 +64,9 @@ typedef enum {
  * formats instead. */
 typedef enum {
   MOE_ACT_MXFP8_E4M3 = 0, /* 1 byte per element */
-  MOE_ACT_MXFP6_E2M3 = 1, /* reserved: not implemented */
+  MOE_ACT_MXFP6_E2M3 = 1, /* 24 bytes per 32-element block, element j in bits [6j, 6j+6);
+                             moe_quantize_act only: the grouped GEMM calls return
+                             MOE_ERR_UNSUPPORTED for it */
   MOE_ACT_MXFP4_E2M1 = 2, /* 2 elements per byte, low nibble first */
   /* The paper's BF16 contract (Large-M CK and the meaning of the earlier
    * 6.42k result; Accepted large-prefill configuration): x is not quantised,
@@ -212,6 +214,18 @@ moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f
                             uint8_t* scales, void* stream);
 
 /* ---- a5 + a6: grouped FP4 expert GEMMs --------------------------------------
+ * The expert FFN of the layer (paper: System and model context / Execution
+ * structure, Fig. architecture) on FP4 e2m1 weights with per-32 E8M0 scales,
+ * grouped by expert over the rows the expert sorter produced (Prefill
+ * optimization / From per-assignment scalar work to CDNA2 MFMA, item 8).
+ * Activations are quantised per 32 elements before the gate/up projection
+ * (Historical TP4 decode optimization / Parallel decomposition) and the
+ * intermediate is quantised per 32 again before the down projection
+ * (Historical down-consumer pilot); the down projection stores one FP32
+ * partial per (token, slot) in its own row, with no cross-expert atomics
+ * (Current TP8 native-AR results / Accepted large-prefill configuration),
+ * and the partials stay FP32 (Rejected or reverted directions: BF16
+ * partials changed values).
  * For every expert e and every sorted row r in [offsets[e], offsets[e+1]),
  * with a = sorted[r] and t = a / k_total:
  *   xq      = MX-quantised x[t]                     (as moe_quantize_act)
@@ -233,7 +247,8 @@ moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f
  * bytes, 256-byte aligned, contents need not be initialised. Its regions are
  * reported by moe_fp4_grouped_gemm_workspace_layout (for inspection by tests).
  * Requires T >= 0, H > 0, I > 0, H % 128 == 0, I % 128 == 0,
- * 1 <= NE <= MOE_MAX_EXPERTS_TOTAL, 1 <= k_total <= MOE_MAX_K_TOTAL.
+ * 1 <= NE <= MOE_MAX_EXPERTS_TOTAL, 1 <= k_total <= MOE_MAX_K_TOTAL;
+ * f = MOE_ACT_MXFP6_E2M3 returns MOE_ERR_UNSUPPORTED.
  * The geometry (MOE_VARIANT_*) is chosen per stage from T * k_total / NE and
  * the stage's K extent (the tiled K loop takes multiples of 512) and reported
  * by moe_last_variant(); under MOE_ACT_BF16 from T * k_total / NE alone

@@ -92,8 +92,10 @@ def dequant_fp4(packed, scales) -> np.ndarray:
     packed: uint8 [N, K/2] (two e2m1 codes per byte); scales: uint8 [N, K/32]
     (one E8M0 byte per 32 consecutive K elements). Returns fp64 [N, K] with
     W[n, kk] = e2m1(code[n, kk]) * e8m0(scales[n, kk // 32]) -- exact in fp64.
+    The 16 code values are decoded from their bits once and looked up per
+    code (the same values as decoding every code, in a fraction of the time).
     """
-    vals = e2m1_decode(unpack_nibbles(packed))
+    vals = e2m1_decode(np.arange(16))[unpack_nibbles(packed)]
     s = e8m0_decode(scales)
     n, k = vals.shape
     if s.shape != (n, k // 32):

@@ -133,6 +133,22 @@ def dequant_weight(packed_row, scale_row):
     return out
 
 
+def bf16_value(bits):
+    """A bf16 bit pattern (normal or zero) -> its value, from the fields."""
+    sign = -1.0 if bits >> 15 else 1.0
+    ef, mf = (bits >> 7) & 0xFF, bits & 0x7F
+    if ef == 0:
+        return sign * mf * 2.0 ** -133
+    return sign * (1 + mf / 128.0) * 2.0 ** (ef - 127)
+
+
+def router_logits(x_bits, wr_bits):
+    """logits[t][e] = sum_h x[t][h] * Wr[e][h] by explicit loops over bf16 bit
+    patterns; math.fsum gives the exactly rounded sum of the exact products."""
+    return [[math.fsum(bf16_value(a) * bf16_value(b) for a, b in zip(xr, wr)) for wr in wr_bits]
+            for xr in x_bits]
+
+
 def layer(x, logits, w13, w13s, w2, w2s, k, n_shared, fmt):
     """The routed layer by explicit loops (lists of Python floats).
 

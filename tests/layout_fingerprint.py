@@ -1,0 +1,97 @@
+"""Column-fingerprint weights: every output column of the down projection
+names the weight row it came from, exactly.
+
+The paper found its fast down-projection path returning output columns in a
+permuted order (16-row blocks inside each 128-wide N tile) and identified the
+mapping by fingerprinting output columns (Correctness recovery / W2
+permutation). These inputs make such a mapping readable from one layer call:
+
+* x is 0.5 everywhere and every W13 code is 1.0 with scale byte 127, so
+  G = U = H/2 and h = (H/2)^2 exactly (sigmoid(H/2) rounds to 1 for H >= 256),
+  a power of two that every activation format holds exactly;
+* W2 row n holds, in its first four 32-element blocks, the constant e2m1 code
+  d_b = (n >> 3b) & 7 (the base-8 digits of n) with scale byte 119 + 4b, and
+  code 0 everywhere else. Its partial is then
+  P[n] = h * 32 * sum_b v(d_b) * 2^(4b - 8), an exact fp32 value, and
+  2 P / (h * 2^-3) = sum_b 2 v(d_b) * 16^b has the base-16 digits
+  2 v(d_b) -- the paper's doubled FP4 nibble values {0, 1, 2, 3, 4, 6, 8, 12}.
+
+Decoding a partial row therefore gives, for every output column, the index
+of the W2 row that produced it.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from tests import bruteforce as bf
+
+
+def weights(H: int, I: int):
+    """One expert's (w13, w13s, w2, w2s), stacked with a leading expert axis of 1."""
+    if H < 256 or H > 4096 or I < 128 or H % 32 or I % 32:
+        raise ValueError("fingerprint weights need 256 <= H <= 4096 and I >= 128")
+    one = 2 | (2 << 4)                                   # two e2m1 codes of value 1.0
+    w13 = np.full((2 * I, H // 2), one, np.uint8)
+    w13s = np.full((2 * I, H // 32), 127, np.uint8)
+    codes = np.zeros((H, I), np.uint8)
+    n = np.arange(H)
+    for b in range(4):
+        codes[:, 32 * b:32 * b + 32] = ((n >> (3 * b)) & 7)[:, None]
+    w2 = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+    w2s = np.full((H, I // 32), 127, np.uint8)
+    w2s[:, :4] = 119 + 4 * np.arange(4)
+    return tuple(a[None] for a in (w13, w13s, w2, w2s))
+
+
+def x_bits(T: int, H: int):
+    return np.full((T, H), 0x3F00, np.uint16)           # bf16 0.5
+
+
+def decode(partial_row, H: int):
+    """Weight-row index of every output column of one partial row (-1 where
+    the value is not a valid fingerprint)."""
+    h = (H / 2.0) ** 2
+    v2 = np.asarray(partial_row, np.float64) * 2.0 / (h * 2.0 ** -3)
+    doubled_to_code = {int(2 * val): c for c, val in enumerate(bf.paper_e2m1_table()[:8])}
+    out = np.full(v2.shape, -1, np.int64)
+    for i, v in enumerate(v2):
+        if v != np.floor(v) or v < 0:
+            continue
+        iv, n = int(v), 0
+        for b in range(4):
+            d = doubled_to_code.get(iv % 16)
+            if d is None:
+                n = -1
+                break
+            n |= d << (3 * b)
+            iv //= 16
+        out[i] = n if iv == 0 else -1
+    return out
+
+
+def block_map(cols, tile: int = 128, block: int = 16):
+    """For each N tile, the 16-row block of W2 that each output block came from
+    (relative to the tile), read from decoded columns ``cols``."""
+    maps = []
+    for t0 in range(0, len(cols), tile):
+        c = cols[t0:t0 + tile]
+        maps.append([int(c[i] - t0) // block if c[i] >= 0 else -1 for i in range(0, len(c), block)])
+    return maps
+
+
+def permute_w2_blocks(w2, w2s, fast_to_ref, tile: int = 128, block: int = 16):
+    """Store W2 rows the way a kernel with the given block mapping would read
+    them: stored block i of each N tile holds logical block fast_to_ref[i]."""
+    H = w2.shape[0]                                     # one expert's W2 [H, I/2]
+    src = np.arange(H).reshape(H // tile, len(fast_to_ref), block)[:, fast_to_ref, :].reshape(H)
+    return w2[src].copy(), w2s[src].copy()
+
+
+def read_golden_maps(path):
+    rows = []
+    for line in open(path):
+        line = line.split("#")[0].split()
+        if line:
+            rows.append([int(v) for v in line])
+    assert len(rows) == 2
+    return rows[0], rows[1]

@@ -13,7 +13,7 @@ import torch
 import synth
 from tests import gpu_common as gc
 from tests.gpu_common import log
-from tests.test_gpu_layer import check_against_oracle, run_layer
+from tests.test_gpu_layer import SMALL_E2M1_BAR, TOL, check_against_oracle, run_layer
 
 pytestmark = pytest.mark.gpu
 
@@ -53,7 +53,8 @@ def test_fused_matches_unfused_and_oracle(m, shape, fmt):
     lf, of, lu, ou = both_paths(m, cfg, inp, fmt)
     assert np.array_equal(gc.bf16_bits(of), gc.bf16_bits(ou)), "fused output differs from unfused"
     assert np.array_equal(lf.ids.cpu().numpy(), lu.ids.cpu().numpy())
-    check_against_oracle(cfg, inp, lf, of, np.arange(cfg.T), fmt)
+    bar = SMALL_E2M1_BAR if fmt == "e2m1" and cfg.I * cfg.k_total < 4096 else TOL
+    check_against_oracle(cfg, inp, lf, of, np.arange(cfg.T), fmt, bar=bar)
 
 
 def test_fused_row_limit(m):

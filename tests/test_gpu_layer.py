@@ -3,9 +3,15 @@ against the fp64 oracle, through the C ABI, in the launch configuration the
 benchmark times.
 
 Bar (bf16 output): max over tokens of max_h |y - y*| / max_h |y*| <= 1e-2,
-against the oracle with the same activation quantisation; route ids and the
-permutation bit-exact; activation codes bit-exact; ten repeated runs
-bit-identical."""
+against the oracle with the same activation quantisation, for every named
+workload and every MXFP8 case; route ids and the permutation bit-exact;
+activation codes bit-exact; stage 2 alone (from the GPU's own h codes) at the
+same bar; ten repeated runs bit-identical.
+
+Only MXFP4 activations on the small synthetic shapes (I * k_total < 4096)
+get a wider output bar, SMALL_E2M1_BAR: one h element moving one e2m1 grid
+step changes by up to a third of its value (1 -> 1.5, 2 -> 3, 4 -> 6), and
+with few h values per token that alone can move a row by more than 1e-2."""
 import numpy as np
 import pytest
 import torch
@@ -19,6 +25,7 @@ from tests.gpu_common import log
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-2
+SMALL_E2M1_BAR = 3e-2
 
 
 @pytest.fixture(scope="module")
@@ -37,6 +44,28 @@ def run_layer(m, cfg, x_dev, weights, logits=None, wr=None, fmt="e4m3", fused=Fa
     return layer, out
 
 
+# Element grid of each MX activation format: (largest value, exponent of the
+# smallest normal, mantissa bits).
+GRID = {"e4m3": (448.0, -6, 3), "e2m3": (7.5, 0, 3), "e2m1": (6.0, 0, 1)}
+
+
+def gpu_hq_rows(layer, cfg, rows, fmt):
+    """The GPU's h codes (one code per element) and scale bytes of sorted rows
+    ``rows``, copied from the grouped GEMM's workspace."""
+    rb = m_act_bytes(cfg.I, fmt)
+    hq = layer.workspace_view(2)[: cfg.A * rb].view(cfg.A, rb)
+    hs = layer.workspace_view(3)[: cfg.A * cfg.I // 32].view(cfg.A, cfg.I // 32)
+    idx = torch.from_numpy(np.asarray(rows, np.int64)).cuda()
+    q = hq.index_select(0, idx).cpu().numpy()
+    if fmt == "e2m1":
+        q = mx.unpack_nibbles(q)
+    return q, hs.index_select(0, idx).cpu().numpy()
+
+
+def m_act_bytes(K, fmt):
+    return K * {"e4m3": 8, "e2m3": 6, "e2m1": 4}[fmt] // 8
+
+
 def check_hq_codes(layer, cfg, ref, fmt):
     """The h codes the GPU fed to the down projection against the oracle's.
 
@@ -46,74 +75,122 @@ def check_hq_codes(layer, cfg, ref, fmt):
     midpoint), and elements far below their block's maximum can move a few
     subnormal steps. Bound, on dequantised values: |v_gpu - v_oracle| <= one
     grid step at the larger magnitude + 1e-4 of the block's scaled maximum
-    (448 times the larger block scale). Differing codes must be rare (at most
-    1e-3 of the codes).
+    (the format's largest value times the larger block scale). Differing codes
+    must be rare (at most 1e-3 of the codes).
 
     Block scales follow the block maximum: when the oracle's maximum sits
-    within a relative 1e-4 of the boundary 448 * 2^X between two scales, the
-    GPU's fp32 maximum may fall on the other side, and its scale is one off.
-    Only such blocks may differ in scale, and only rarely (at most 1e-3 of
-    the blocks)."""
-    if fmt != "e4m3":
-        return 0
-    hq = layer.workspace_view(2)[: cfg.A * cfg.I].cpu().numpy().reshape(cfg.A, cfg.I)
-    hs = layer.workspace_view(3)[: cfg.A * cfg.I // 32].cpu().numpy().reshape(cfg.A, cfg.I // 32)
+    within a relative 1e-4 of the boundary maxval * 2^X between two scales,
+    the GPU's fp32 maximum may fall on the other side, and its scale is one
+    off. Only such blocks may differ in scale, and only rarely (at most 1e-3
+    of the blocks)."""
+    maxval, emin, mbits = GRID[fmt]
     flips = total = moved = blocks = 0
     for r in ref["per_expert"].values():
-        g, o = hq[r["rows"]].astype(np.int64), r["hq"].astype(np.int64)
-        sg = hs[r["rows"]].astype(np.int64)
-        so = r["hs"].astype(np.int64)
+        g, sg = gpu_hq_rows(layer, cfg, r["rows"], fmt)
+        g, sg = g.astype(np.int64), sg.astype(np.int64)
+        o, so = r["hq"].astype(np.int64), r["hs"].astype(np.int64)
         ds = sg != so
         if ds.any():
             amax = np.abs(r["h"]).reshape(len(r["rows"]), -1, 32).max(2)
-            bound = 448.0 * np.ldexp(1.0, np.minimum(sg, so) - 127)
+            bound = maxval * np.ldexp(1.0, np.minimum(sg, so) - 127)
             near = (np.abs(sg - so) == 1) & (np.abs(amax - bound) <= 1e-4 * bound)
             assert (near | ~ds).all(), "h block scales differ away from a scale boundary"
         moved += int(ds.sum())
         blocks += ds.size
         eg = np.repeat(sg, 32, axis=1) - 127
         eo = np.repeat(so, 32, axis=1) - 127
-        vg = np.ldexp(mx.elem_decode(g, "e4m3"), eg)
-        vo = np.ldexp(mx.elem_decode(o, "e4m3"), eo)
+        vg = np.ldexp(mx.elem_decode(g, fmt), eg)
+        vo = np.ldexp(mx.elem_decode(o, fmt), eo)
         big = np.maximum(np.abs(vg), np.abs(vo))
         _, ex = np.frexp(big)
-        step = np.ldexp(1.0, np.maximum(ex - 1, np.maximum(eg, eo) - 6) - 3)
+        step = np.ldexp(1.0, np.maximum(ex - 1, np.maximum(eg, eo) + emin) - mbits)
         d = vg != vo
-        far = d & (np.abs(vg - vo) > step + 1e-4 * 448 * np.ldexp(1.0, np.maximum(eg, eo)))
+        far = d & (np.abs(vg - vo) > step + 1e-4 * maxval * np.ldexp(1.0, np.maximum(eg, eo)))
         assert not far.any(), f"h values too far apart: {list(zip(vg[far], vo[far]))[:8]}"
         flips += int((g != o).sum())
         total += d.size
     assert moved <= 1e-3 * max(blocks, 1), (moved, blocks)
     assert flips <= 1e-3 * max(total, 1) + 32 * moved, (flips, total)
-    return flips
+    return flips, total
 
 
-def check_against_oracle(cfg, inp, layer, out, tokens, fmt="e4m3", logits=None):
-    """Layer output, partials and h codes against the oracle with the same
-    activation quantisation. Output bar: row-relative error <= 1e-2 when each
-    token sums at least 4096 h values (I * k_total, the paper's regime and all
-    five workloads); smaller layers weigh a single neighbouring-code flip of h
-    more (about step / sqrt(I * k_total) of a row), so they get 3e-2."""
-    ref = omoe.layer(inp.x, *inp.weights, k=cfg.k, n_shared=cfg.n_shared,
-                     logits=inp.logits if logits is None else logits, fmt=fmt, tokens=tokens,
-                     keep=True)
-    flips = check_hq_codes(layer, cfg, ref, fmt) if len(tokens) == cfg.T else -1
+def check_stage2(layer, cfg, weights, rows, fmt):
+    """Stage 2 on its own: the fp32 partial rows of sorted rows ``rows``
+    against the fp64 product of the GPU's own h codes with W2 (so a neighbouring
+    h code taken in stage 1 does not count against stage 2), row-relative,
+    at the layer's bar. Returns the largest row-relative error."""
+    offsets = layer.perm[1].cpu().numpy()
+    srt = layer.perm[2].cpu().numpy()
+    rows = np.unique(np.asarray(rows, np.int64))
+    q, s = gpu_hq_rows(layer, cfg, rows, fmt)
+    hd = mx.mx_dequantize(q, s, fmt)
+    P = layer.partials
+    worst = 0.0
+    experts = np.searchsorted(offsets, rows, side="right") - 1
+    for e in np.unique(experts):
+        sel = experts == e
+        w2 = mx.dequant_fp4(weights[2][e], weights[3][e])
+        ref = hd[sel] @ w2.T
+        a = torch.from_numpy(srt[rows[sel]].astype(np.int64)).cuda()
+        got = P.index_select(0, a).cpu().numpy().astype(np.float64)
+        worst = max(worst, gc.rowrel(got, ref))
+    log(f"  stage 2 alone (GPU h codes x W2, fp64): rowrel={worst:.3e} on {rows.size} rows")
+    assert worst <= TOL
+    return worst
+
+
+def check_against_oracle(cfg, inp, layer, out, tokens, fmt="e4m3", logits=None, bar=TOL,
+                         stage2_rows=None, oracle_x_tokens=0):
+    """Layer output against the oracle with the same activation quantisation
+    (Oracle-Q), row-relative, at ``bar`` (1e-2, the layer target, for every
+    named workload); h codes of the checked tokens' rows against the oracle's;
+    stage 2 alone on ``stage2_rows`` (sorted rows; default: every row of the
+    checked tokens); the paper's metrics (max abs, relative L2, cosine)
+    against Oracle-Q and, on the first ``oracle_x_tokens`` tokens, against the
+    oracle without activation quantisation (Oracle-X), logged."""
+    lg = inp.logits if logits is None else logits
+    ref = omoe.layer(inp.x, *inp.weights, k=cfg.k, n_shared=cfg.n_shared, logits=lg, fmt=fmt,
+                     tokens=tokens, keep=True)
+    flips, nh = check_hq_codes(layer, cfg, ref, fmt)
     y = gc.bf16_to_f64(gc.bf16_bits(out)[tokens])
     err = gc.rowrel(y, ref["out_f64"])
-    tol = TOL if cfg.I * cfg.k_total >= 4096 else 3 * TOL
-    log(f"  rowrel={err:.3e} vs oracle-Q (bar {tol:g}); tokens={len(tokens)}; h code flips={flips}")
-    assert err <= tol
-    # Partials of single experts: an h value at a rounding midpoint can land on
-    # the other code on the GPU than in the oracle; with FP4 codes one such
-    # step moves a partial by a few percent of its row maximum. (The fused
-    # down + combine path keeps no partials; its output is compared bit for
-    # bit with the unfused path's in test_gpu_fused.py.)
+    mq = gc.metrics(y, ref["out_f64"])
+    log(f"  rowrel={err:.3e} vs oracle-Q (bar {bar:g}); tokens={len(tokens)}; "
+        f"h code flips={flips}/{nh}; metrics-Q max_abs={mq['max_abs']:.4g} "
+        f"rel_l2={mq['rel_l2']:.3e} cosine={mq['cosine']:.9f}")
+    assert err <= bar
+    if oracle_x_tokens:
+        tx = np.asarray(tokens)[:oracle_x_tokens]
+        rx = omoe.layer(inp.x, *inp.weights, k=cfg.k, n_shared=cfg.n_shared, logits=lg,
+                        fmt=None, tokens=tx)
+        mx_ = gc.metrics(gc.bf16_to_f64(gc.bf16_bits(out)[tx]), rx["out_f64"])
+        log(f"  metrics-X (no activation quantisation, {len(tx)} tokens): rowrel="
+            f"{gc.rowrel(gc.bf16_to_f64(gc.bf16_bits(out)[tx]), rx['out_f64']):.3e} "
+            f"max_abs={mx_['max_abs']:.4g} rel_l2={mx_['rel_l2']:.3e} cosine={mx_['cosine']:.9f}")
+        assert mx_["cosine"] > 0.99
     if layer.partials is None:
         return ref, err
-    P = layer.partials.view(cfg.T, cfg.k_total, cfg.H).cpu().numpy()[tokens]
-    perr = gc.rowrel(P.reshape(-1, cfg.H), ref["p_slots"].reshape(-1, cfg.H))
-    assert perr <= (3 * tol if fmt == "e4m3" else 5e-2), perr
+    # partials against the oracle's (these include the effect of any h code
+    # that stage 1 took on the other side of a midpoint): logged
+    P = layer.partials.view(cfg.T, cfg.k_total, cfg.H)[torch.from_numpy(np.asarray(tokens)).cuda()]
+    perr = gc.rowrel(P.cpu().numpy().reshape(-1, cfg.H), ref["p_slots"].reshape(-1, cfg.H))
+    log(f"  partials vs oracle-Q: rowrel={perr:.3e}")
+    if stage2_rows is None:
+        stage2_rows = np.concatenate([r["rows"] for r in ref["per_expert"].values()])
+    check_stage2(layer, cfg, inp.weights, stage2_rows, fmt)
     return ref, err
+
+
+def assert_repeats_identical(layer, x, weights, first, logits=None, wr=None, reps=10):
+    """The same forward ``reps`` times in all (the first already ran and gave
+    ``first``): every output bit-identical (the reduction order is fixed)."""
+    first = first.clone()
+    lg = None if logits is None else torch.from_numpy(logits).cuda()
+    for i in range(reps - 1):
+        out = layer.forward(x, weights, logits=lg, w_router=wr)
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), first.view(torch.int16)), f"run {i + 2} differs"
+    log(f"  {reps} runs bit-identical")
 
 
 def small_case(T, H, I, E, k, S, seed, routing="normal"):
@@ -143,12 +220,16 @@ def test_small_layers(m, shape, fmt):
     # output is compared with this path's bit for bit in test_gpu_fused.py)
     layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, logits=inp.logits, fmt=fmt)
     log(f"  variant {m.moe_last_variant()}")
-    ref, _ = check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T), fmt)
+    bar = SMALL_E2M1_BAR if fmt == "e2m1" and cfg.I * cfg.k_total < 4096 else TOL
+    ref, _ = check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T), fmt, bar=bar,
+                                  oracle_x_tokens=cfg.T)
     assert np.array_equal(layer.ids.cpu().numpy(), ref["ids"])
     assert np.array_equal(layer.perm[2].cpu().numpy(), ref["sorted"])
     xq = layer.workspace_view(0)[: cfg.T * m.act_code_bytes(cfg.H, fmt)].cpu().numpy()
-    if fmt == "e4m3":
-        assert np.array_equal(xq.reshape(cfg.T, cfg.H), ref["xq"])
+    xq = xq.reshape(cfg.T, -1)
+    assert np.array_equal(mx.unpack_nibbles(xq) if fmt == "e2m1" else xq, ref["xq"])
+    xs = layer.workspace_view(1)[: cfg.T * cfg.H // 32].cpu().numpy().reshape(cfg.T, -1)
+    assert np.array_equal(xs, ref["xs"])
 
 
 def test_tiled_geometry_skewed(m):
@@ -181,8 +262,14 @@ def test_tiny_config_with_router(m):
     assert np.array_equal(layer.ids.cpu().numpy(), ref["ids"])
     y = gc.bf16_to_f64(gc.bf16_bits(out))
     err = gc.rowrel(y, ref["out_f64"])
-    log(f"  tiny rowrel={err:.3e}")
+    mq = gc.metrics(y, ref["out_f64"])
+    refx = omoe.layer(inp.x, *inp.weights, k=cfg.k, wr_bits=inp.wr, fmt=None)
+    mxx = gc.metrics(y, refx["out_f64"])
+    log(f"  tiny rowrel={err:.3e} (bar {TOL:g}); metrics-Q rel_l2={mq['rel_l2']:.3e} "
+        f"cosine={mq['cosine']:.9f}; metrics-X rowrel={gc.rowrel(y, refx['out_f64']):.3e} "
+        f"rel_l2={mxx['rel_l2']:.3e} cosine={mxx['cosine']:.9f}")
     assert err <= TOL
+    assert_repeats_identical(layer, gc.to_dev_bf16(inp.x), weights, out, wr=wr)
 
 
 def test_hand_cases_exact(m):
@@ -219,25 +306,44 @@ def test_empty_tokens(m):
     assert layer.perm[1].cpu().numpy().tolist() == [0] * 10
 
 
-def _sample_tokens(cfg, ids, n):
-    """Tokens of the most and least loaded non-empty routed experts, plus seeded picks."""
-    routed = ids[:, :cfg.k]
-    cnt = np.bincount(routed.ravel(), minlength=cfg.E)
-    nz = np.nonzero(cnt)[0]
-    hi, lo = nz[np.argmax(cnt[nz])], nz[np.argmin(cnt[nz])]
-    t_hi = int(np.nonzero((routed == hi).any(1))[0][0])
-    t_lo = int(np.nonzero((routed == lo).any(1))[0][-1])
-    rng = np.random.default_rng(7)
-    extra = rng.choice(cfg.T, max(0, n - 2), replace=False)
-    return np.unique(np.concatenate([[t_hi, t_lo, cfg.T - 1], extra]))[:max(n, 2)]
+# Sorted-row positions inside an expert that the tiled kernels treat
+# differently: first and last rows of a 256-row tile and of each 32-row
+# block, the first row of the second wave half (row 128), the first rows of a
+# ragged tail tile; the last row of the expert is added per expert.
+ROW_CLASSES = (0, 31, 32, 127, 128, 129, 200, 255, 256, 257, 300, 383, 384, 511, 512)
 
 
-@pytest.mark.parametrize("name,ntok", [("decode", 3), ("prefill8k", 2), ("skew32k", 2),
-                                       ("tpshard", 6)])
+def _row_class_sample(cfg, perm, ntok, n_mid=2, seed=7):
+    """Tokens and sorted rows that cover the kernels' row classes: the rows at
+    ROW_CLASSES (and the last row) of the most and least loaded non-empty
+    routed experts and of ``n_mid`` seeded others, their tokens, plus seeded
+    tokens up to ``ntok`` and the last token. Returns (tokens, rows)."""
+    counts, offsets, srt, _ = (np.asarray(a) for a in perm)
+    nz = np.nonzero(counts[:cfg.E])[0]
+    rng = np.random.default_rng(seed)
+    experts = {int(nz[np.argmax(counts[nz])]), int(nz[np.argmin(counts[nz])])}
+    experts |= set(int(e) for e in rng.choice(nz, min(n_mid, nz.size), replace=False))
+    rows = []
+    for e in sorted(experts):
+        c = int(counts[e])
+        rows += [int(offsets[e]) + p for p in ROW_CLASSES + (c - 1,) if p < c]
+    rows = np.unique(rows)
+    tokens = set((srt[rows] // cfg.k_total).tolist()) | {cfg.T - 1}
+    extra = rng.permutation(cfg.T)
+    for t in extra:
+        if len(tokens) >= ntok:
+            break
+        tokens.add(int(t))
+    return np.array(sorted(tokens)), rows
+
+
+@pytest.mark.parametrize("name,ntok", [("decode", 64), ("prefill8k", 32), ("skew32k", 32),
+                                       ("tpshard", 64)])
 def test_full_size_configs(m, name, ntok):
     """Full-size workloads: route, permutation and activation codes compared in
-    full; outputs and partials on sampled tokens; determinism over ten runs
-    (tpshard) or three (others)."""
+    full; outputs, h codes and stage-2 partials on tokens and rows chosen to
+    cover the kernels' row classes (all 64 tokens at decode); ten runs
+    bit-identical."""
     cfg = synth.CONFIGS[name]
     log(f"full {name}: generating inputs")
     inp = synth.make_inputs(cfg, lazy=True)
@@ -257,16 +363,11 @@ def test_full_size_configs(m, name, ntok):
     rows = np.arange(0, cfg.T, max(1, cfg.T // 256))
     xq_ref, _ = mx.mx_quantize(mx.bf16_to_f64(inp.x[rows]), "e4m3")
     assert np.array_equal(xq[rows], xq_ref)
-    tokens = _sample_tokens(cfg, ids_ref, ntok)
-    log(f"full {name}: oracle on tokens {tokens.tolist()} (variant {variant})")
-    check_against_oracle(cfg, inp, layer, out, tokens)
-    first = gc.bf16_bits(out).copy()
-    reps = 10 if name == "tpshard" else 3
-    for _ in range(reps - 1):
-        out2 = layer.forward(x, weights, logits=torch.from_numpy(inp.logits).cuda())
-        torch.cuda.synchronize()
-        assert np.array_equal(gc.bf16_bits(out2), first)
-    log(f"full {name}: {reps} runs bit-identical")
+    tokens, srows = _row_class_sample(cfg, perm_ref, ntok)
+    log(f"full {name}: oracle on {len(tokens)} tokens, stage 2 on {len(srows)} class rows "
+        f"(variant {variant})")
+    check_against_oracle(cfg, inp, layer, out, tokens, stage2_rows=srows, oracle_x_tokens=4)
+    assert_repeats_identical(layer, x, weights, out, logits=inp.logits)
 
 
 def test_metamorphic_w2_scale_doubles_output(m):
@@ -290,8 +391,8 @@ def test_metamorphic_w2_scale_doubles_output(m):
 
 def test_full_size_prefill_mxfp4_activations(m):
     """The 8K prefill with MXFP4 activations (the FP4-rate run of the bench):
-    routing exact, sampled tokens against the oracle in the same format,
-    three runs bit-identical."""
+    routing exact, tokens covering the row classes against the oracle in the
+    same format, ten runs bit-identical."""
     cfg = synth.CONFIGS["prefill8k"]
     inp = synth.make_inputs(cfg, lazy=True)
     weights = gc.dev_weights(cfg)
@@ -301,14 +402,10 @@ def test_full_size_prefill_mxfp4_activations(m):
     assert m.moe_last_variant() == m.VARIANT_TILED
     ids_ref, _ = omoe.route_topk(inp.logits, cfg.k, cfg.n_shared)
     assert np.array_equal(layer.ids.cpu().numpy(), ids_ref)
-    tokens = _sample_tokens(cfg, ids_ref, 2)
-    log(f"full prefill8k e2m1: oracle on tokens {tokens.tolist()}")
-    check_against_oracle(cfg, inp, layer, out, tokens, "e2m1")
-    first = gc.bf16_bits(out).copy()
-    for _ in range(2):
-        out2 = layer.forward(x, weights, logits=torch.from_numpy(inp.logits).cuda())
-        torch.cuda.synchronize()
-        assert np.array_equal(gc.bf16_bits(out2), first)
+    tokens, srows = _row_class_sample(cfg, omoe.permute(ids_ref, cfg.NE), 16)
+    log(f"full prefill8k e2m1: oracle on {len(tokens)} tokens")
+    check_against_oracle(cfg, inp, layer, out, tokens, "e2m1", stage2_rows=srows)
+    assert_repeats_identical(layer, x, weights, out, logits=inp.logits)
 
 
 def test_layer_at_expert_and_k_limits(m):

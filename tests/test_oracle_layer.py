@@ -68,6 +68,41 @@ def test_h2_tie_and_combine():
     assert np.all(r["out_f64"] == c["out"])
 
 
+def test_h4_router_projection_closed_form():
+    """The router projection (the "Router" box of the layer figure) on the
+    hand case H4: exact in fp64 where an fp32 sum would drop the 2^-30 term,
+    and row 0 tells an [E, H] reading of the router matrix from an [H, E] one."""
+    c = HAND["H4"]
+    x = np.array(c["x_bits"], np.uint16)
+    wr = np.repeat(np.array(c["wr_row_bits"], np.uint16)[:, None], x.shape[1], axis=1)
+    lg = moe.router_logits(x, wr)
+    assert lg.tolist() == c["logits"]
+    # the 2^-30 term really is invisible to an fp32 sum
+    assert np.float32(1.0) + np.float32(2.0 ** -30) == np.float32(1.0)
+    # and the layer routes on these logits when given router weights
+    w = _stack([_const_expert(64, 32)] * 3)
+    r = moe.layer(x, *w, k=1, wr_bits=wr, fmt="e4m3")
+    assert r["ids"].ravel().tolist() == [2, 2]
+    assert r["logits_f64"].tolist() == c["logits"]
+
+
+@pytest.mark.parametrize("shape", [(1, 8, 1), (3, 32, 5), (4, 64, 7), (2, 96, 16)])
+def test_router_projection_brute_force(shape):
+    """Explicit loops over the bf16 fields with exactly rounded sums, on random
+    bf16 values spanning several binades (products of two bf16 values are exact
+    in fp64, so the oracle is within a few ulps of the exact sum)."""
+    t, h, e = shape
+    rng = np.random.default_rng(sum(shape))
+    xf = rng.standard_normal((t, h)).astype(np.float32) * np.float32(2.0) ** rng.integers(-8, 8, (t, h))
+    wf = rng.standard_normal((e, h)).astype(np.float32) * np.float32(0.02)
+    xb, wb = synth.f32_to_bf16_bits(xf), synth.f32_to_bf16_bits(wf)
+    lg = moe.router_logits(xb, wb)
+    ref = np.array(bf.router_logits(xb.tolist(), wb.tolist()))
+    scale = np.abs(mx.bf16_to_f64(xb)) @ np.abs(mx.bf16_to_f64(wb)).T
+    assert lg.shape == (t, e)
+    assert np.all(np.abs(lg - ref) <= 4 * h * 2.0 ** -53 * scale)
+
+
 def test_h3_permutation():
     c = HAND["H3"]
     counts, offsets, srt, pos = moe.permute(np.array(c["ids"]), 3)

@@ -81,6 +81,19 @@ def _pins():
                    for a in (0.5, 255.99997, 1.0, 448.0, 449.0, 3e-5))
     check("scale_rule", scale_rule)
 
+    h4 = HAND["H4"]
+    x4 = np.array(h4["x_bits"], np.uint16)
+    wr4 = np.repeat(np.array(h4["wr_row_bits"], np.uint16)[:, None], x4.shape[1], axis=1)
+    check("H4", lambda: moe.router_logits(x4, wr4).tolist() == h4["logits"])
+
+    def router_brute():
+        rng = np.random.default_rng(3)
+        xb = synth.f32_to_bf16_bits(rng.standard_normal((3, 40)).astype(np.float32))
+        wb = synth.f32_to_bf16_bits(rng.standard_normal((5, 40)).astype(np.float32))
+        ref = np.array(bf.router_logits(xb.tolist(), wb.tolist()))
+        return np.all(np.abs(moe.router_logits(xb, wb) - ref) <= 1e-14 * np.abs(ref).max())
+    check("router_brute", router_brute)
+
     def brute():
         cfg = synth.LayerConfig("mut", 3, 64, 4, 2, 64, 1, "normal", 21)
         inp = synth.make_inputs(cfg)
@@ -102,9 +115,23 @@ def patched(mod, name, fn):
         setattr(mod, name, old)
 
 
-_orig = {n: getattr(moe, n) for n in ("route_topk", "permute", "swiglu", "expert_ffn", "combine")}
+_orig = {n: getattr(moe, n) for n in ("router_logits", "route_topk", "permute", "swiglu",
+                                      "expert_ffn", "combine")}
 _origmx = {n: getattr(mx, n) for n in ("e2m1_decode", "e8m0_decode", "unpack_nibbles",
                                        "mx_scale_exponent", "_round_to_elem", "dequant_fp4")}
+
+
+def m_router_transposed(x_bits, wr_bits):
+    """Router matrix read as [H, E] (its buffer reinterpreted) instead of [E, H]."""
+    wr = mx.bf16_to_f64(wr_bits)
+    return mx.bf16_to_f64(x_bits) @ wr.reshape(wr.shape[1], wr.shape[0])
+
+
+def m_router_fp32(x_bits, wr_bits):
+    """x and the router weights cast to fp32 before the product (fp32 sums)."""
+    x32 = mx.bf16_to_f64(x_bits).astype(np.float32)
+    w32 = mx.bf16_to_f64(wr_bits).astype(np.float32)
+    return (x32 @ w32.T).astype(np.float64)
 
 
 def m_swiglu_sign(g, u):
@@ -206,6 +233,8 @@ def m_scale_index_off(packed, scales):
 
 
 MUTATIONS = {
+    "router_transposed": (moe, "router_logits", m_router_transposed),
+    "router_fp32": (moe, "router_logits", m_router_fp32),
     "swiglu_sign": (moe, "swiglu", m_swiglu_sign),
     "swiglu_drops_up": (moe, "swiglu", m_swiglu_gate_only),
     "route_ties_high": (moe, "route_topk", m_route_ties_high),
