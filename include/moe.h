@@ -288,6 +288,31 @@ moe_status moe_fp4_grouped_gemm_stages(const uint16_t* x, int T, int H, int I,
                                        const uint8_t* w2_s, moe_act_format f, float* partials,
                                        void* ws, size_t ws_bytes, int stages, void* stream);
 
+/* ---- allocation-free grouped GEMM -------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc. Exactly
+ * moe_fp4_grouped_gemm (same kernels, same results, same argument meaning
+ * and validation) without a workspace argument: the workspace is a static
+ * device array of MOE_NOALLOC_SCRATCH_BYTES bytes inside the library, one per
+ * GPU, held until the process ends. The call allocates and frees nothing.
+ *  - A shape whose workspace (moe_fp4_grouped_gemm_workspace_bytes) exceeds
+ *    MOE_NOALLOC_SCRATCH_BYTES returns MOE_ERR_WORKSPACE and enqueues nothing
+ *    (32 MiB holds decode batches of up to about 1400 tokens at H = 4096,
+ *    I = 2048, top-8 + shared).
+ *  - Every call on one GPU uses that GPU's one array, and each call clears
+ *    what must start at zero itself. Calls that overlap on one GPU (on
+ *    different streams, or from threads without ordering between them) race
+ *    on the array and must not be made; calls ordered on one stream are safe.
+ *  - The GPU the stream belongs to must be the current device: the first call
+ *    on a device looks up that device's copy of the array. */
+#define MOE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+moe_status moe_fp4_grouped_gemm_noalloc(const uint16_t* x, int T, int H, int I,
+                                        int n_experts_total, int k_total, const int32_t* offsets,
+                                        const int32_t* sorted, const uint8_t* w13,
+                                        const uint8_t* w13_s, const uint8_t* w2,
+                                        const uint8_t* w2_s, moe_act_format f, float* partials,
+                                        void* stream);
+
 /* ---- f3: small-M down projection fused with the combine ---------------------
  * moe_fp4_grouped_gemm followed by moe_combine_fixed_order as one call, for
  * decode-sized batches: the down projection of every row and the

@@ -5,9 +5,40 @@
 
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "moe_launch.h"
 
 namespace {
+
+// Workspace of moe_fp4_grouped_gemm_noalloc: one static array per GPU. In
+// host code `scratch` only stands in for the symbol; its device address on
+// the current GPU comes from scratch_address().
+constexpr size_t kScratchBytes = MOE_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch`, per device, looked up once
+
+// Device address of the current GPU's scratch array (looked up on the first
+// call on that device, with that device current).
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 thread_local int g_last_variant = MOE_VARIANT_NONE;
 
@@ -185,13 +216,15 @@ moe_status moe_fp4_grouped_gemm_workspace_layout(int T, int H, int I, int n_expe
 }
 
 // fused: stage 2 writes out through the combine (topk_w, out) instead of
-// partials.
+// partials. use_scratch: the workspace is the library's static scratch array
+// (ws is ignored); shapes that need more return MOE_ERR_WORKSPACE.
 static moe_status grouped_gemm(const uint16_t* x, int T, int H, int I, int n_experts_total,
                                int k_total, const int32_t* offsets, const int32_t* sorted,
                                const uint8_t* w13, const uint8_t* w13_s, const uint8_t* w2,
                                const uint8_t* w2_s, moe_act_format f, float* partials,
                                bool fused, const float* topk_w, uint16_t* out, void* ws,
-                               size_t ws_bytes, int stages, void* stream) {
+                               size_t ws_bytes, int stages, void* stream,
+                               bool use_scratch = false) {
   const int fc = fmt_code(f);
   if (fc < 0 || !gemm_dims_ok(T, H, I, n_experts_total, k_total)) return MOE_ERR_INVALID_ARG;
   if (stages < 1 || stages > 7) return MOE_ERR_INVALID_ARG;
@@ -204,6 +237,12 @@ static moe_status grouped_gemm(const uint16_t* x, int T, int H, int I, int n_exp
     return MOE_ERR_INVALID_ARG;
   if (!offsets_fit(T, H, I, k_total, fc)) return MOE_ERR_UNSUPPORTED;
   const size_t need = moe::gemm_workspace(T, H, I, n_experts_total, k_total, fc).off[5];
+  if (use_scratch) {
+    if (need > kScratchBytes) return MOE_ERR_WORKSPACE;
+    ws = nullptr;
+    ws_bytes = kScratchBytes;
+    if (T > 0 && scratch_address(&ws) != hipSuccess) return MOE_ERR_LAUNCH;
+  }
   if (T > 0 && (!ws || ws_bytes < need || !aligned(ws, 256))) return MOE_ERR_WORKSPACE;
   moe::GemmArgs a{x, T, H, I, n_experts_total, k_total, fc, offsets, sorted,
                   w13, w13_s, w2, w2_s, partials, static_cast<uint8_t*>(ws), topk_w, out};
@@ -231,6 +270,16 @@ moe_status moe_fp4_grouped_gemm_stages(const uint16_t* x, int T, int H, int I,
                                        void* ws, size_t ws_bytes, int stages, void* stream) {
   return grouped_gemm(x, T, H, I, n_experts_total, k_total, offsets, sorted, w13, w13_s, w2, w2_s,
                       f, partials, false, nullptr, nullptr, ws, ws_bytes, stages, stream);
+}
+
+moe_status moe_fp4_grouped_gemm_noalloc(const uint16_t* x, int T, int H, int I,
+                                        int n_experts_total, int k_total, const int32_t* offsets,
+                                        const int32_t* sorted, const uint8_t* w13,
+                                        const uint8_t* w13_s, const uint8_t* w2,
+                                        const uint8_t* w2_s, moe_act_format f, float* partials,
+                                        void* stream) {
+  return grouped_gemm(x, T, H, I, n_experts_total, k_total, offsets, sorted, w13, w13_s, w2, w2_s,
+                      f, partials, false, nullptr, nullptr, nullptr, 0, 7, stream, true);
 }
 
 int moe_fp4_grouped_gemm_combine_supported(int T, int H, int I, int n_experts_total, int k_total,

@@ -40,6 +40,8 @@ _SIGNATURES = {
                                   _SZ, _P]),
     "moe_fp4_grouped_gemm_stages": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P,
                                          _P, _SZ, _I, _P]),
+    "moe_fp4_grouped_gemm_noalloc": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P,
+                                          _P]),
     "moe_fp4_grouped_gemm_combine_supported": (_I, [_I, _I, _I, _I, _I, _I]),
     "moe_fp4_grouped_gemm_combine": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P,
                                           _P, _P, _SZ, _I, _P]),
@@ -258,6 +260,31 @@ def moe_fp4_grouped_gemm(x, offsets, sorted_, w13, w13_s, w2, w2_s, k_total, fmt
     else:
         _check(lib.moe_fp4_grouped_gemm_stages(*args, stages, _stream(stream)),
                "moe_fp4_grouped_gemm_stages")
+    return partials
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20  # MOE_NOALLOC_SCRATCH_BYTES
+
+
+def moe_fp4_grouped_gemm_noalloc(x, offsets, sorted_, w13, w13_s, w2, w2_s, k_total, partials,
+                                 fmt="e4m3", stream=None):
+    """moe_fp4_grouped_gemm with the library's static scratch as its workspace:
+    nothing is allocated (``partials`` must be given)."""
+    T, H = x.shape
+    NE, two_i, _ = w13.shape
+    I = two_i // 2
+    _need(x, torch.bfloat16, (T, H), "x")
+    _need(offsets, torch.int32, (NE + 1,), "offsets")
+    _need(sorted_, torch.int32, (T * k_total,), "sorted")
+    _need(w13, torch.uint8, (NE, 2 * I, H // 2), "w13")
+    _need(w13_s, torch.uint8, (NE, 2 * I, H // 32), "w13_s")
+    _need(w2, torch.uint8, (NE, H, I // 2), "w2")
+    _need(w2_s, torch.uint8, (NE, H, I // 32), "w2_s")
+    _need(partials, torch.float32, (T * k_total, H), "partials")
+    _check(lib.moe_fp4_grouped_gemm_noalloc(
+        _ptr(x), T, H, I, NE, k_total, _ptr(offsets), _ptr(sorted_), _ptr(w13), _ptr(w13_s),
+        _ptr(w2), _ptr(w2_s), ACT_FORMATS[fmt], _ptr(partials), _stream(stream)),
+        "moe_fp4_grouped_gemm_noalloc")
     return partials
 
 

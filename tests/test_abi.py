@@ -182,3 +182,24 @@ def test_gemm_rejects_shapes_past_32_bit_offsets(m):
     assert call(1 << 20) == m.MOE_ERR_UNSUPPORTED
     assert call((1 << 20) - 1) == m.MOE_ERR_WORKSPACE
     assert call(1 << 19, f=m.ACT_FORMATS["bf16"]) == m.MOE_ERR_UNSUPPORTED   # 2 bytes an element
+
+
+def test_noalloc_gemm_rejects_before_touching_the_gpu(m):
+    """The allocation-free grouped GEMM validates like moe_fp4_grouped_gemm and
+    refuses shapes whose workspace exceeds its static scratch, before any HIP
+    call (so these run without a GPU)."""
+    L = m.lib
+
+    def call(T, H=4096, I=2048, NE=257, kt=9, f=0, x=FAKE):
+        return L.moe_fp4_grouped_gemm_noalloc(x, T, H, I, NE, kt, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                              FAKE, f, FAKE, NUL)
+    need = m.moe_fp4_grouped_gemm_workspace_bytes
+    big = next(T for T in range(1000, 4000, 8) if need(T, 4096, 2048, 257, 9) > m.NOALLOC_SCRATCH_BYTES)
+    assert need(big - 8, 4096, 2048, 257, 9) <= m.NOALLOC_SCRATCH_BYTES < need(big, 4096, 2048, 257, 9)
+    assert call(big) == m.MOE_ERR_WORKSPACE
+    assert call(8192) == m.MOE_ERR_WORKSPACE
+    assert call(64, H=200) == m.MOE_ERR_INVALID_ARG                  # H % 128
+    assert call(64, f=9) == m.MOE_ERR_INVALID_ARG                    # format
+    assert call(64, f=1) == m.MOE_ERR_UNSUPPORTED                    # MXFP6
+    assert call(64, x=NUL) == m.MOE_ERR_INVALID_ARG                  # null pointer
+    assert call(0) == m.MOE_OK                                       # empty batch: nothing enqueued

@@ -1,0 +1,80 @@
+"""The allocation-free grouped GEMM (moe_fp4_grouped_gemm_noalloc) against
+moe_fp4_grouped_gemm with a caller workspace, through the C ABI.
+
+Both run the same kernels, so the fp32 partials must be bit-identical. Two
+calls in a row share the library's static scratch: the second, on a smaller
+input of another geometry, must not see anything the first one left there
+(the work queue and tile lists are rebuilt by every call). The GPU test
+marker applies; it is collected last so that a failure here hides no other
+test."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from tests import gpu_common as gc
+from tests.gpu_common import log
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def m():
+    from paper_2609_15627_amd import moe
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return moe
+
+
+def _inputs(m, shape, seed, fmt):
+    T, H, I, E, k, S = shape
+    cfg = synth.LayerConfig("noalloc", T, H, E, k, I, S, "normal", seed)
+    inp = synth.make_inputs(cfg)
+    x = gc.to_dev_bf16(inp.x)
+    w = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    ids, _ = m.moe_route_topk(torch.from_numpy(inp.logits).cuda(), k, S)
+    _, offsets, srt, _ = m.moe_permute(ids, cfg.NE)
+    return cfg, x, w, offsets, srt
+
+
+def _both(m, cfg, x, w, offsets, srt, fmt):
+    ref = m.moe_fp4_grouped_gemm(x, offsets, srt, *w, cfg.k_total, fmt=fmt)
+    torch.cuda.synchronize()
+    variant = m.moe_last_variant()
+    part = torch.full((cfg.A, cfg.H), float("nan"), dtype=torch.float32, device="cuda")
+    m.moe_fp4_grouped_gemm_noalloc(x, offsets, srt, *w, cfg.k_total, part, fmt=fmt)
+    torch.cuda.synchronize()
+    assert m.moe_last_variant() == variant
+    return ref, part, variant
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e2m1", "bf16"])
+def test_noalloc_matches_workspace_call_twice(m, fmt):
+    # first call: tiled geometry, several row tiles per expert
+    cfg, x, w, offsets, srt = _inputs(m, (300, 512, 512, 4, 2, 0), 3, fmt)
+    log(f"noalloc {fmt}: first call T={cfg.T}")
+    ref, part, v1 = _both(m, cfg, x, w, offsets, srt, fmt)
+    assert torch.equal(part.view(torch.int32), ref.view(torch.int32)), "first call differs"
+    # second call right after, smaller and on the streaming geometry
+    cfg2, x2, w2, offsets2, srt2 = _inputs(m, (37, 512, 384, 16, 4, 1), 5, fmt)
+    log(f"noalloc {fmt}: second call T={cfg2.T}")
+    ref2, part2, v2 = _both(m, cfg2, x2, w2, offsets2, srt2, fmt)
+    assert v2 != v1
+    assert torch.equal(part2.view(torch.int32), ref2.view(torch.int32)), "second call differs"
+    assert not torch.isnan(part2).any()
+
+
+def test_noalloc_decode_shape(m):
+    """The decode workload's dims (T = 64, H = 4096, I = 2048, 256 + 1 experts,
+    top-8), the batch the static scratch is sized for, then a smaller one."""
+    cfg = synth.CONFIGS["decode"]
+    weights = gc.dev_weights(cfg)
+    for T in (64, 5):
+        c = cfg.with_(T=T)
+        inp = synth.make_inputs(c, lazy=True)
+        x = gc.to_dev_bf16(inp.x)
+        ids, _ = m.moe_route_topk(torch.from_numpy(inp.logits).cuda(), c.k, c.n_shared)
+        _, offsets, srt, _ = m.moe_permute(ids, c.NE)
+        log(f"noalloc decode dims T={T}")
+        ref, part, _ = _both(m, c, x, weights, offsets, srt, "e4m3")
+        assert torch.equal(part.view(torch.int32), ref.view(torch.int32))
+    assert m.moe_fp4_grouped_gemm_workspace_bytes(64, 4096, 2048, 257, 9) <= m.NOALLOC_SCRATCH_BYTES
