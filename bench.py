@@ -129,17 +129,21 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True, fused=False):
     # timed region 2: K steps launched eagerly, kernel by kernel
     eager_ms, eager_wall = timed(fwd, steps)
     use_g = graph_ms is not None and graph_ms < eager_ms
-    # distribution of single steps in the faster launch mode (separate pass:
-    # one event between consecutive steps)
+    # distribution of the step time in the faster launch mode (separate pass:
+    # the K steps in 10 batches with an event between batches, so that event
+    # records do not add to short steps); median and minimum over the batches
     one = layer.replay if use_g else fwd
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    nb = min(10, steps)
+    sizes = [steps // nb + (1 if i < steps % nb else 0) for i in range(nb)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(nb + 1)]
     torch.cuda.synchronize()
     evs[0].record(stream)
-    for i in range(steps):
-        one()
+    for i, n in enumerate(sizes):
+        for _ in range(n):
+            one()
         evs[i + 1].record(stream)
     torch.cuda.synchronize()
-    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(steps)])
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) / n for i, n in enumerate(sizes)])
     # per-step breakdown (separate pass: events between the steps of the layer)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
     for i in range(steps):

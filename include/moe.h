@@ -84,7 +84,10 @@ enum {
   MOE_VARIANT_TILED = 2,  /* LDS-tiled MFMA geometry for many rows per expert (prefill) */
   MOE_VARIANT_BF16 = 3,   /* MOE_ACT_BF16: LDS-tiled bf16 geometry (many rows per expert) */
   MOE_VARIANT_MIXED = 4,  /* tiled stage 1, streaming stage 2 (I not a multiple of 512) */
-  MOE_VARIANT_BF16_STREAM = 5 /* MOE_ACT_BF16: weight-streaming bf16 geometry (few rows) */
+  MOE_VARIANT_BF16_STREAM = 5, /* MOE_ACT_BF16: weight-streaming bf16 geometry (few rows) */
+  MOE_VARIANT_SHORT = 6   /* stage 2 on the short-K geometry (I = 128 or 256, many rows per
+                             expert: the whole K extent of a 128-row tile in LDS); stage 1
+                             tiled when H is a multiple of 512, else streaming */
 };
 
 /* Limits checked by the validators. */

@@ -152,13 +152,15 @@ static int max_lds_per_block() {
 // Geometry rule (runtime M), per stage: the LDS-tiled geometry when experts
 // average at least kTiledMinRows rows and the stage's K is a multiple of the
 // tiled K loop's 512 (stage 1: K = H, N tiles of 128 h columns; stage 2:
-// K = I, N tiles of 256 output columns); the weight-streaming geometry
-// otherwise. So a shape like the TP8 expert shard (I = 256) runs stage 1
-// tiled and stage 2 streaming.
+// K = I, N tiles of 256 output columns); with as many rows but K = I of 128
+// or 256, stage 2 runs on the short-K geometry (a tile's whole K extent in
+// LDS); the weight-streaming geometry otherwise. So a shape like the TP8
+// expert shard (I = 256) runs stage 1 tiled and stage 2 short-K.
 constexpr int kTiledMinRows = 64;
 
 struct Geometry {
   bool s1_tiled, s2_tiled;
+  bool s2_short;  // stage 2 on the short-K geometry (I = 128 or 256, many rows)
 };
 
 static Geometry geometry(const GemmArgs& a) {
@@ -166,16 +168,19 @@ static Geometry geometry(const GemmArgs& a) {
   // the BF16 contract: its LDS-tiled kernel takes any K (a multiple of 128)
   if (a.fmt == kFmtBf16) {
     const bool many_bf = A >= (long)kTiledMinRows * a.NE;
-    return Geometry{many_bf, many_bf};
+    return Geometry{many_bf, many_bf, false};
   }
-  const bool many = A >= (long)kTiledMinRows * a.NE &&
-                    (size_t)max_lds_per_block() >= tiled_lds_bytes(a.fmt);
-  return Geometry{many && tiled_k_ok(a.H) && a.I % 128 == 0, many && tiled_ok(a.H, a.I)};
+  const bool rows = A >= (long)kTiledMinRows * a.NE;
+  const bool many = rows && (size_t)max_lds_per_block() >= tiled_lds_bytes(a.fmt);
+  const bool s2_tiled = many && tiled_ok(a.H, a.I);
+  const bool s2_short = rows && !s2_tiled && short_k_ok(a.I) && a.H % 256 == 0 &&
+                        (size_t)max_lds_per_block() >= short_lds_bytes(a.fmt, a.I);
+  return Geometry{many && tiled_k_ok(a.H) && a.I % 128 == 0, s2_tiled, s2_short};
 }
 
 bool fused_combine_ok(const GemmArgs& a) {
   const Geometry g = geometry(a);
-  return a.fmt != kFmtBf16 && !g.s1_tiled && !g.s2_tiled &&
+  return a.fmt != kFmtBf16 && !g.s1_tiled && !g.s2_tiled && !g.s2_short &&
          fused_lds_bytes(a.T, a.k_total, a.I) <= (size_t)max_lds_per_block();
 }
 
@@ -183,7 +188,8 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
                                   Geometry g, hipStream_t s) {
   const bool bf = a.fmt == kFmtBf16;
   const int BM1 = g.s1_tiled ? (bf ? bf16_rows() : tiled_rows()) : (bf ? bf16_stream_rows() : 16);
-  const int BM2 = g.s2_tiled ? (bf ? bf16_rows() : tiled_rows()) : (bf ? bf16_stream_rows() : 16);
+  const int BM2 = g.s2_tiled ? (bf ? bf16_rows() : tiled_rows())
+                             : (g.s2_short ? short_rows() : (bf ? bf16_stream_rows() : 16));
   const long A = (long)a.T * a.k_total;
   uint8_t* lists = a.ws + w.off[4];
   const TileArgs t1 = tile_list(lists, A, a.NE, BM1);
@@ -236,6 +242,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     if (a.out) launch_s2c_stream(S2CArgs{p2, a.topk_w, a.out, a.T, a.k_total}, a.fmt, s);
     else if (bf) (g.s2_tiled ? launch_s2_bf16 : launch_s2_bf16_stream)(p2, t2.mt_bound, s);
     else if (g.s2_tiled) launch_s2_tiled(p2, t2.mt_bound, a.fmt, s);
+    else if (g.s2_short) launch_s2_short(p2, t2.mt_bound, a.fmt, s);
     else launch_s2_stream(p2, t2.mt_bound, a.fmt, s);
   }
   return hipGetLastError();
@@ -244,7 +251,8 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
 hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int* variant) {
   const GemmWorkspace w = gemm_workspace(a.T, a.H, a.I, a.NE, a.k_total, a.fmt);
   const Geometry g = geometry(a);
-  *variant = a.fmt == kFmtBf16 ? (g.s1_tiled ? 3 : 5) : (g.s2_tiled ? 2 : (g.s1_tiled ? 4 : 1));
+  *variant = a.fmt == kFmtBf16 ? (g.s1_tiled ? 3 : 5)
+                               : (g.s2_tiled ? 2 : (g.s2_short ? 6 : (g.s1_tiled ? 4 : 1)));
   if (a.T == 0) return hipSuccess;
   if (a.fmt != 0 && a.fmt != 4 && a.fmt != kFmtBf16) return hipErrorNotSupported;
   if (a.out && !fused_combine_ok(a)) return hipErrorNotSupported;

@@ -38,4 +38,11 @@ bool tiled_k_ok(int K);       // a K extent fits the tiled K loop
 void launch_s1_tiled(const S1Args& p, long mt, int fa, hipStream_t s);
 void launch_s2_tiled(const S2Args& p, long mt, int fa, hipStream_t s);
 
+// Short-K geometry of stage 2 (K = I of 128 or 256, many rows per expert):
+// row tiles of short_rows() rows, the whole K extent of a tile in LDS.
+int short_rows();
+bool short_k_ok(int I);
+size_t short_lds_bytes(int fa, int I);
+void launch_s2_short(const S2Args& p, long mt, int fa, hipStream_t s);
+
 }  // namespace moe

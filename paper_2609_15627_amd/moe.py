@@ -20,6 +20,7 @@ ACT_FORMATS = {"e4m3": 0, "e2m3": 1, "e2m1": 2, "bf16": 3}
 ACT_BITS = {"e4m3": 8, "e2m3": 6, "e2m1": 4, "bf16": 16}
 VARIANT_NONE, VARIANT_STREAM, VARIANT_TILED, VARIANT_BF16, VARIANT_MIXED = 0, 1, 2, 3, 4
 VARIANT_BF16_STREAM = 5
+VARIANT_SHORT = 6
 WS_REGIONS = 6
 
 _P = ctypes.c_void_p

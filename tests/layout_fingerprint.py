@@ -6,9 +6,10 @@ permuted order (16-row blocks inside each 128-wide N tile) and identified the
 mapping by fingerprinting output columns (Correctness recovery / W2
 permutation). These inputs make such a mapping readable from one layer call:
 
-* x is 0.5 everywhere and every W13 code is 1.0 with scale byte 127, so
-  G = U = H/2 and h = (H/2)^2 exactly (sigmoid(H/2) rounds to 1 for H >= 256),
-  a power of two that every activation format holds exactly;
+* x is 0.5 everywhere and the first 256 codes of every W13 row are 1.0 (the
+  rest 0) with scale byte 127, so G = U = 128 and h = 128^2 = 2^14 exactly
+  for every H (sigmoid(128) rounds to 1), a power of two that every
+  activation format holds exactly;
 * W2 row n holds, in its first four 32-element blocks, the constant e2m1 code
   d_b = (n >> 3b) & 7 (the base-8 digits of n) with scale byte 119 + 4b, and
   code 0 everywhere else. Its partial is then
@@ -31,7 +32,8 @@ def weights(H: int, I: int):
     if H < 256 or H > 4096 or I < 128 or H % 32 or I % 32:
         raise ValueError("fingerprint weights need 256 <= H <= 4096 and I >= 128")
     one = 2 | (2 << 4)                                   # two e2m1 codes of value 1.0
-    w13 = np.full((2 * I, H // 2), one, np.uint8)
+    w13 = np.zeros((2 * I, H // 2), np.uint8)
+    w13[:, :128] = one                                   # K elements 0..255
     w13s = np.full((2 * I, H // 32), 127, np.uint8)
     codes = np.zeros((H, I), np.uint8)
     n = np.arange(H)
@@ -50,7 +52,7 @@ def x_bits(T: int, H: int):
 def decode(partial_row, H: int):
     """Weight-row index of every output column of one partial row (-1 where
     the value is not a valid fingerprint)."""
-    h = (H / 2.0) ** 2
+    h = 128.0 ** 2
     v2 = np.asarray(partial_row, np.float64) * 2.0 / (h * 2.0 ** -3)
     doubled_to_code = {int(2 * val): c for c, val in enumerate(bf.paper_e2m1_table()[:8])}
     out = np.full(v2.shape, -1, np.int64)

@@ -241,8 +241,10 @@ def small_case(T, H, I, E, k, S, seed, routing="normal"):
     (300, 1024, 512, 4, 2, 1),    # tiled geometry: ~150-300 rows per expert, ragged tiles
     (600, 512, 1024, 2, 1, 0),    # tiled geometry: a full 256-row tile plus a ragged one
     (130, 512, 512, 2, 1, 0),     # tiled geometry: ~65 rows per expert, partial row blocks
-    (400, 512, 256, 4, 2, 0),     # tiled stage 1, streaming stage 2 (I = 256, like the TP shard)
-    (300, 1024, 384, 4, 2, 1),    # the same with I = 384 and a shared expert
+    (400, 512, 256, 4, 2, 0),     # tiled stage 1, short-K stage 2 (I = 256, like the TP shard)
+    (300, 1024, 384, 4, 2, 1),    # tiled stage 1, streaming stage 2 (I = 384) and a shared expert
+    (700, 768, 128, 5, 2, 1),     # streaming stage 1 (H = 768), short-K stage 2 with K = 128
+    (170, 1024, 256, 3, 2, 0),    # short-K stage 2: tiles of 128 rows and ragged ones under 64
     (300, 2048, 512, 4, 2, 0),    # tiled stage 1 with K = 2048: middle groups of the K loop
 ])
 def test_small_layers(m, shape, fmt):
@@ -384,7 +386,7 @@ def test_full_size_configs(m, name, ntok):
     log(f"full {name}: forward")
     layer, out = run_layer(m, cfg, x, weights, logits=inp.logits)
     variant = m.moe_last_variant()
-    assert variant == {"decode": m.VARIANT_STREAM, "tpshard": m.VARIANT_MIXED}.get(
+    assert variant == {"decode": m.VARIANT_STREAM, "tpshard": m.VARIANT_SHORT}.get(
         name, m.VARIANT_TILED)
     ids_ref, w_ref = omoe.route_topk(inp.logits, cfg.k, cfg.n_shared)
     assert np.array_equal(layer.ids.cpu().numpy(), ids_ref)

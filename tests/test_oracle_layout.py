@@ -35,7 +35,7 @@ def test_printed_maps_are_mutual_inverses():
 
 
 @pytest.mark.parametrize("fmt", ["e4m3", "e2m1", "bf16", None])
-@pytest.mark.parametrize("H,I", [(256, 128), (512, 512)])
+@pytest.mark.parametrize("H,I", [(256, 128), (512, 512), (768, 128)])
 def test_logical_layout_decodes_to_identity(H, I, fmt):
     p = _partials(fp.weights(H, I), H, fmt=fmt)
     for row in p:
