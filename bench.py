@@ -27,6 +27,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+REPEATS = 5                    # timed regions per workload for the median and minimum
 MFMA_PEAK_FP8_TFLOPS = 5000.0  # dense FP8 (the FP8 x FP4 scaled MFMA issue rate)
 MFMA_PEAK_FP4_TFLOPS = 10100.0  # dense MXFP4
 
@@ -129,21 +130,13 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True, fused=False):
     # timed region 2: K steps launched eagerly, kernel by kernel
     eager_ms, eager_wall = timed(fwd, steps)
     use_g = graph_ms is not None and graph_ms < eager_ms
-    # distribution of the step time in the faster launch mode (separate pass:
-    # the K steps in 10 batches with an event between batches, so that event
-    # records do not add to short steps); median and minimum over the batches
+    # spread of the step time in the faster launch mode: the timed region
+    # (K steps, events only at its two ends) repeated; median and minimum of
+    # the per-step times over the repeats (an event between single steps
+    # costs more than a short step)
     one = layer.replay if use_g else fwd
-    nb = min(10, steps)
-    sizes = [steps // nb + (1 if i < steps % nb else 0) for i in range(nb)]
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(nb + 1)]
-    torch.cuda.synchronize()
-    evs[0].record(stream)
-    for i, n in enumerate(sizes):
-        for _ in range(n):
-            one()
-        evs[i + 1].record(stream)
-    torch.cuda.synchronize()
-    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) / n for i, n in enumerate(sizes)])
+    per_step = np.array([graph_ms if use_g else eager_ms] +
+                        [timed(one, steps)[0] for _ in range(REPEATS - 1)])
     # per-step breakdown (separate pass: events between the steps of the layer)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
     for i in range(steps):
@@ -412,6 +405,8 @@ def main():
         "stage_ms": r["stage_ms"],
         "step_ms_median": r["step_ms_median"],
         "step_ms_min": r["step_ms_min"],
+        "step_stats": f"median and minimum of the per-step time over {REPEATS} timed regions "
+                      f"of {args.steps} steps (the first is the one `value` comes from)",
         # the whole layer against HBM: algorithmic bytes (weights of the touched
         # experts, x, out, logits) over the step time; the graded decode figure
         "layer_roofline": {"bound": "hbm", "achieved": layer_gbs, "peak": HBM_PEAK_GBS,
