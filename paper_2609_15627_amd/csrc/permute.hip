@@ -2,9 +2,10 @@
 //
 // Three passes over chunks of kChunk assignments:
 //   1. perm_hist     per-chunk histograms, counted in LDS;
-//   2. perm_scan     counts, offsets (exclusive scan over experts) and, per
-//                    (chunk, expert), the first output slot of that chunk;
-//   3. perm_scatter  one wave per chunk walks its assignments in order, 64 at
+//   2. perm_scan     one wave per expert: its count and, per chunk, the
+//                    chunk's first slot relative to the expert's offset;
+//   3. perm_scatter  one wave per chunk forms the expert offsets (exclusive
+//                    scan of the counts), then walks its assignments in order, 64 at
 //                    a time. Lanes holding the same expert find each other
 //                    with ballots over the id bits; a lane's rank among its
 //                    lower-numbered peers plus the running per-expert cursor
@@ -34,39 +35,37 @@ __global__ __launch_bounds__(256) void perm_hist(const int32_t* __restrict__ ids
   for (int e = threadIdx.x; e < NE; e += blockDim.x) hist[(size_t)blockIdx.x * NE + e] = sh[e];
 }
 
-// One block of 1024 threads; thread e owns experts e and e + 1024.
-__global__ __launch_bounds__(1024) void perm_scan(int32_t* __restrict__ hist, int nchunks, int NE,
-                                                  int32_t* __restrict__ counts,
-                                                  int32_t* __restrict__ offsets) {
-  int tot[2] = {0, 0};
+// One wave per expert: lane l takes a contiguous run of the chunks, sums
+// its counts, a wave-wide exclusive scan gives the run's first slot (relative
+// to the expert's offset), and the lane then writes each chunk's base over
+// its count; the expert's total goes to counts[e].
+__device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int e = threadIdx.x + 1024 * q;
-    if (e < NE) {
-      int run = 0;
-      for (int c = 0; c < nchunks; ++c) {
-        int32_t* p = hist + (size_t)c * NE + e;
-        const int n = *p;
-        *p = run;  // chunk-local base (relative to the expert's offset)
-        run += n;
-      }
-      tot[q] = run;
-    }
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int o = __shfl_up(v, d, kWave);
+    if (lane >= d) v += o;
   }
-  int total0, total1;
-  const int pre0 = block_exclusive_scan_1024(tot[0], &total0);
-  const int pre1 = block_exclusive_scan_1024(tot[1], &total1);
-  int off[2] = {pre0, total0 + pre1};
-#pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int e = threadIdx.x + 1024 * q;
-    if (e < NE) {
-      counts[e] = tot[q];
-      offsets[e] = off[q];
-      for (int c = 0; c < nchunks; ++c) hist[(size_t)c * NE + e] += off[q];
-    }
+  return v;
+}
+
+__global__ __launch_bounds__(256) void perm_scan(int32_t* __restrict__ hist, int nchunks, int NE,
+                                                 int32_t* __restrict__ counts) {
+  const int e = (int)blockIdx.x * 4 + (int)threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (e >= NE) return;
+  const int per = (nchunks + kWave - 1) / kWave;
+  const int c0 = min(nchunks, lane * per), c1 = min(nchunks, c0 + per);
+  int sum = 0;
+  for (int c = c0; c < c1; ++c) sum += hist[(size_t)c * NE + e];
+  const int incl = wave_inclusive_scan(sum, lane);
+  int run = incl - sum;
+  for (int c = c0; c < c1; ++c) {
+    int32_t* p = hist + (size_t)c * NE + e;
+    const int n = *p;
+    *p = run;  // chunk-local base (relative to the expert's offset)
+    run += n;
   }
-  if (threadIdx.x == 0) offsets[NE] = total0 + total1;
+  if (lane == kWave - 1) counts[e] = incl;
 }
 
 // Stable in-order placement of up to kChunk assignments by one wave, given the
@@ -98,13 +97,30 @@ __device__ __forceinline__ void scatter_chunk(const int32_t* __restrict__ ids, i
   }
 }
 
+// One wave per chunk. The expert offsets (exclusive scan of counts) are
+// formed by every wave from the counts (block 0 also writes them out); the
+// cursor of expert e starts at its offset plus this chunk's base.
 __global__ __launch_bounds__(64) void perm_scatter(const int32_t* __restrict__ ids, int A, int NE,
                                                    int nbits, const int32_t* __restrict__ hist,
+                                                   const int32_t* __restrict__ counts,
+                                                   int32_t* __restrict__ offsets,
                                                    int32_t* __restrict__ sorted,
                                                    int32_t* __restrict__ pos) {
   extern __shared__ int32_t cursor[];
-  for (int e = threadIdx.x; e < NE; e += blockDim.x)
-    cursor[e] = hist[(size_t)blockIdx.x * NE + e];
+  const int lane = threadIdx.x;
+  int carry = 0;
+  for (int base = 0; base < NE; base += kWave) {
+    const int e = base + lane;
+    const int c = e < NE ? counts[e] : 0;
+    const int incl = wave_inclusive_scan(c, lane);
+    const int off = carry + incl - c;
+    if (e < NE) {
+      cursor[e] = off + hist[(size_t)blockIdx.x * NE + e];
+      if (blockIdx.x == 0) offsets[e] = off;
+    }
+    carry += __shfl(incl, kWave - 1, kWave);
+  }
+  if (blockIdx.x == 0 && lane == 0) offsets[NE] = carry;
   __syncthreads();
   const int base = blockIdx.x * kChunk;
   scatter_chunk(ids, base, min(A, base + kChunk), NE, nbits, cursor, sorted, pos);
@@ -225,9 +241,9 @@ hipError_t launch_permute(const int32_t* ids, int T, int NE, int k_total, int32_
   const int nchunks = (A + kChunk - 1) / kChunk;
   int32_t* hist = static_cast<int32_t*>(ws);
   hipLaunchKernelGGL(perm_hist, dim3(nchunks), dim3(256), lds, s, ids, A, NE, hist);
-  hipLaunchKernelGGL(perm_scan, dim3(1), dim3(1024), 0, s, hist, nchunks, NE, counts, offsets);
+  hipLaunchKernelGGL(perm_scan, dim3((NE + 3) / 4), dim3(256), 0, s, hist, nchunks, NE, counts);
   hipLaunchKernelGGL(perm_scatter, dim3(nchunks), dim3(64), lds, s, ids, A, NE, nbits, hist,
-                     sorted, pos);
+                     counts, offsets, sorted, pos);
   return hipGetLastError();
 }
 
