@@ -221,6 +221,32 @@ def test_combine_fixed_order(m):
     assert np.all(np.abs(gotf - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-3)
 
 
+@pytest.mark.parametrize("kt", [8, 9, 3])
+def test_combine_layouts_bit_identical(m, kt):
+    """Batches of 256 tokens or more take the wide layout (4 columns a
+    thread, non-temporal loads); smaller ones the narrow one. The same rows
+    through both give the same bits, and the wide one is the exact fp32 fmaf
+    chain on sampled elements."""
+    log(f"combine layouts kt={kt}")
+    rng = np.random.default_rng(kt)
+    T, H = 300, 512
+    P = (rng.standard_normal((T * kt, H)) * 1e3).astype(np.float32)
+    w = rng.random((T, kt)).astype(np.float32)
+    Pd, wd = torch.from_numpy(P).cuda(), torch.from_numpy(w).cuda()
+    wide = bf16_bits(m.moe_combine_fixed_order(Pd, wd))
+    narrow = np.concatenate([
+        bf16_bits(m.moe_combine_fixed_order(Pd[: 200 * kt].contiguous(), wd[:200].contiguous())),
+        bf16_bits(m.moe_combine_fixed_order(Pd[200 * kt:].contiguous(), wd[200:].contiguous()))])
+    torch.cuda.synchronize()
+    assert np.array_equal(wide, narrow)
+    for t, h in [(0, 0), (257, 3), (299, 511), (128, 260)]:
+        acc = np.float32(0)
+        for j in range(kt):
+            acc = _round_f32(Fraction(float(w[t, j])) * Fraction(float(P[t * kt + j, h]))
+                             + Fraction(float(acc)))
+        assert wide[t, h] == mx.f64_to_bf16(np.array([float(acc)]))[0]
+
+
 @pytest.mark.parametrize("fmt", ["e4m3", "bf16"])
 def test_layer_empty_batch(m, fmt):
     """T = 0 through every call of the layer: empty outputs, status OK, no
