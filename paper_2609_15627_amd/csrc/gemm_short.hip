@@ -174,7 +174,8 @@ __global__ __launch_bounds__(256, 2) void s2_short_kernel(S2Args p) {
     }
   }
 
-  // ---- unique-slot fp32 partial stores ----
+  // ---- unique-slot fp32 partial stores (non-temporal: read once, much
+  // later, by the combine) ----
   const int* sidx = reinterpret_cast<const int*>(lds + L::kIdx);
   float* const col = p.partials + nc0 + 128 * wn + r;
 #pragma unroll
@@ -186,7 +187,7 @@ __global__ __launch_bounds__(256, 2) void s2_short_kernel(S2Args p) {
         if (row < nrows) {
           float* dst = col + (size_t)sidx[row] * p.H;
 #pragma unroll
-          for (int nb = 0; nb < 4; ++nb) dst[32 * nb] = acc[mb][nb][i];
+          for (int nb = 0; nb < 4; ++nb) __builtin_nontemporal_store(acc[mb][nb][i], dst + 32 * nb);
         }
       }
     }

@@ -746,7 +746,8 @@ __device__ __forceinline__ S2Tile<FA> s2_setup(const S2Args& p, int4 tile, int n
 
 // Persistent stage-2 kernel. Per tile: K loop; then the next tile's first
 // DMA stages go out before this tile's epilogue (fp32 partial rows to their
-// unique assignment slots), so the epilogue's stores cover their latency.
+// unique assignment slots, non-temporal stores: the combine reads them once,
+// much later), so the epilogue's stores cover their latency.
 // The epilogue only uses the second scale buffer (assignment slots of the
 // tile's rows, and the ticket word), which no prologue writes.
 template <int FA>
@@ -807,7 +808,7 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
           if (row < nrows) {
             float* dst = col + (size_t)slot16[i] * p.H;
 #pragma unroll
-            for (int nb = 0; nb < 4; ++nb) dst[32 * nb] = acc[mb][nb][i];
+            for (int nb = 0; nb < 4; ++nb) __builtin_nontemporal_store(acc[mb][nb][i], dst + 32 * nb);
           }
         }
       }
