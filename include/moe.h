@@ -64,9 +64,10 @@ typedef enum {
  * formats instead. */
 typedef enum {
   MOE_ACT_MXFP8_E4M3 = 0, /* 1 byte per element */
-  MOE_ACT_MXFP6_E2M3 = 1, /* 24 bytes per 32-element block, element j in bits [6j, 6j+6);
-                             moe_quantize_act only: the grouped GEMM calls return
-                             MOE_ERR_UNSUPPORTED for it */
+  MOE_ACT_MXFP6_E2M3 = 1, /* 24 bytes per 32-element block, element j in bits [6j, 6j+6)
+                             (the matrix cores' FP6 operand: a lane's 32 elements in six
+                             words); in the grouped GEMM's workspace each block's 24 bytes
+                             sit in a 32-byte slot. Not available fused with the combine. */
   MOE_ACT_MXFP4_E2M1 = 2, /* 2 elements per byte, low nibble first */
   /* The paper's BF16 contract (Large-M CK and the meaning of the earlier
    * 6.42k result; Accepted large-prefill configuration): x is not quantised,
@@ -250,8 +251,7 @@ moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f
  * bytes, 256-byte aligned, contents need not be initialised. Its regions are
  * reported by moe_fp4_grouped_gemm_workspace_layout (for inspection by tests).
  * Requires T >= 0, H > 0, I > 0, H % 128 == 0, I % 128 == 0,
- * 1 <= NE <= MOE_MAX_EXPERTS_TOTAL, 1 <= k_total <= MOE_MAX_K_TOTAL;
- * f = MOE_ACT_MXFP6_E2M3 returns MOE_ERR_UNSUPPORTED.
+ * 1 <= NE <= MOE_MAX_EXPERTS_TOTAL, 1 <= k_total <= MOE_MAX_K_TOTAL.
  * The geometry (MOE_VARIANT_*) is chosen per stage from T * k_total / NE and
  * the stage's K extent (the tiled K loop takes multiples of 512) and reported
  * by moe_last_variant(); under MOE_ACT_BF16 from T * k_total / NE alone
@@ -264,8 +264,10 @@ size_t moe_fp4_grouped_gemm_workspace_bytes(int T, int H, int I, int n_experts_t
 
 /* Byte offsets of the workspace regions: [0] x codes [T, H*bits/8], [1] x
  * scales [T, H/32], [2] h codes [T*k_total, I*bits/8] in sorted-row order,
- * [3] h scales [T*k_total, I/32], [4] tile list, [5] total bytes. With
- * MOE_ACT_BF16 regions 0, 1 and 3 are empty and region 2 holds h as bf16. */
+ * [3] h scales [T*k_total, I/32], [4] tile list, [5] total bytes. bits is 8
+ * for MXFP8 and for MXFP6 (its 24-byte blocks in 32-byte slots), 4 for
+ * MXFP4. With MOE_ACT_BF16 regions 0, 1 and 3 are empty and region 2 holds
+ * h as bf16. */
 #define MOE_WS_REGIONS 6
 moe_status moe_fp4_grouped_gemm_workspace_layout(int T, int H, int I, int n_experts_total,
                                                  int k_total, moe_act_format f,

@@ -187,7 +187,7 @@ moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f
 // The GEMM kernels address activation rows (x, h) and one expert's weights
 // with 32-bit byte offsets from a base: each must stay below 4 GiB.
 static bool offsets_fit(int T, int H, int I, int k_total, int fc) {
-  const double bits = moe::act_bits(fc);
+  const double bits = moe::ws_act_bits(fc);
   const double lim = 4294967296.0;
   return (double)T * H * bits / 8 < lim && (double)T * k_total * I * bits / 8 < lim &&
          (double)H * I < lim;
@@ -228,7 +228,7 @@ static moe_status grouped_gemm(const uint16_t* x, int T, int H, int I, int n_exp
   const int fc = fmt_code(f);
   if (fc < 0 || !gemm_dims_ok(T, H, I, n_experts_total, k_total)) return MOE_ERR_INVALID_ARG;
   if (stages < 1 || stages > 7) return MOE_ERR_INVALID_ARG;
-  if (fc == 2) return MOE_ERR_UNSUPPORTED;
+  if (fused && fc == 2) return MOE_ERR_UNSUPPORTED;
   if (T > 0 && (!x || !offsets || !sorted || !w13 || !w13_s || !w2 || !w2_s))
     return MOE_ERR_INVALID_ARG;
   if (T > 0 && (fused ? (!topk_w || !out) : !partials)) return MOE_ERR_INVALID_ARG;

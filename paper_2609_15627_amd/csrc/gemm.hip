@@ -88,7 +88,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(const uint16_t* __restrict__
   if ((int)blockIdx.x < nqb) {
     if constexpr (FMT >= 0) {
       const long b = (long)blockIdx.x * 1024 + threadIdx.x;
-      if (b < nblk) quant_block<FMT>(x, b, codes, scales);
+      if (b < nblk) quant_block<FMT, true>(x, b, codes, scales);
     }
     return;
   }
@@ -122,7 +122,7 @@ static TileArgs tile_list(uint8_t* base, long A, int NE, int BM) {
 GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt) {
   auto al = [](size_t v) { return (v + 255) / 256 * 256; };
   const size_t A = (size_t)T * k_total;
-  const size_t bits = act_bits(fmt);
+  const size_t bits = ws_act_bits(fmt);
   GemmWorkspace w;
   size_t o = 0;
   const bool mx = fmt != kFmtBf16;  // the BF16 contract has no x codes and no scales
@@ -207,6 +207,9 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     else if (a.fmt == 0)
       hipLaunchKernelGGL(prep_kernel<0>, grid, dim3(1024), lds, s, a.x, nblk, codes, scales, nqb,
                          a.offsets, a.NE, BM1, t1, BM2, t2);
+    else if (a.fmt == 2)
+      hipLaunchKernelGGL(prep_kernel<2>, grid, dim3(1024), lds, s, a.x, nblk, codes, scales, nqb,
+                         a.offsets, a.NE, BM1, t1, BM2, t2);
     else
       hipLaunchKernelGGL(prep_kernel<4>, grid, dim3(1024), lds, s, a.x, nblk, codes, scales, nqb,
                          a.offsets, a.NE, BM1, t1, BM2, t2);
@@ -254,7 +257,7 @@ hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int
   *variant = a.fmt == kFmtBf16 ? (g.s1_tiled ? 3 : 5)
                                : (g.s2_tiled ? 2 : (g.s2_short ? 6 : (g.s1_tiled ? 4 : 1)));
   if (a.T == 0) return hipSuccess;
-  if (a.fmt != 0 && a.fmt != 4 && a.fmt != kFmtBf16) return hipErrorNotSupported;
+  if (a.fmt != 0 && a.fmt != 2 && a.fmt != 4 && a.fmt != kFmtBf16) return hipErrorNotSupported;
   if (a.out && !fused_combine_ok(a)) return hipErrorNotSupported;
   return launch_geometry(a, w, stages, g, s);
 }

@@ -14,6 +14,10 @@ struct ActBytes<0> {
   static constexpr int kBlock = 32;
 };
 template <>
+struct ActBytes<2> {
+  static constexpr int kBlock = 32;  // a 24-byte e2m3 block in a 32-byte slot
+};
+template <>
 struct ActBytes<4> {
   static constexpr int kBlock = 16;
 };
@@ -185,6 +189,32 @@ __device__ __forceinline__ void s1_epilogue(const v4f* acc, const S1Args& p, int
         if (rl < nrows) {
           p.hq[r * p.I + col] = (uint8_t)c0;
           p.hq[r * p.I + col + 16] = (uint8_t)c1;
+        }
+      } else if constexpr (FA == 2) {
+        // the block's 32 codes are spread over the 16 lanes of group g (two
+        // each, positions c16 and c16 + 16): each lane places its two at bits
+        // 6 c16 and 96 + 6 c16 of the 192-bit block, an OR over the 16 lanes
+        // joins them, and lanes 0..5 store the six words of the slot
+        uint32_t wv[6];
+#pragma unroll
+        for (int k = 0; k < 6; ++k) wv[k] = 0;
+        const int o0 = 6 * c16, o1 = 96 + 6 * c16;
+#pragma unroll
+        for (int k = 0; k < 6; ++k) {
+          if (o0 / 32 == k) wv[k] |= c0 << (o0 % 32);
+          if (o0 / 32 + 1 == k && o0 % 32 > 26) wv[k] |= c0 >> (32 - o0 % 32);
+          if (o1 / 32 == k) wv[k] |= c1 << (o1 % 32);
+          if (o1 / 32 + 1 == k && o1 % 32 > 26) wv[k] |= c1 >> (32 - o1 % 32);
+        }
+#pragma unroll
+        for (int k = 0; k < 6; ++k) {
+          static_for<4>([&](auto L) { wv[k] |= (uint32_t)wave_partner<decltype(L)::value>((int)wv[k]); });
+        }
+        if (rl < nrows && c16 < 6) {
+          uint32_t v = wv[0];
+#pragma unroll
+          for (int k = 1; k < 6; ++k) v = c16 == k ? wv[k] : v;
+          *reinterpret_cast<uint32_t*>(p.hq + r * p.I + (hc0 + 32 * q) + 4 * c16) = v;
         }
       } else {
         // two adjacent columns per byte, low nibble first

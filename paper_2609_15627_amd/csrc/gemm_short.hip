@@ -55,7 +55,7 @@ __device__ __forceinline__ void s_dma4(const uint8_t* src, uint8_t* base) {
 template <int FA, int KS>
 struct SL {
   static constexpr int K = 128 * KS;
-  static constexpr int kARow = FA == 0 ? K : K / 2;  // activation bytes per row
+  static constexpr int kARow = FA == 4 ? K / 2 : K;  // activation bytes per row (e2m3: slots)
   static constexpr int kBRow = K / 2;                // weight bytes per row
   static constexpr int kACh = kARow / 16, kBCh = kBRow / 16;
   static constexpr int kSRow = K / 32;               // scale bytes per row
@@ -69,8 +69,8 @@ struct SL {
 
 size_t short_lds_bytes(int fa, int I) {
   const int ks = I / 128;
-  if (fa == 0) return ks == 1 ? SL<0, 1>::kBytes : SL<0, 2>::kBytes;
-  return ks == 1 ? SL<4, 1>::kBytes : SL<4, 2>::kBytes;
+  if (fa == 4) return ks == 1 ? SL<4, 1>::kBytes : SL<4, 2>::kBytes;
+  return ks == 1 ? SL<0, 1>::kBytes : SL<0, 2>::kBytes;
 }
 
 bool short_k_ok(int I) { return I == 128 || I == 256; }
@@ -142,6 +142,11 @@ __global__ __launch_bounds__(256, 2) void s2_short_kernel(S2Args p) {
           const v4u hi = *reinterpret_cast<const v4u*>(row + 16 * ((8 * t + 4 + 2 * s + h) ^ key));
           a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w,
                       (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+        } else if constexpr (FA == 2) {  // the 32-byte slot of block 4t + 2h + s
+          const int b = 4 * t + 2 * h + s;
+          const v4u lo = *reinterpret_cast<const v4u*>(row + 16 * ((2 * b) ^ key));
+          const v4u hi = *reinterpret_cast<const v4u*>(row + 16 * ((2 * b + 1) ^ key));
+          a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, 0, 0};
         } else {
           const v4u lo = *reinterpret_cast<const v4u*>(row + 16 * ((4 * t + 2 * h + s) ^ key));
           a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, 0, 0, 0, 0};
@@ -212,6 +217,9 @@ void launch_s2_short(const S2Args& p, long mt, int fa, hipStream_t s) {
   if (fa == 0) {
     if (one) launch_short<0, 1>(p, mt, s);
     else launch_short<0, 2>(p, mt, s);
+  } else if (fa == 2) {
+    if (one) launch_short<2, 1>(p, mt, s);
+    else launch_short<2, 2>(p, mt, s);
   } else {
     if (one) launch_short<4, 1>(p, mt, s);
     else launch_short<4, 2>(p, mt, s);

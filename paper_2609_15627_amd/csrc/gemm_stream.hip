@@ -95,6 +95,10 @@ __device__ __forceinline__ void frag_codes(Frag<FA, J, NB>& f, const uint8_t* a_
         const uint8_t* base = a_row + (size_t)step * 32 + 128 * j + 16 * g;
         f.a[2 * j] = ld16<false>(base);
         f.a[2 * j + 1] = ld16<false>(base + 64);
+      } else if constexpr (FA == 2) {  // block step + 4j + g: the 32-byte slot
+        const uint8_t* base = a_row + (size_t)(step + 4 * j + g) * 32;
+        f.a[2 * j] = ld16<false>(base);
+        f.a[2 * j + 1] = ld16<false>(base + 16);
       } else {
         f.a[j] = ld16<false>(a_row + (size_t)(step + 4 * j + g) * 16);
       }
@@ -144,6 +148,9 @@ __device__ __forceinline__ void frag_mma(const Frag<FA, J, NB>& f, v4f* acc) {
     if constexpr (FA == 0) {
       const v4u lo = f.a[2 * j], hi = f.a[2 * j + 1];
       a = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+    } else if constexpr (FA == 2) {  // six words: the 32 codes of the block at 6 bits each
+      const v4u lo = f.a[2 * j], hi = f.a[2 * j + 1];
+      a = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, 0, 0};
     } else {
       const v4u lo = f.a[j];
       a = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, 0, 0, 0, 0};
@@ -554,11 +561,13 @@ static void launch_s2(const S2Args& p, long mt, hipStream_t s) {
 // per wave in stage 2.
 void launch_s1_stream(const S1Args& p, long mt, int fa, hipStream_t s) {
   if (fa == 0) launch_s1<0, 2>(p, mt, s);
+  else if (fa == 2) launch_s1<2, 2>(p, mt, s);
   else launch_s1<4, 2>(p, mt, s);
 }
 
 void launch_s2_stream(const S2Args& p, long mt, int fa, hipStream_t s) {
   if (fa == 0) launch_s2<0, 4>(p, mt, s);
+  else if (fa == 2) launch_s2<2, 4>(p, mt, s);
   else launch_s2<4, 4>(p, mt, s);
 }
 

@@ -44,6 +44,7 @@
 // current tile's epilogue.
 #include "gemm_common.h"
 #include "gemm_launch.h"
+#include "quant_dev.h"
 
 namespace moe {
 
@@ -56,13 +57,14 @@ constexpr int kSG = 4;         // K steps per scale group (16 scale bytes per ro
 
 template <int FA>
 struct TL {
-  static constexpr int kARow = FA == 0 ? 128 : 64;  // activation bytes per row per K step
+  // activation bytes per row per K step (e2m3: four 32-byte slots, like e4m3)
+  static constexpr int kARow = FA == 4 ? 64 : 128;
   static constexpr int kB = TBM * kARow;             // weight rows follow the activation rows
   static constexpr int kStage = kB + TBN * 64;
   // K-step stages in the LDS ring: 3 of 48 KiB with FP8 activations, 4 of
   // 32 KiB with FP4 ones (one more step of DMA lead in the same LDS, and the
   // ring slot of step 4q + J is J)
-  static constexpr int kNS = FA == 0 ? 3 : 4;
+  static constexpr int kNS = FA == 4 ? 4 : 3;
   static constexpr int kS = kNS * kStage;            // two scale buffers follow the stages
   static constexpr int kSBuf = (TBM + TBN) * 16;
   static constexpr int kLoop = kS + 2 * kSBuf;
@@ -119,7 +121,7 @@ struct TSrc {
 // DMA instruction ci (1 KiB of the chunk-swizzled activation rows).
 template <int FA>
 __device__ __forceinline__ void t_aslot(int ci, int lane, int* row, int* chunk) {
-  if constexpr (FA == 0) {
+  if constexpr (FA != 4) {
     *row = 8 * ci + lane / 8;
     *chunk = (lane % 8) ^ ((*row >> 1) & 7);
   } else {
@@ -206,6 +208,9 @@ __device__ __forceinline__ void t_read_ops(const uint8_t* st, const TLane& L, TO
       const v4u hi = *reinterpret_cast<const v4u*>(st + L.a1[S] + mb * 32 * Lo::kARow);
       o.a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w,
                     (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+    } else if constexpr (FA == 2) {
+      const v4u hi = *reinterpret_cast<const v4u*>(st + L.a1[S] + mb * 32 * Lo::kARow);
+      o.a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, 0, 0};
     } else {
       o.a[mb] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, 0, 0, 0, 0};
     }
@@ -314,7 +319,7 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   // group's first step when that came after stage k + 1 (1 <= J <= NS - 2).
   constexpr int kOutStages = !LAST ? NS - 2 : (NS - 2 < 2 - J ? NS - 2 : 2 - J);
   constexpr int kOutScales = (!LAST && J >= 1 && J <= NS - 2) ? 1 : 0;
-  constexpr int kAPieces = FA == 0 ? 2 : 1;
+  constexpr int kAPieces = FA == 4 ? 1 : 2;
   constexpr int kOpReads = NMB > 0 ? 4 + kAPieces * NMB : 0;
   constexpr int kScaleReads = NMB > 0 ? 4 + NMB : 0;
   constexpr int kPreN = 4 * NMB < kPre ? 4 * NMB : kPre;  // sub-step-1 products before the barrier
@@ -405,6 +410,9 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
       if constexpr (FA == 0)
         X.a[mb] = v8i{(int)alo[mb].x, (int)alo[mb].y, (int)alo[mb].z, (int)alo[mb].w,
                       (int)ahi[mb].x, (int)ahi[mb].y, (int)ahi[mb].z, (int)ahi[mb].w};
+      else if constexpr (FA == 2)
+        X.a[mb] = v8i{(int)alo[mb].x, (int)alo[mb].y, (int)alo[mb].z, (int)alo[mb].w,
+                      (int)ahi[mb].x, (int)ahi[mb].y, 0, 0};
       else
         X.a[mb] = v8i{(int)alo[mb].x, (int)alo[mb].y, (int)alo[mb].z, (int)alo[mb].w, 0, 0, 0, 0};
     }
@@ -568,6 +576,11 @@ __device__ __forceinline__ TLane t_lane(int w, int lane) {
       const int sw = (ar >> 1) & 7;
       L.a0[s] = ar * 128 + 16 * ((2 * s + h) ^ sw);
       L.a1[s] = ar * 128 + 16 * ((4 + 2 * s + h) ^ sw);
+    } else if constexpr (FA == 2) {
+      // the 32-byte slot of block 2h + s: chunks 2(2h + s) and 2(2h + s) + 1
+      const int sw = (ar >> 1) & 7, b = 2 * h + s;
+      L.a0[s] = ar * 128 + 16 * ((2 * b) ^ sw);
+      L.a1[s] = ar * 128 + 16 * ((2 * b + 1) ^ sw);
     } else {
       L.a0[s] = ar * 64 + 16 * ((2 * h + s) ^ ((ar >> 2) & 3));
       L.a1[s] = L.a0[s];
@@ -647,7 +660,7 @@ __device__ __forceinline__ uint32_t t_xhalf(uint32_t x, int h) {
 template <int FA>
 __device__ __forceinline__ void s1_epilogue(const S1Args& p, v16f (*acc)[4], int row0, int nrows,
                                             int hc0, int wm, int wn, int lane, int nmb) {
-  constexpr int kCB = FA == 0 ? 32 : 16;  // code bytes per 32-element block
+  constexpr int kCB = FA == 4 ? 16 : 32;  // code bytes per 32-element block (e2m3: its slot)
   const int r = lane & 31, h = lane >> 5;
   const size_t crow = (size_t)(p.I / 32) * kCB;  // code bytes per hq row
   const int blk0 = (hc0 + 64 * wn) / 32;         // the wave's two h blocks
@@ -676,6 +689,11 @@ __device__ __forceinline__ void s1_epilogue(const S1Args& p, v16f (*acc)[4], int
           if constexpr (FA == 0) {
             d[k] = e4m3_pack4(ldexpf(hv[4 * k], -X), ldexpf(hv[4 * k + 1], -X),
                               ldexpf(hv[4 * k + 2], -X), ldexpf(hv[4 * k + 3], -X));
+          } else if constexpr (FA == 2) {  // one code per byte, packed to 6 bits below
+            uint32_t v = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v |= mx_encode<FA>(ldexpf(hv[4 * k + j], -X)) << (8 * j);
+            d[k] = v;
           } else {
             uint32_t v = 0;
 #pragma unroll
@@ -690,6 +708,14 @@ __device__ __forceinline__ void s1_epilogue(const S1Args& p, v16f (*acc)[4], int
           if constexpr (FA == 0) {
             const uint4 v = h ? make_uint4(r0, d[2], r1, d[3]) : make_uint4(d[0], r0, d[1], r1);
             *reinterpret_cast<uint4*>(crow_p + (blk0 + q) * kCB + 16 * h) = v;
+          } else if constexpr (FA == 2) {  // 16 codes at 6 bits: 12 bytes of the slot
+            const uint32_t wv[4] = {h ? r0 : d[0], h ? d[2] : r0, h ? r1 : d[1], h ? d[3] : r1};
+            uint32_t pk[3];
+            pack6x16(wv, pk);
+            uint32_t* dst = reinterpret_cast<uint32_t*>(crow_p + (blk0 + q) * kCB + 12 * h);
+            dst[0] = pk[0];
+            dst[1] = pk[1];
+            dst[2] = pk[2];
           } else {
             const uint2 v = h ? make_uint2(r0 | (d[2] << 16), r1 | (d[3] << 16))
                               : make_uint2(d[0] | (r0 << 16), d[1] | (r1 << 16));
@@ -869,7 +895,7 @@ __global__ __launch_bounds__(256, 1) void s1_tiled_kernel(S1Args p) {
 int tiled_rows() { return TBM; }
 
 size_t tiled_lds_bytes(int fa) {
-  return fa == 0 ? (size_t)t_lds_s1<0>() : (size_t)t_lds_s1<4>();
+  return fa == 4 ? (size_t)t_lds_s1<4>() : (size_t)t_lds_s1<0>();
 }
 
 // Scale groups cover 512 K elements in both stages; N tiles are 128 h
@@ -908,11 +934,13 @@ static void launch_t2(const S2Args& p, long mt, hipStream_t s) {
 
 void launch_s1_tiled(const S1Args& p, long mt, int fa, hipStream_t s) {
   if (fa == 0) launch_t1<0>(p, mt, s);
+  else if (fa == 2) launch_t1<2>(p, mt, s);
   else launch_t1<4>(p, mt, s);
 }
 
 void launch_s2_tiled(const S2Args& p, long mt, int fa, hipStream_t s) {
   if (fa == 0) launch_t2<0>(p, mt, s);
+  else if (fa == 2) launch_t2<2>(p, mt, s);
   else launch_t2<4>(p, mt, s);
 }
 

@@ -37,6 +37,9 @@ hipError_t launch_permute(const int32_t* ids, int T, int NE, int k_total, int32_
 // e2m1, kFmtBf16 the BF16 contract (bf16 activations, no scales).
 constexpr int kFmtBf16 = 16;
 int act_bits(int fmt);
+// Bits per activation element in the grouped GEMM's workspace (e2m3 blocks
+// sit in 32-byte slots there).
+int ws_act_bits(int fmt);
 hipError_t launch_quantize_act(const uint16_t* x, long rows, int K, int fmt, uint8_t* codes,
                                uint8_t* scales, hipStream_t s);
 

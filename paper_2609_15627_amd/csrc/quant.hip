@@ -6,6 +6,7 @@
 namespace moe {
 
 int act_bits(int fmt) { return fmt == kFmtBf16 ? 16 : (fmt == 0 ? 8 : (fmt == 2 ? 6 : 4)); }
+int ws_act_bits(int fmt) { return fmt == 2 ? 8 : act_bits(fmt); }
 
 template <int FMT>
 __global__ __launch_bounds__(256) void quant_act_kernel(const uint16_t* __restrict__ x, long nblk,

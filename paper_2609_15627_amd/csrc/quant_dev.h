@@ -8,15 +8,35 @@
 //   e2m3  24 bytes, element j in bits [6j, 6j+6) of the little-endian block;
 //   e2m1  16 bytes, element 2i in the low nibble of byte i.
 // These are the register layouts the matrix cores read, so the GEMM loads a
-// lane's 32-element operand as one contiguous run of bytes.
+// lane's 32-element operand as one contiguous run of bytes. Inside the
+// grouped GEMM's workspace an e2m3 block sits in a 32-byte slot (its 24 bytes,
+// then 8 unused), so its activation rows have the FP8 rows' byte geometry
+// (SLOT = true).
 #pragma once
 
 #include "moe_dev.h"
 
 namespace moe {
 
+// 16 e2m3 codes, one per byte of w[0..3] (code j in byte j % 4 of w[j / 4]),
+// packed at 6 bits each into 12 bytes (code j at bits 6j).
+__device__ __forceinline__ void pack6x16(const uint32_t* w, uint32_t* p) {
+  uint64_t lo = 0, hi = 0;  // codes 0..9 in lo (60 bits), 10..15 in hi
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const uint64_t c = (w[j / 4] >> (8 * (j % 4))) & 0x3fu;
+    if (j < 10) lo |= c << (6 * j);
+    else hi |= c << (6 * (j - 10));
+  }
+  // 96 bits: lo holds bits 0..59, hi bits 60..95
+  const uint64_t b0 = lo | (hi << 60), b1 = hi >> 4;
+  p[0] = (uint32_t)b0;
+  p[1] = (uint32_t)(b0 >> 32);
+  p[2] = (uint32_t)b1;
+}
+
 // Quantise block b (32 consecutive elements of x) into codes and scales[b].
-template <int FMT>
+template <int FMT, bool SLOT = false>
 __device__ __forceinline__ void quant_block(const uint16_t* __restrict__ x, long b,
                                             uint8_t* __restrict__ codes,
                                             uint8_t* __restrict__ scales) {
@@ -72,7 +92,7 @@ __device__ __forceinline__ void quant_block(const uint16_t* __restrict__ x, long
       p[word] |= c[j] << sh;
       if (sh > 26) p[word + 1] |= c[j] >> (32 - sh);
     }
-    uint2* dst = reinterpret_cast<uint2*>(codes + b * 24);
+    uint2* dst = reinterpret_cast<uint2*>(codes + b * (SLOT ? 32 : 24));
     dst[0] = make_uint2(p[0], p[1]);
     dst[1] = make_uint2(p[2], p[3]);
     dst[2] = make_uint2(p[4], p[5]);

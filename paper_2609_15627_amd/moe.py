@@ -207,7 +207,14 @@ def moe_permute(topk_ids, n_experts_total, out=None, ws=None, stream=None):
 
 
 def act_code_bytes(K, fmt):
+    """Bytes of K activation codes as moe_quantize_act packs them."""
     return K * ACT_BITS[fmt] // 8
+
+
+def ws_code_bytes(K, fmt):
+    """Bytes of K activation codes in the grouped GEMM's workspace (an e2m3
+    block of 24 bytes sits in a 32-byte slot there)."""
+    return K if fmt == "e2m3" else act_code_bytes(K, fmt)
 
 
 def moe_quantize_act(x, fmt="e4m3", codes=None, scales=None, stream=None):

@@ -62,6 +62,22 @@ def dev_weights(cfg, share=True):
     return tuple(a[:cfg.NE] for a in full)
 
 
+def ws_codes(b, fmt):
+    """Workspace activation code bytes [rows, n] -> one code per element: e2m1
+    packs two per byte (low nibble first); e2m3 holds each 32-element block's
+    24 bytes (code j at bits 6j) in a 32-byte slot; e4m3 one per byte."""
+    b = np.asarray(b, np.uint8)
+    if fmt == "e4m3":
+        return b
+    if fmt == "e2m1":
+        out = np.empty(b.shape[:-1] + (2 * b.shape[-1],), np.uint8)
+        out[..., 0::2], out[..., 1::2] = b & 15, b >> 4
+        return out
+    slots = b.reshape(b.shape[0], -1, 32)[:, :, :24]
+    bits = np.unpackbits(slots, axis=-1, bitorder="little").reshape(b.shape[0], -1, 32, 6)
+    return (bits * (1 << np.arange(6))).sum(-1).reshape(b.shape[0], -1).astype(np.uint8)
+
+
 def rowrel(y, ref):
     """max over rows of max|y - ref| / max|ref| (row-wise infinity-norm relative error)."""
     y = np.asarray(y, np.float64)

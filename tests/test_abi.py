@@ -92,8 +92,11 @@ def test_gemm_rejects(m):
     assert call(NE=0) == 1
     assert call(kt=40) == 1
     assert call(f=7) == 1
-    assert call(f=1) == m.MOE_ERR_UNSUPPORTED   # MXFP6 activations not built
     assert call(ws=NUL) == m.MOE_ERR_WORKSPACE
+    assert call(f=1, ws=NUL) == m.MOE_ERR_WORKSPACE   # MXFP6 goes as far as the workspace check
+    # MXFP6 blocks sit in 32-byte slots in the workspace: as many code bytes as MXFP8
+    assert m.moe_fp4_grouped_gemm_workspace_layout(8, 256, 128, 4, 2, "e2m3") == \
+        m.moe_fp4_grouped_gemm_workspace_layout(8, 256, 128, 4, 2, "e4m3")
     need = m.moe_fp4_grouped_gemm_workspace_bytes(8, 256, 128, 4, 2, "e4m3")
     assert need > 0 and call(ws_bytes=need - 1) == m.MOE_ERR_WORKSPACE
     assert m.moe_fp4_grouped_gemm_workspace_bytes(8, 200, 128, 4, 2) == 0
@@ -200,6 +203,5 @@ def test_noalloc_gemm_rejects_before_touching_the_gpu(m):
     assert call(8192) == m.MOE_ERR_WORKSPACE
     assert call(64, H=200) == m.MOE_ERR_INVALID_ARG                  # H % 128
     assert call(64, f=9) == m.MOE_ERR_INVALID_ARG                    # format
-    assert call(64, f=1) == m.MOE_ERR_UNSUPPORTED                    # MXFP6
     assert call(64, x=NUL) == m.MOE_ERR_INVALID_ARG                  # null pointer
     assert call(0) == m.MOE_OK                                       # empty batch: nothing enqueued

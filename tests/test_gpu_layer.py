@@ -54,18 +54,17 @@ GRID = {"e4m3": (448.0, -6, 3), "e2m3": (7.5, 0, 3), "e2m1": (6.0, 0, 1)}
 def gpu_hq_rows(layer, cfg, rows, fmt):
     """The GPU's h codes (one code per element) and scale bytes of sorted rows
     ``rows``, copied from the grouped GEMM's workspace."""
-    rb = m_act_bytes(cfg.I, fmt)
+    rb = m_ws_bytes(cfg.I, fmt)
     hq = layer.workspace_view(2)[: cfg.A * rb].view(cfg.A, rb)
     hs = layer.workspace_view(3)[: cfg.A * cfg.I // 32].view(cfg.A, cfg.I // 32)
     idx = torch.from_numpy(np.asarray(rows, np.int64)).cuda()
-    q = hq.index_select(0, idx).cpu().numpy()
-    if fmt == "e2m1":
-        q = mx.unpack_nibbles(q)
+    q = gc.ws_codes(hq.index_select(0, idx).cpu().numpy(), fmt)
     return q, hs.index_select(0, idx).cpu().numpy()
 
 
-def m_act_bytes(K, fmt):
-    return K * {"e4m3": 8, "e2m3": 6, "e2m1": 4}[fmt] // 8
+def m_ws_bytes(K, fmt):
+    """Workspace bytes of K activation codes (e2m3 blocks in 32-byte slots)."""
+    return K * {"e4m3": 8, "e2m3": 8, "e2m1": 4}[fmt] // 8
 
 
 def check_hq_codes(layer, cfg, ref, fmt):
@@ -231,7 +230,7 @@ def small_case(T, H, I, E, k, S, seed, routing="normal"):
     return cfg, synth.make_inputs(cfg)
 
 
-@pytest.mark.parametrize("fmt", ["e4m3", "e2m1"])
+@pytest.mark.parametrize("fmt", ["e4m3", "e2m3", "e2m1"])
 @pytest.mark.parametrize("shape", [
     (37, 512, 384, 16, 4, 1),     # ragged: ~10 rows per expert, K tail, 3 h tiles
     (200, 384, 384, 4, 2, 0),     # many rows per expert: 7 row tiles with a ragged tail
@@ -259,9 +258,8 @@ def test_small_layers(m, shape, fmt):
                                   oracle_x_tokens=cfg.T)
     assert np.array_equal(layer.ids.cpu().numpy(), ref["ids"])
     assert np.array_equal(layer.perm[2].cpu().numpy(), ref["sorted"])
-    xq = layer.workspace_view(0)[: cfg.T * m.act_code_bytes(cfg.H, fmt)].cpu().numpy()
-    xq = xq.reshape(cfg.T, -1)
-    assert np.array_equal(mx.unpack_nibbles(xq) if fmt == "e2m1" else xq, ref["xq"])
+    xq = layer.workspace_view(0)[: cfg.T * m.ws_code_bytes(cfg.H, fmt)].cpu().numpy()
+    assert np.array_equal(gc.ws_codes(xq.reshape(cfg.T, -1), fmt), ref["xq"])
     xs = layer.workspace_view(1)[: cfg.T * cfg.H // 32].cpu().numpy().reshape(cfg.T, -1)
     assert np.array_equal(xs, ref["xs"])
 
@@ -424,22 +422,23 @@ def test_metamorphic_w2_scale_doubles_output(m):
     assert np.array_equal(gc.bf16_bits(out3), gc.bf16_bits(out)[perm])
 
 
-def test_full_size_prefill_mxfp4_activations(m):
-    """The 8K prefill with MXFP4 activations (the FP4-rate run of the bench):
-    routing exact, tokens covering the row classes against the oracle in the
-    same format, ten runs bit-identical."""
+@pytest.mark.parametrize("fmt", ["e2m1", "e2m3"])
+def test_full_size_prefill_fp4_rate_activations(m, fmt):
+    """The 8K prefill with MXFP4 or MXFP6 activations (the FP4-rate runs of the
+    bench): routing exact, tokens covering the row classes against the oracle
+    in the same format, ten runs bit-identical."""
     cfg = synth.CONFIGS["prefill8k"]
     inp = synth.make_inputs(cfg, lazy=True)
     weights = gc.dev_weights(cfg)
     x = gc.to_dev_bf16(inp.x)
-    log("full prefill8k e2m1: forward")
-    layer, out = run_layer(m, cfg, x, weights, logits=inp.logits, fmt="e2m1")
+    log(f"full prefill8k {fmt}: forward")
+    layer, out = run_layer(m, cfg, x, weights, logits=inp.logits, fmt=fmt)
     assert m.moe_last_variant() == m.VARIANT_TILED
     ids_ref, _ = omoe.route_topk(inp.logits, cfg.k, cfg.n_shared)
     assert np.array_equal(layer.ids.cpu().numpy(), ids_ref)
     tokens, srows = _row_class_sample(cfg, omoe.permute(ids_ref, cfg.NE), 16)
-    log(f"full prefill8k e2m1: oracle on {len(tokens)} tokens")
-    check_against_oracle(cfg, inp, layer, out, tokens, "e2m1", stage2_rows=srows, named=True)
+    log(f"full prefill8k {fmt}: oracle on {len(tokens)} tokens")
+    check_against_oracle(cfg, inp, layer, out, tokens, fmt, stage2_rows=srows, named=True)
     assert_repeats_identical(layer, x, weights, out, logits=inp.logits)
 
 

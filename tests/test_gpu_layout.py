@@ -26,7 +26,7 @@ def m():
     return moe
 
 
-@pytest.mark.parametrize("fmt", ["e4m3", "e2m1", "bf16"])
+@pytest.mark.parametrize("fmt", ["e4m3", "e2m3", "e2m1", "bf16"])
 @pytest.mark.parametrize("T,H,I,variants", [
     (5, 256, 128, (1, 5)),       # weight-streaming geometry (MX / BF16 contract)
     (300, 512, 512, (2, 3)),     # LDS-tiled geometry: a full 256-row tile and a ragged one
