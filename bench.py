@@ -39,8 +39,9 @@ def log(msg):
 # Source files each timed kernel is built from; a stored counter reading is
 # only reused while these are unchanged.
 KERNEL_SOURCES = {
-    "s1_stream_kernel": ["gemm_stream.hip", "gemm_common.h", "moe_dev.h"],
-    "s1_tiled_kernel": ["gemm_tiled.hip", "gemm_common.h", "moe_dev.h"],
+    "s1_stream_kernel": ["gemm_stream.hip", "gemm_common.h", "gemm_launch.h", "moe_dev.h"],
+    "s1_tiled_kernel": ["gemm_tiled.hip", "gemm_common.h", "gemm_launch.h", "quant_dev.h",
+                        "moe_dev.h"],
 }
 PROFILES = os.path.join(ROOT, "profiles")
 
@@ -199,7 +200,9 @@ def measure_workload(name, steps, fmt, use_graph, weights_np=None):
             "down_fused_with_combine": r["fused"],
             "layer_GBps": gb, "layer_hbm_frac": gb / HBM_PEAK_GBS,
             "layer_TFLOPs": tf, "layer_frac_of_fp8_peak": tf / MFMA_PEAK_FP8_TFLOPS,
-            "layer_frac_of_fp4_peak": tf / MFMA_PEAK_FP4_TFLOPS}
+            "layer_frac_of_fp4_peak": tf / MFMA_PEAK_FP4_TFLOPS,
+            "gate_up_traffic": stored_traffic("s1_tiled_kernel", name),
+            "gate_up_algorithmic_bytes": r["gate_up_bytes"]}
 
 
 MFMA_PEAK_BF16_TFLOPS = 2500.0  # dense bf16
