@@ -4,12 +4,17 @@
 //   1. perm_hist     per-chunk histograms, counted in LDS;
 //   2. perm_scan     one wave per expert: its count and, per chunk, the
 //                    chunk's first slot relative to the expert's offset;
-//   3. perm_scatter  one wave per chunk forms the expert offsets (exclusive
-//                    scan of the counts), then walks its assignments in order, 64 at
-//                    a time. Lanes holding the same expert find each other
-//                    with ballots over the id bits; a lane's rank among its
-//                    lower-numbered peers plus the running per-expert cursor
-//                    in LDS is its slot, which keeps the sort stable.
+//   3. perm_scatter  one workgroup of 16 waves per chunk forms the expert
+//                    offsets (exclusive scan of the counts); wave w places
+//                    the chunk's assignments [64 w, 64 w + 64). Lanes holding
+//                    the same expert find each other with ballots over the
+//                    id bits (a lane's rank among its lower-numbered peers);
+//                    per-wave expert counts in LDS, prefixed over the waves,
+//                    order the waves. Slot = expert offset + chunk base +
+//                    earlier waves' count + rank, which keeps the sort stable
+//                    with no serial pass. (More experts than fit the per-wave
+//                    counts: one wave walks the chunk 64 at a time with a
+//                    running per-expert cursor instead.)
 // Small inputs (one chunk) run all three steps in one workgroup, spread over
 // its 16 waves when the experts' per-wave counts fit LDS.
 // Integer counting only, so the result is exact and run-to-run identical.
@@ -126,6 +131,79 @@ __global__ __launch_bounds__(64) void perm_scatter(const int32_t* __restrict__ i
   scatter_chunk(ids, base, min(A, base + kChunk), NE, nbits, cursor, sorted, pos);
 }
 
+// Wave-level part of the 16-wave placement: assignment a of this lane (a < A
+// taken), its expert e (ok: a valid id) and its rank among the wave's
+// earlier lanes with the same expert; the group's highest lane records the
+// group size in cnt[w * NE + e] (cnt zeroed beforehand, a barrier after).
+__device__ __forceinline__ void wave_rank16(const int32_t* __restrict__ ids, int a, int A, int NE,
+                                            int nbits, int32_t* cnt, int* e_out, bool* ok_out,
+                                            int* rank_out) {
+  const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int e = a < A ? ids[a] : -1;
+  const bool ok = (unsigned)e < (unsigned)NE;
+  uint64_t peers = __ballot(ok);
+  for (int b = 0; b < nbits; ++b) {
+    const bool bit = ok && ((e >> b) & 1);
+    const uint64_t m = __ballot(bit);
+    peers &= bit ? m : ~m;
+  }
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+  const int rank = __popcll(peers & lt);
+  __syncthreads();  // cnt was zeroed by other threads
+  if (ok && (peers >> lane) == 1ull) cnt[w * NE + e] = rank + 1;
+  *e_out = e;
+  *ok_out = ok;
+  *rank_out = rank;
+}
+
+// Exclusive prefix of the 16 per-wave counts of expert threadIdx.x (in
+// place); returns the expert's total. Call after a barrier.
+__device__ __forceinline__ int prefix_waves16(int32_t* cnt, int NE) {
+  int c = 0;
+  if ((int)threadIdx.x < NE) {
+    for (int v = 0; v < 16; ++v) {
+      const int n = cnt[v * NE + threadIdx.x];
+      cnt[v * NE + threadIdx.x] = c;
+      c += n;
+    }
+  }
+  return c;
+}
+
+// The scatter with 16 waves per chunk (NE <= kSmallNE).
+__global__ __launch_bounds__(1024) void perm_scatter16(const int32_t* __restrict__ ids, int A,
+                                                       int NE, int nbits,
+                                                       const int32_t* __restrict__ hist,
+                                                       const int32_t* __restrict__ counts,
+                                                       int32_t* __restrict__ offsets,
+                                                       int32_t* __restrict__ sorted,
+                                                       int32_t* __restrict__ pos) {
+  extern __shared__ int32_t sh[];
+  int32_t* cnt = sh;            // [16][NE]
+  int32_t* base = sh + 16 * NE;  // [NE]: expert offset + this chunk's base
+  for (int i = threadIdx.x; i < 16 * NE; i += blockDim.x) cnt[i] = 0;
+  const int c = (int)threadIdx.x < NE ? counts[threadIdx.x] : 0;
+  int total;
+  const int off = block_exclusive_scan_1024(c, &total);
+  if ((int)threadIdx.x < NE) {
+    base[threadIdx.x] = off + hist[(size_t)blockIdx.x * NE + threadIdx.x];
+    if (blockIdx.x == 0) offsets[threadIdx.x] = off;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) offsets[NE] = total;
+  const int a = (int)blockIdx.x * kChunk + (int)threadIdx.x;
+  int e, rank;
+  bool ok;
+  wave_rank16(ids, a, A, NE, nbits, cnt, &e, &ok, &rank);
+  __syncthreads();
+  prefix_waves16(cnt, NE);
+  __syncthreads();
+  if (ok) {
+    const int dest = base[e] + cnt[(threadIdx.x / kWave) * NE + e] + rank;
+    sorted[dest] = a;
+    pos[a] = dest;
+  }
+}
+
 // All three steps in one workgroup of 1024 threads (A <= kChunk).
 __global__ __launch_bounds__(1024) void perm_small(const int32_t* __restrict__ ids, int A, int NE,
                                                    int nbits, int32_t* __restrict__ counts,
@@ -175,30 +253,12 @@ __global__ __launch_bounds__(1024) void perm_small16(const int32_t* __restrict__
   extern __shared__ int32_t sh[];
   int32_t* cnt = sh;             // [16][NE]: per-wave counts, then their prefix over waves
   int32_t* off = sh + 16 * NE;   // [NE]: expert offsets
-  const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   for (int i = threadIdx.x; i < 16 * NE; i += blockDim.x) cnt[i] = 0;
-  const int a = 64 * w + lane;
-  const int e = a < A ? ids[a] : -1;
-  const bool ok = (unsigned)e < (unsigned)NE;
-  uint64_t peers = __ballot(ok);
-  for (int b = 0; b < nbits; ++b) {
-    const bool bit = ok && ((e >> b) & 1);
-    const uint64_t m = __ballot(bit);
-    peers &= bit ? m : ~m;
-  }
-  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
-  const int rank = __popcll(peers & lt);
+  int e, rank;
+  bool ok;
+  wave_rank16(ids, (int)threadIdx.x, A, NE, nbits, cnt, &e, &ok, &rank);
   __syncthreads();
-  if (ok && (peers >> lane) == 1ull) cnt[w * NE + e] = rank + 1;  // the group's highest lane
-  __syncthreads();
-  int c = 0;
-  if ((int)threadIdx.x < NE) {
-    for (int v = 0; v < 16; ++v) {
-      const int n = cnt[v * NE + threadIdx.x];
-      cnt[v * NE + threadIdx.x] = c;
-      c += n;
-    }
-  }
+  const int c = prefix_waves16(cnt, NE);
   int total;
   const int p0 = block_exclusive_scan_1024(c, &total);
   if ((int)threadIdx.x < NE) {
@@ -209,9 +269,9 @@ __global__ __launch_bounds__(1024) void perm_small16(const int32_t* __restrict__
   if (threadIdx.x == 0) offsets[NE] = total;
   __syncthreads();
   if (ok) {
-    const int dest = off[e] + cnt[w * NE + e] + rank;
-    sorted[dest] = a;
-    pos[a] = dest;
+    const int dest = off[e] + cnt[(threadIdx.x / kWave) * NE + e] + rank;
+    sorted[dest] = threadIdx.x;
+    pos[threadIdx.x] = dest;
   }
 }
 
@@ -242,8 +302,12 @@ hipError_t launch_permute(const int32_t* ids, int T, int NE, int k_total, int32_
   int32_t* hist = static_cast<int32_t*>(ws);
   hipLaunchKernelGGL(perm_hist, dim3(nchunks), dim3(256), lds, s, ids, A, NE, hist);
   hipLaunchKernelGGL(perm_scan, dim3((NE + 3) / 4), dim3(256), 0, s, hist, nchunks, NE, counts);
-  hipLaunchKernelGGL(perm_scatter, dim3(nchunks), dim3(64), lds, s, ids, A, NE, nbits, hist,
-                     counts, offsets, sorted, pos);
+  if (NE <= kSmallNE)
+    hipLaunchKernelGGL(perm_scatter16, dim3(nchunks), dim3(1024), 17 * lds, s, ids, A, NE, nbits,
+                       hist, counts, offsets, sorted, pos);
+  else
+    hipLaunchKernelGGL(perm_scatter, dim3(nchunks), dim3(64), lds, s, ids, A, NE, nbits, hist,
+                       counts, offsets, sorted, pos);
   return hipGetLastError();
 }
 

@@ -141,7 +141,9 @@ def test_permute_configs(m, name):
                                      (1000, 9, 257), (5000, 2, 1), (3000, 32, 1100),
                                      # one workgroup, 16 waves: up to 1024 assignments, 512 experts
                                      (341, 3, 512), (113, 9, 257), (64, 16, 300), (1, 32, 512),
-                                     (32, 32, 2)])
+                                     (32, 32, 2),
+                                     # chunks of 1024 placed by 16 waves each (512 experts at most)
+                                     (700, 3, 512), (2049, 1, 64), (4100, 8, 256)])
 def test_permute_shapes(m, T, kt, ne):
     log(f"permute T={T} kt={kt} ne={ne}")
     rng = np.random.default_rng(T + ne)
