@@ -22,6 +22,10 @@ skew32k    32768   4096   256   8   2048   0       Zipf(1.2) popularity + Gumbel
 tpshard    4096    4096   256   8   256    0       logits N(0, 1)
 =========  ======  =====  ====  ==  =====  ======  =========================
 
+prefill8k_bal is prefill8k with 'balanced' routing (every routed expert gets
+exactly T*k/E = 256 rows, so no row tile is ragged): a measurement companion
+of prefill8k, not a separate workload.
+
 Common to all: activations x ~ N(0, 1) rounded to bf16; expert weights are FP4
 e2m1 codes uniform over the 16 codes (bytes uniform over 0..255 hold two
 independent codes); one E8M0 scale per 32 weights with exponent uniform over
@@ -47,7 +51,7 @@ class LayerConfig:
     k: int
     I: int
     n_shared: int = 0
-    routing: str = "normal"      # 'router' | 'normal' | 'zipf'
+    routing: str = "normal"      # 'router' | 'normal' | 'zipf' | 'balanced'
     seed: int = 0
     zipf_s: float = 1.2
     zipf_empty: int = 8          # least-popular experts forced empty (zipf only)
@@ -76,6 +80,7 @@ CONFIGS = {
     "prefill8k": LayerConfig("prefill8k", 8192, 4096, 256, 8, 2048, 1, "normal"),
     "skew32k": LayerConfig("skew32k", 32768, 4096, 256, 8, 2048, 0, "zipf"),
     "tpshard": LayerConfig("tpshard", 4096, 4096, 256, 8, 256, 0, "normal"),
+    "prefill8k_bal": LayerConfig("prefill8k_bal", 8192, 4096, 256, 8, 2048, 1, "balanced"),
 }
 
 
@@ -109,7 +114,7 @@ def gen_router_weight(cfg: LayerConfig) -> np.ndarray:
 
 
 def gen_logits(cfg: LayerConfig) -> np.ndarray:
-    """fp32 router logits [T, E] for 'normal' and 'zipf' routing.
+    """fp32 router logits [T, E] for 'normal', 'zipf' and 'balanced' routing.
 
     normal: iid N(0, 1), near-uniform expert load.
     zipf:   expert with popularity rank r gets bias -s*ln(r) (the ``zipf_empty``
@@ -120,6 +125,16 @@ def gen_logits(cfg: LayerConfig) -> np.ndarray:
     """
     if cfg.routing == "normal":
         return _rng(cfg, S_ROUTE, 1).standard_normal((cfg.T, cfg.E), dtype=np.float32)
+    if cfg.routing == "balanced":
+        # token t picks experts (t*k + j) % E, j = 0..k-1, in that order
+        # (logit 16 - j); every other logit is N(0, 1) clipped to [-8, 8].
+        # Expert e then holds exactly T*k/E assignments when E divides T*k.
+        lg = np.clip(_rng(cfg, S_ROUTE, 3).standard_normal((cfg.T, cfg.E), dtype=np.float32),
+                     -8, 8)
+        t = np.arange(cfg.T)[:, None]
+        j = np.arange(cfg.k)[None, :]
+        lg[np.broadcast_to(t, (cfg.T, cfg.k)), (t * cfg.k + j) % cfg.E] = 16.0 - j
+        return lg
     if cfg.routing == "zipf":
         rng = _rng(cfg, S_ROUTE, 2)
         rank = rng.permutation(cfg.E) + 1

@@ -370,7 +370,7 @@ def _row_class_sample(cfg, perm, ntok, n_mid=2, seed=7):
 
 
 @pytest.mark.parametrize("name,ntok", [("decode", 64), ("prefill8k", 32), ("skew32k", 32),
-                                       ("tpshard", 64)])
+                                       ("tpshard", 64), ("prefill8k_bal", 16)])
 def test_full_size_configs(m, name, ntok):
     """Full-size workloads: route, permutation and activation codes compared in
     full; outputs, h codes and stage-2 partials on tokens and rows chosen to

@@ -120,3 +120,16 @@ def test_shared_column_kept():
 def test_rejects_bad_options(bad):
     with pytest.raises(ValueError):
         omoe.route_topk_ex(_logits(2, 16, 7), 2, **bad)
+
+
+def test_balanced_routing_gives_equal_loads():
+    """The 'balanced' synthetic routing (the prefill8k_bal measurement
+    companion) gives every routed expert exactly T*k/E assignments and token t
+    the experts (t*k + j) % E in pick order j."""
+    import synth
+    cfg = synth.CONFIGS["prefill8k_bal"]
+    ids, w = omoe.route_topk(synth.gen_logits(cfg), cfg.k, cfg.n_shared)
+    t = np.arange(cfg.T)[:, None]
+    assert np.array_equal(ids[:, :cfg.k], (t * cfg.k + np.arange(cfg.k)[None, :]) % cfg.E)
+    counts = np.bincount(ids.ravel(), minlength=cfg.NE)
+    assert (counts[:cfg.E] == cfg.T * cfg.k // cfg.E).all() and counts[cfg.E] == cfg.T
