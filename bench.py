@@ -299,8 +299,11 @@ def host_cpu():
 
 def cpu_baseline(cfg, weights_np, fmt):
     """The fp64 oracle, as it is, on the whole layer of the workload (every
-    token, routing included) and on the whole tiny layer (router projection
-    included), BLAS threads set to the host cores this process may use."""
+    token, routing included), on the whole tiny layer (router projection
+    included) and on the whole TP-shard layer, BLAS threads set to the host
+    cores this process may use. (The 8K and 32K prefill layers are left out:
+    any token sample of them touches every expert, and the oracle expands
+    each expert's weights to fp64 first, about a minute of CPU time.)"""
     import synth
     from oracle import moe as omoe
     from threadpoolctl import threadpool_limits
@@ -316,12 +319,20 @@ def cpu_baseline(cfg, weights_np, fmt):
         t = time.perf_counter()
         omoe.layer(x, *weights_np, k=cfg.k, n_shared=cfg.n_shared, logits=logits, fmt=fmt)
         dt = time.perf_counter() - t
+        # the TP-shard layer in full as well (I = 256: ~12 s on 8 threads)
+        tp = synth.CONFIGS["tpshard"]
+        tpi = synth.make_inputs(tp, lazy=True)
+        t = time.perf_counter()
+        omoe.layer(tpi.x, *tpi.weights, k=tp.k, n_shared=tp.n_shared, logits=tpi.logits, fmt=fmt)
+        dt4 = time.perf_counter() - t
     return {"value": cfg.T / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": f"the whole {cfg.name} layer (all {cfg.T} tokens, {cfg.k}+{cfg.n_shared} "
                       f"experts each, routing included), {dt:.1f} s on {cores} threads",
             "seconds": dt, "cpu_model": model, "affinity_cores": aff,
             "tiny": {"tokens_per_s": tiny.T / dt0, "seconds": dt0,
-                     "sample": f"the whole tiny layer (T={tiny.T}, router projection included)"}}
+                     "sample": f"the whole tiny layer (T={tiny.T}, router projection included)"},
+            "tpshard": {"tokens_per_s": tp.T / dt4, "seconds": dt4,
+                        "sample": f"the whole tpshard layer (all {tp.T} tokens)"}}
 
 
 def main():
