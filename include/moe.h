@@ -175,9 +175,10 @@ moe_status moe_route_topk_ex(const float* logits, int T, int E, int k, int n_sha
  * With a logits buffer and T < 1024 the call runs moe_router_logits and
  * moe_route_topk_ex instead (two kernels; faster for few tokens, where a
  * fused workgroup streams the whole router matrix for a handful of tokens).
- * Requires H % 128 == 0, 1 <= E <= 256, plus the requirements of
- * moe_route_topk_ex; E > 256 returns MOE_ERR_UNSUPPORTED (use
- * moe_router_logits + moe_route_topk_ex). */
+ * The fused workgroup holds 32 tokens' logits of all E experts in LDS
+ * (32 * (E rounded up to 64, plus 1) * 4 bytes: 131 KB at E = 1024).
+ * Requires H % 128 == 0 plus the requirements of moe_route_topk_ex
+ * (1 <= E <= MOE_MAX_EXPERTS). */
 moe_status moe_router_topk(const uint16_t* x, const uint16_t* w_router, int T, int H, int E, int k,
                            int n_shared, const moe_route_opts* opts, float* logits,
                            int32_t* topk_ids, float* topk_w, void* stream);

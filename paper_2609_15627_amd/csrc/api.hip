@@ -130,7 +130,6 @@ moe_status moe_router_topk(const uint16_t* x, const uint16_t* w_router, int T, i
   const moe_status st = check_route(T, E, k, n_shared, opts);
   if (st != MOE_OK) return st;
   if (H <= 0 || H % 128 != 0) return MOE_ERR_INVALID_ARG;
-  if (E > 256) return MOE_ERR_UNSUPPORTED;
   if (T > 0 && (!x || !w_router || !topk_ids || !topk_w)) return MOE_ERR_INVALID_ARG;
   // Few tokens: each fused workgroup streams the whole router matrix, which
   // takes longer than computing the logits with many waves and routing them

@@ -261,16 +261,19 @@ __global__ __launch_bounds__(256) void route_topk_ex_kernel(const float* __restr
 }
 
 // Fused router projection and routing (f1). A workgroup owns 32 tokens and
-// all E <= 256 experts: wave w computes logits of experts [64 w, 64 w + 64)
-// for the 32 tokens on the 32x32x16 bf16 matrix cores (products exact, fp32
-// accumulation), operands loaded straight to registers (row l % 32 and 8
-// consecutive K elements per lane, the same placement for both operands);
-// the 32 x E logits go to LDS, then each wave routes 8 of the tokens.
+// all E experts, in chunks of 256: wave w computes logits of experts
+// [c0 + 64 w, +64) of chunk c0 for the 32 tokens on the 32x32x16 bf16 matrix
+// cores (products exact, fp32 accumulation), operands loaded straight to
+// registers (row l % 32 and 8 consecutive K elements per lane, the same
+// placement for both operands); the 32 x E logits go to LDS (row stride
+// rt_stride(E), odd), then each wave routes 8 of the tokens.
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef float v16f_r __attribute__((ext_vector_type(16)));
 
-constexpr int kRtTok = 32;       // tokens per workgroup
-constexpr int kRtStride = 257;   // fp32 row stride of the LDS logits
+constexpr int kRtTok = 32;  // tokens per workgroup
+
+// fp32 row stride of the LDS logits: E rounded up to 64, plus one.
+__host__ __device__ inline int rt_stride(int E) { return (E + 63) / 64 * 64 + 1; }
 
 template <int EPL>
 __global__ __launch_bounds__(256) void router_topk_kernel(const uint16_t* __restrict__ x,
@@ -279,57 +282,64 @@ __global__ __launch_bounds__(256) void router_topk_kernel(const uint16_t* __rest
                                                           RouteOpts o, float* __restrict__ logits,
                                                           int32_t* __restrict__ ids,
                                                           float* __restrict__ wts) {
-  __shared__ float lg[kRtTok * kRtStride];
+  extern __shared__ float lg[];  // [kRtTok][stride]
+  const int stride = rt_stride(E);
   const int t0 = blockIdx.x * kRtTok;
   const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int r = lane & 31, h = lane >> 5;
+  const int ng = H / 128;  // groups of 128 K elements
+  if (ng * 128 != H) return;  // the launcher only passes H % 128 == 0
   // operand rows (clamped to valid rows; the extra results are never used)
   const uint16_t* xa = x + (size_t)min(t0 + r, T - 1) * H + 8 * h;
-  const uint16_t* wb0 = wr + (size_t)min(64 * w + r, E - 1) * H + 8 * h;
-  const uint16_t* wb1 = wr + (size_t)min(64 * w + 32 + r, E - 1) * H + 8 * h;
-  v16f_r acc0 = v16f_r{}, acc1 = v16f_r{};
-  constexpr int kU = 8;  // K steps of 16 per group (two groups of loads in flight)
-  v8bf a[2][kU], b0[2][kU], b1[2][kU];
-  auto load = [&](int buf, int k0) {
+  for (int c0 = 0; c0 < E; c0 += 256) {
+    const int e0 = c0 + 64 * w;  // this wave's first expert of the chunk
+    const uint16_t* wb0 = wr + (size_t)min(e0 + r, E - 1) * H + 8 * h;
+    const uint16_t* wb1 = wr + (size_t)min(e0 + 32 + r, E - 1) * H + 8 * h;
+    v16f_r acc0 = v16f_r{}, acc1 = v16f_r{};
+    constexpr int kU = 8;  // K steps of 16 per group (two groups of loads in flight)
+    v8bf a[2][kU], b0[2][kU], b1[2][kU];
+    auto load = [&](int buf, int k0) {
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int kk = k0 + 16 * u;
-      a[buf][u] = *reinterpret_cast<const v8bf*>(xa + kk);
-      b0[buf][u] = *reinterpret_cast<const v8bf*>(wb0 + kk);
-      b1[buf][u] = *reinterpret_cast<const v8bf*>(wb1 + kk);
+      for (int u = 0; u < kU; ++u) {
+        const int kk = k0 + 16 * u;
+        a[buf][u] = *reinterpret_cast<const v8bf*>(xa + kk);
+        b0[buf][u] = *reinterpret_cast<const v8bf*>(wb0 + kk);
+        b1[buf][u] = *reinterpret_cast<const v8bf*>(wb1 + kk);
+      }
+    };
+    auto mma = [&](int buf) {
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][u], b0[buf][u], acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][u], b1[buf][u], acc1, 0, 0, 0);
+      }
+    };
+    load(0, 0);
+    int g = 0;
+    for (; g + 2 <= ng; g += 2) {
+      if (g + 1 < ng) load(1, 16 * kU * (g + 1));
+      mma(0);
+      if (g + 2 < ng) load(0, 16 * kU * (g + 2));
+      mma(1);
     }
-  };
-  auto mma = [&](int buf) {
+    if (g < ng) mma(0);
+    // D: lane l, element i = token 8 (i / 4) + 4 h + i % 4, expert column l % 32
+    // (columns at or past E are padding: stored, never read)
+    if (e0 < E) {
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][u], b0[buf][u], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][u], b1[buf][u], acc1, 0, 0, 0);
+      for (int i = 0; i < 16; ++i) {
+        const int tr = 8 * (i / 4) + 4 * h + (i % 4);
+        lg[tr * stride + e0 + r] = acc0[i];
+        lg[tr * stride + e0 + 32 + r] = acc1[i];
+      }
     }
-  };
-  const int ng = H / (16 * kU);  // groups of 128 K elements
-  if (ng * 16 * kU != H) return;   // the launcher only passes H % 128 == 0
-  load(0, 0);
-  int g = 0;
-  for (; g + 2 <= ng; g += 2) {
-    if (g + 1 < ng) load(1, 16 * kU * (g + 1));
-    mma(0);
-    if (g + 2 < ng) load(0, 16 * kU * (g + 2));
-    mma(1);
-  }
-  if (g < ng) mma(0);
-  // D: lane l, element i = token 8 (i / 4) + 4 h + i % 4, expert column l % 32
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int tr = 8 * (i / 4) + 4 * h + (i % 4);
-    lg[tr * kRtStride + 64 * w + r] = acc0[i];
-    lg[tr * kRtStride + 64 * w + 32 + r] = acc1[i];
   }
   __syncthreads();
   const int kt = k + n_shared;
   for (int tt = w; tt < kRtTok; tt += 4) {
     const int t = t0 + tt;
     if (t >= T) break;
-    const float* row = lg + tt * kRtStride;
+    const float* row = lg + tt * stride;
     if (logits)
       for (int e = lane; e < E; e += kWave) logits[(size_t)t * E + e] = row[e];
     route_token<EPL>(row, E, k, n_shared, o, ids + (size_t)t * kt, wts + (size_t)t * kt, lane);
@@ -342,15 +352,20 @@ hipError_t launch_router_topk(const uint16_t* x, const uint16_t* wr, int T, int 
   if (T == 0) return hipSuccess;
   const int blocks = (T + kRtTok - 1) / kRtTok;
   const int epl = (E + kWave - 1) / kWave;
+  const size_t lds = (size_t)kRtTok * rt_stride(E) * sizeof(float);
 #define MOE_RT(N)                                                                               \
-  hipLaunchKernelGGL(router_topk_kernel<N>, dim3(blocks), dim3(256), 0, s, x, wr, T, H, E, k, \
+  hipLaunchKernelGGL(router_topk_kernel<N>, dim3(blocks), dim3(256), lds, s, x, wr, T, H, E, k, \
                      n_shared, o, logits, ids, w)
   if (epl <= 1)
     MOE_RT(1);
   else if (epl <= 2)
     MOE_RT(2);
-  else
+  else if (epl <= 4)
     MOE_RT(4);
+  else if (epl <= 8)
+    MOE_RT(8);
+  else
+    MOE_RT(16);
 #undef MOE_RT
   return hipGetLastError();
 }

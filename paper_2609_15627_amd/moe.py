@@ -153,7 +153,7 @@ def moe_route_topk(logits, k, n_shared=0, topk_ids=None, topk_w=None, stream=Non
 def moe_router_topk(x, w_router, k, n_shared=0, logits=None, topk_ids=None, topk_w=None,
                     stream=None, score="softmax", bias=None, n_group=1, topk_group=1,
                     renorm=True, scale=1.0, want_logits=False):
-    """Fused router projection + routing (E <= 256). Returns (ids, w) or, with
+    """Fused router projection + routing (any E <= 1024). Returns (ids, w) or, with
     ``want_logits``, (ids, w, logits)."""
     T, H = x.shape
     E = w_router.shape[0]

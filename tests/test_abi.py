@@ -141,8 +141,7 @@ def test_route_ex_and_router_reject(m):
     assert L.moe_route_topk_ex(NUL, 4, 8, 2, 0, ref(ok), FAKE, FAKE, NUL) == 1     # null logits
     assert L.moe_router_topk(FAKE, FAKE, 4, 100, 8, 2, 0, None, NUL, FAKE, FAKE, NUL) == 1  # H % 128
     assert L.moe_router_topk(FAKE, FAKE, 4, 128, 8, 9, 0, None, NUL, FAKE, FAKE, NUL) == 1  # k > E
-    assert L.moe_router_topk(FAKE, FAKE, 4, 128, 512, 8, 0, None, NUL, FAKE, FAKE, NUL) == \
-        m.MOE_ERR_UNSUPPORTED                                                            # E > 256
+    assert L.moe_router_topk(FAKE, FAKE, 4, 128, 1025, 8, 0, None, NUL, FAKE, FAKE, NUL) == 1  # E
     assert L.moe_router_topk(NUL, FAKE, 4, 128, 8, 2, 0, None, NUL, FAKE, FAKE, NUL) == 1   # null x
 
 

@@ -128,6 +128,9 @@ def _router_case(T, H, E, seed):
     (37, 256, 8, 2, 0, {}),                                        # ragged token block, E < 64
     (1500, 512, 64, 4, 0, dict(score="sigmoid")),                  # fused path, ragged last block
     (65, 512, 100, 7, 1, dict(renorm=False)),                      # E not a multiple of 64
+    (1024, 512, 300, 6, 0, {}),                                    # fused, two expert chunks
+    (1100, 256, 1024, 8, 1, dict(score="sigmoid", n_group=8, topk_group=4, bias=True)),
+    (2048, 1024, 384, 8, 1, {}),                                   # fused, E = 384
 ])
 def test_router_topk_fused(m, T, H, E, k, S, opts):
     xb, wb = _router_case(T, H, E, T + H + E)
@@ -166,8 +169,9 @@ def test_router_topk_fused(m, T, H, E, k, S, opts):
 
 def test_router_topk_rejects(m):
     x = torch.zeros((4, 64), dtype=torch.bfloat16, device="cuda")
-    with pytest.raises(m.MoeError):
-        m.moe_router_topk(x, torch.zeros((300, 64), dtype=torch.bfloat16, device="cuda"), 2)
+    with pytest.raises(m.MoeError):  # more experts than MOE_MAX_EXPERTS
+        m.moe_router_topk(torch.zeros((4, 128), dtype=torch.bfloat16, device="cuda"),
+                          torch.zeros((1025, 128), dtype=torch.bfloat16, device="cuda"), 2)
     with pytest.raises(m.MoeError):
         m.moe_router_topk(torch.zeros((4, 96), dtype=torch.bfloat16, device="cuda"),
                           torch.zeros((16, 96), dtype=torch.bfloat16, device="cuda"), 2)
