@@ -297,6 +297,30 @@ def host_cpu():
     return cores, aff, model
 
 
+def gpu_processes():
+    """Processes on the GPUs before this one starts (amd-smi process), so a
+    measurement taken beside another owner of the GPU shows it: the number
+    of listed processes, or None when amd-smi is missing or fails. Run
+    before this process touches the GPU."""
+    import shutil
+    import subprocess
+    exe = shutil.which("amd-smi")
+    if not exe:
+        return None
+    try:
+        r = subprocess.run([exe, "process", "--json"], capture_output=True, text=True, timeout=30)
+        data = json.loads(r.stdout)
+    except Exception:  # no JSON or no answer: unknown
+        return None
+    n = 0
+    for gpu in data if isinstance(data, list) else []:
+        for proc in gpu.get("process_list", []):
+            info = proc.get("process_info")
+            if isinstance(info, dict):  # a process (the empty list is a message string)
+                n += 1
+    return n
+
+
 def cpu_baseline(cfg, weights_np, fmt):
     """The fp64 oracle, as it is, on the whole layer of the workload (every
     token, routing included), on the whole tiny layer (router projection
@@ -365,6 +389,7 @@ def main():
               f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}).", file=sys.stderr)
         sys.exit(2)
 
+    foreign = gpu_processes()  # before this process touches the GPU
     import torch
 
     import synth
@@ -430,6 +455,7 @@ def main():
                            "unit": "GB/s", "frac": layer_gbs / HBM_PEAK_GBS,
                            "algorithmic_bytes": r["layer_bytes"]},
         "layer_hbm_frac": layer_gbs / HBM_PEAK_GBS,
+        "gpu_processes_before": foreign,
     }
     if cfg.name == "decode":
         log("measuring the tiny layer")
