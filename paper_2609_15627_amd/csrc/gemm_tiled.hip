@@ -300,7 +300,7 @@ __device__ __forceinline__ void t_sched_b() {
 //      group q - 1 used), interleaved with the remaining sub-step-1 products.
 // LAST marks the final group (k = nk - 4 + J), where the ring drains.
 #ifndef MOE_TILED_PRE
-#define MOE_TILED_PRE 2
+#define MOE_TILED_PRE 4
 #endif
 // Sub-step-1 products issued before the barrier (they cover its wait).
 constexpr int kPre = MOE_TILED_PRE;
