@@ -1,5 +1,5 @@
 // a5 / a6: grouped FP4 expert GEMMs, weight-streaming geometry with register
-// double buffering (one wave per workgroup).
+// double or triple buffering (one wave per workgroup).
 //
 // Work item: (row tile of up to 16 sorted rows of one expert, N tile). Every
 // workgroup streams its N tile of the expert's packed FP4 weights from HBM
@@ -208,6 +208,52 @@ __device__ __forceinline__ void stream_k(const uint8_t* a_row, const uint8_t* co
   }
 }
 
+// The same K loop with three register buffers, for a compile-time step
+// count NST: the codes of step c + 2 go out before the products of step c,
+// so two steps of loads are in flight while one is multiplied (the
+// products and their order are those of stream_k). A third buffer still
+// fits the two waves per SIMD the double-buffered loop runs at.
+template <int FA, int J, int NB, int NST, typename Pro>
+__device__ __forceinline__ void stream_k3(const uint8_t* a_row, const uint8_t* const* b_rows,
+                                          uint32_t xa, uint32_t wb, const uint32_t* wo, int g,
+                                          v4f* acc, Pro pro, bool av) {
+  constexpr int kc = 4 * J;
+  Frag<FA, J, NB> f[3];
+#pragma unroll
+  for (int q = 0; q < 3; ++q)
+#pragma unroll
+    for (int i = 0; i < Frag<FA, J, NB>::kAV; ++i) f[q].a[i] = v4u{0u, 0u, 0u, 0u};
+  frag_codes<FA, J, NB>(f[0], a_row, b_rows, 0, 0, g, av);
+  pro();
+  wait_all_vmem();
+  frag_codes<FA, J, NB>(f[1], a_row, b_rows, 0, kc, g, av);
+  static_for<NST>([&](auto C) {
+    constexpr int c = decltype(C)::value;
+    if constexpr (c + 2 < NST)
+      frag_codes<FA, J, NB>(f[(c + 2) % 3], a_row, b_rows, 0, (c + 2) * kc, g, av);
+    frag_scales<FA, J, NB>(f[c % 3], xa, wb, wo, c * kc, g);
+    frag_mma<FA, J, NB>(f[c % 3], acc);
+  });
+}
+
+// K loop of a streaming wave: triple-buffered for steps of 8 blocks and K of
+// 1024, 2048, 4096 or 8192 (nst = 4 .. 32), double-buffered otherwise.
+template <int FA, int J, int NB, bool EVEN, typename Pro>
+__device__ __forceinline__ void stream_any(const uint8_t* a_row, const uint8_t* const* b_rows,
+                                           int nst, uint32_t xa, uint32_t wb, const uint32_t* wo,
+                                           int g, v4f* acc, Pro pro, bool av) {
+  if constexpr (EVEN && J == 2) {
+    switch (nst) {
+      case 4: return stream_k3<FA, J, NB, 4>(a_row, b_rows, xa, wb, wo, g, acc, pro, av);
+      case 8: return stream_k3<FA, J, NB, 8>(a_row, b_rows, xa, wb, wo, g, acc, pro, av);
+      case 16: return stream_k3<FA, J, NB, 16>(a_row, b_rows, xa, wb, wo, g, acc, pro, av);
+      case 32: return stream_k3<FA, J, NB, 32>(a_row, b_rows, xa, wb, wo, g, acc, pro, av);
+      default: break;
+    }
+  }
+  stream_k<FA, J, NB, EVEN>(a_row, b_rows, nst, xa, wb, wo, g, acc, pro, av);
+}
+
 template <int FA, int J, int NBW, bool EVEN>
 __global__ __launch_bounds__(64) void s1_stream_kernel(S1Args p) {
   static_assert(NBW % 2 == 0, "a quantisation block spans two 16-column tiles");
@@ -242,7 +288,7 @@ __global__ __launch_bounds__(64) void s1_stream_kernel(S1Args p) {
   v4f acc[NB];
 #pragma unroll
   for (int n = 0; n < NB; ++n) acc[n] = v4f{0.f, 0.f, 0.f, 0.f};
-  stream_k<FA, J, NB, EVEN>(a_row, b_rows, kb / (4 * J), c16 * kb, 16 * kb, wo, g, acc, [&]() {
+  stream_any<FA, J, NB, EVEN>(a_row, b_rows, kb / (4 * J), c16 * kb, 16 * kb, wo, g, acc, [&]() {
     dma_gather16(
         lds,
         [&](int r) {
@@ -282,7 +328,7 @@ __global__ __launch_bounds__(64) void s2_stream_kernel(S2Args p) {
   v4f acc[NB];
 #pragma unroll
   for (int n = 0; n < NB; ++n) acc[n] = v4f{0.f, 0.f, 0.f, 0.f};
-  stream_k<FA, J, NB, EVEN>(a_row, b_rows, kb / (4 * J), c16 * kb, 16 * kb, wo, g, acc, [&]() {
+  stream_any<FA, J, NB, EVEN>(a_row, b_rows, kb / (4 * J), c16 * kb, 16 * kb, wo, g, acc, [&]() {
     dma_gather16(
         lds, [&](int r) { return p.hs + ((size_t)row0 + (r < nrows ? r : 0)) * kb; }, kb, lane);
     dma_rows16(lds + 16 * kb, p.w2s + rbase * kb, NB * 16 * kb, lane);

@@ -245,6 +245,9 @@ def small_case(T, H, I, E, k, S, seed, routing="normal"):
     (700, 768, 128, 5, 2, 1),     # streaming stage 1 (H = 768), short-K stage 2 with K = 128
     (170, 1024, 256, 3, 2, 0),    # short-K stage 2: tiles of 128 rows and ragged ones under 64
     (300, 2048, 512, 4, 2, 0),    # tiled stage 1 with K = 2048: middle groups of the K loop
+    (40, 2048, 2048, 8, 2, 1),    # streaming, K = 2048 in both stages (8 triple-buffered steps)
+    (16, 1024, 4096, 4, 2, 0),    # streaming stage 2 with K = 4096 (16 steps)
+    (24, 8192, 512, 8, 2, 0),     # streaming stage 1 with K = 8192 (32 steps)
 ])
 def test_small_layers(m, shape, fmt):
     cfg, inp = small_case(*shape, seed=sum(shape))
