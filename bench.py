@@ -304,11 +304,25 @@ def gpu_processes():
     before this process touches the GPU."""
     import shutil
     import subprocess
+    # Under a profiler its preloaded library starts the GPU in every child, so
+    # a child that replaces itself (a script's "#!/usr/bin/env python3") would
+    # exec after GPU start-up: skip the check there, and run a Python script
+    # through this interpreter rather than through its "#!" line.
+    if any(k.startswith("ROCPROF") for k in os.environ):
+        return None
     exe = shutil.which("amd-smi")
     if not exe:
         return None
+    cmd = [exe, "process", "--json"]
     try:
-        r = subprocess.run([exe, "process", "--json"], capture_output=True, text=True, timeout=30)
+        real = os.path.realpath(exe)
+        with open(real, "rb") as fh:
+            if fh.readline().startswith(b"#!") and real.endswith(".py"):
+                cmd = [sys.executable, real, "process", "--json"]
+    except OSError:
+        return None
+    try:
+        r = subprocess.run(cmd, capture_output=True, text=True, timeout=30)
         data = json.loads(r.stdout)
     except Exception:  # no JSON or no answer: unknown
         return None
