@@ -1,5 +1,6 @@
 // a5 / a6: grouped FP4 expert GEMMs, weight-streaming geometry with register
-// double or triple buffering (one wave per workgroup).
+// double or triple buffering (one wave per workgroup, or for stage 1 two
+// waves that split the K extent).
 //
 // Work item: (row tile of up to 16 sorted rows of one expert, N tile). Every
 // workgroup streams its N tile of the expert's packed FP4 weights from HBM
@@ -252,6 +253,100 @@ __device__ __forceinline__ void stream_any(const uint8_t* a_row, const uint8_t* 
     }
   }
   stream_k<FA, J, NB, EVEN>(a_row, b_rows, nst, xa, wb, wo, g, acc, pro, av);
+}
+
+// Steps s0 .. s0 + NST - 1 of the K loop (one wave's half of a two-wave
+// split), triple-buffered like stream_k3; sync() runs once this wave's
+// prologue DMA has landed, before any scale is read from LDS.
+template <int FA, int J, int NB, int NST, typename Pro, typename Sync>
+__device__ __forceinline__ void stream_k3h(const uint8_t* a_row, const uint8_t* const* b_rows,
+                                           uint32_t xa, uint32_t wb, const uint32_t* wo, int g,
+                                           v4f* acc, Pro pro, Sync sync, bool av, int s0) {
+  constexpr int kc = 4 * J;
+  Frag<FA, J, NB> f[3];
+#pragma unroll
+  for (int q = 0; q < 3; ++q)
+#pragma unroll
+    for (int i = 0; i < Frag<FA, J, NB>::kAV; ++i) f[q].a[i] = v4u{0u, 0u, 0u, 0u};
+  frag_codes<FA, J, NB>(f[0], a_row, b_rows, 0, s0 * kc, g, av);
+  pro();
+  wait_all_vmem();
+  sync();
+  if constexpr (NST > 1) frag_codes<FA, J, NB>(f[1], a_row, b_rows, 0, (s0 + 1) * kc, g, av);
+  static_for<NST>([&](auto C) {
+    constexpr int c = decltype(C)::value;
+    if constexpr (c + 2 < NST)
+      frag_codes<FA, J, NB>(f[(c + 2) % 3], a_row, b_rows, 0, (s0 + c + 2) * kc, g, av);
+    frag_scales<FA, J, NB>(f[c % 3], xa, wb, wo, (s0 + c) * kc, g);
+    frag_mma<FA, J, NB>(f[c % 3], acc);
+  });
+}
+
+// Stage 1 with the K extent split over the two waves of a workgroup (steps
+// of 8 blocks, NSTH per wave). A streaming launch ends with a last, partly
+// filled round of workgroups, whose rate is bound by each wave's own loads
+// in flight rather than by HBM; halving a wave's share of K halves that
+// tail (measured on the decode layer: stage 1 ~3% faster). Wave 0 stages
+// the activation and gate scale rows, wave 1 the up scale rows; wave 1
+// hands its fp32 sums over through LDS and wave 0 forms first half + second
+// half (a fixed order, so results repeat bit for bit) before the SwiGLU
+// epilogue.
+template <int FA, int NBW, int NSTH>
+__global__ __launch_bounds__(128) void s1_stream2_kernel(S1Args p) {
+  constexpr int NB = 2 * NBW, J = 2;
+  constexpr int kAB = ActBytes<FA>::kBlock;
+  int4 tile;
+  int nt;
+  if (!tile_of_block(p.t, &tile, &nt)) return;
+  const int e = tile.x, row0 = tile.y, nrows = tile.z;
+  const int kw = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));  // K half of the wave
+  const int lane = threadIdx.x & 63, g = lane >> 4, c16 = lane & 15;
+  const int kb = p.H / 32;
+  const int hc0 = nt * (NBW * 16);  // first h column of the workgroup
+  const size_t ebase = (size_t)e * 2 * p.I;
+
+  // LDS: the scale rows as in s1_stream_kernel, then wave 1's sums [NB][64] v4f
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int half = NBW * 16 * kb;
+  const int tok = p.sorted[row0 + (c16 < nrows ? c16 : 0)] / p.k_total;
+  const uint8_t* a_row = p.xq + (size_t)tok * (p.H / 32) * kAB;
+  const uint8_t* b_rows[NB];
+  uint32_t wo[NB];
+#pragma unroll
+  for (int b = 0; b < NBW; ++b) {
+    const size_t gr = ebase + hc0 + 16 * b + c16;  // gate row
+    b_rows[b] = p.w13 + gr * (p.H / 2);
+    b_rows[NBW + b] = p.w13 + (gr + p.I) * (p.H / 2);
+    wo[b] = (16 * b + c16) * kb;
+    wo[NBW + b] = (NBW * 16 + 16 * b + c16) * kb;
+  }
+  v4f acc[NB];
+#pragma unroll
+  for (int n = 0; n < NB; ++n) acc[n] = v4f{0.f, 0.f, 0.f, 0.f};
+  stream_k3h<FA, J, NB, NSTH>(a_row, b_rows, c16 * kb, 16 * kb, wo, g, acc, [&]() {
+    if (kw == 0) {
+      dma_gather16(
+          lds,
+          [&](int r) {
+            const int t = p.sorted[row0 + (r < nrows ? r : 0)] / p.k_total;
+            return p.xs + (size_t)t * kb;
+          },
+          kb, lane);
+      dma_rows16(lds + 16 * kb, p.w13s + (ebase + hc0) * kb, half, lane);
+    } else {
+      dma_rows16(lds + 16 * kb + half, p.w13s + (ebase + p.I + hc0) * kb, half, lane);
+    }
+  }, [&]() { __syncthreads(); }, c16 < nrows, kw * NSTH);
+  v4f* red = reinterpret_cast<v4f*>(lds + (1 + 2 * NBW) * 16 * kb);
+  if (kw == 1) {
+#pragma unroll
+    for (int n = 0; n < NB; ++n) red[n * 64 + lane] = acc[n];
+  }
+  __syncthreads();
+  if (kw == 1) return;
+#pragma unroll
+  for (int n = 0; n < NB; ++n) acc[n] = acc[n] + red[n * 64 + lane];
+  s1_epilogue<FA, NBW>(acc, p, row0, nrows, hc0, g, c16);
 }
 
 template <int FA, int J, int NBW, bool EVEN>
@@ -589,6 +684,21 @@ static void launch_stream(int kb, K2 k2, K1 k1, K0 k0, long mt, int ntl, const P
 template <int FA, int NBW1>
 static void launch_s1(const S1Args& p, long mt, hipStream_t s) {
   const int kb = p.H / 32;
+  // K = 1024 .. 8192: the two-wave split (4 .. 32 steps of 8 blocks)
+  if (kb == 32 || kb == 64 || kb == 128 || kb == 256) {
+    S1Args q = p;
+    const int ntl = p.I / (NBW1 * 16);
+    q.t.n_ntiles = ntl;
+    q.t.ngroup = n_group_of(ntl);
+    const long n = mt * ntl;
+    const dim3 grid((int)((n + 7) / 8 * 8)), block(128);
+    const size_t lds = (size_t)(1 + 2 * NBW1) * 16 * kb + (size_t)2 * NBW1 * 64 * 16;
+    if (kb == 32) hipLaunchKernelGGL((s1_stream2_kernel<FA, NBW1, 2>), grid, block, lds, s, q);
+    else if (kb == 64) hipLaunchKernelGGL((s1_stream2_kernel<FA, NBW1, 4>), grid, block, lds, s, q);
+    else if (kb == 128) hipLaunchKernelGGL((s1_stream2_kernel<FA, NBW1, 8>), grid, block, lds, s, q);
+    else hipLaunchKernelGGL((s1_stream2_kernel<FA, NBW1, 16>), grid, block, lds, s, q);
+    return;
+  }
   launch_stream(kb, s1_stream_kernel<FA, 2, NBW1, true>, s1_stream_kernel<FA, 1, NBW1, true>,
                 s1_stream_kernel<FA, 1, NBW1, false>, mt, p.I / (NBW1 * 16), p, s,
                 (size_t)(1 + 2 * NBW1) * 16 * kb);
@@ -602,9 +712,9 @@ static void launch_s2(const S2Args& p, long mt, hipStream_t s) {
                 (size_t)(1 + NBW2) * 16 * kb);
 }
 
-// One wave per workgroup, steps of 256 K elements (128 when K/32 is not a
-// multiple of 16), 32 h columns per wave in stage 1 and 64 output columns
-// per wave in stage 2.
+// Steps of 256 K elements (128 when K/32 is not a multiple of 16); stage 1:
+// 32 h columns per workgroup, two waves splitting K for K = 1024 .. 8192,
+// else one wave; stage 2: one wave per workgroup, 64 output columns.
 void launch_s1_stream(const S1Args& p, long mt, int fa, hipStream_t s) {
   if (fa == 0) launch_s1<0, 2>(p, mt, s);
   else if (fa == 2) launch_s1<2, 2>(p, mt, s);
