@@ -336,9 +336,10 @@ moe_status moe_fp4_grouped_gemm_noalloc(const uint16_t* x, int T, int H, int I,
  * Available when moe_fp4_grouped_gemm_combine_supported() returns 1: the
  * weight-streaming geometry is chosen (few rows per expert) and the fp32
  * results of all T * k_total rows for 16 output columns fit one workgroup's
- * LDS (T * k_total * 64 + 32 * I bytes; T * k_total up to 1536 at
- * I = 2048). Otherwise (or without a device) MOE_ERR_UNSUPPORTED, and nothing
- * is enqueued: use the two calls. */
+ * LDS (n * T * k_total * 64 + 32 * I bytes, n = 2 where the down projection
+ * splits K over two waves -- I = 1024, 2048, 4096 or 8192 -- else 1;
+ * T * k_total up to 768 at I = 2048). Otherwise (or without a device)
+ * MOE_ERR_UNSUPPORTED, and nothing is enqueued: use the two calls. */
 int moe_fp4_grouped_gemm_combine_supported(int T, int H, int I, int n_experts_total, int k_total,
                                            moe_act_format f);
 moe_status moe_fp4_grouped_gemm_combine(const uint16_t* x, int T, int H, int I,

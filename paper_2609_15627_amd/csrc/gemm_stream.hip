@@ -431,13 +431,71 @@ __global__ __launch_bounds__(64) void s2_stream_kernel(S2Args p) {
   s2_epilogue<NBW>(acc, p, row0, nrows, nc0, g, c16);
 }
 
+// Stage 2 with the K extent split over two waves, as s1_stream2_kernel
+// (wave 0 stages the activation scale rows, wave 1 the weight scale rows;
+// partial = first half + second half).
+template <int FA, int NBW, int NSTH>
+__global__ __launch_bounds__(128) void s2_stream2_kernel(S2Args p) {
+  constexpr int NB = NBW, J = 2;
+  constexpr int kAB = ActBytes<FA>::kBlock;
+  int4 tile;
+  int nt;
+  if (!tile_of_block(p.t, &tile, &nt)) return;
+  const int e = tile.x, row0 = tile.y, nrows = tile.z;
+  const int kw = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));  // K half of the wave
+  const int lane = threadIdx.x & 63, g = lane >> 4, c16 = lane & 15;
+  const int kb = p.I / 32;
+  const int nc0 = nt * (NBW * 16);  // first output column of the workgroup
+  const size_t rbase = (size_t)e * p.H + nc0;
+
+  // LDS: the scale rows as in s2_stream_kernel, then wave 1's sums [NB][64] v4f
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const size_t ar = (size_t)row0 + (c16 < nrows ? c16 : 0);
+  const uint8_t* a_row = p.hq + ar * (p.I / 32) * kAB;
+  const uint8_t* b_rows[NB];
+  uint32_t wo[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    b_rows[b] = p.w2 + (rbase + 16 * b + c16) * (p.I / 2);
+    wo[b] = (16 * b + c16) * kb;
+  }
+  v4f acc[NB];
+#pragma unroll
+  for (int n = 0; n < NB; ++n) acc[n] = v4f{0.f, 0.f, 0.f, 0.f};
+  stream_k3h<FA, J, NB, NSTH>(a_row, b_rows, c16 * kb, 16 * kb, wo, g, acc, [&]() {
+    if (kw == 0)
+      dma_gather16(
+          lds, [&](int r) { return p.hs + ((size_t)row0 + (r < nrows ? r : 0)) * kb; }, kb, lane);
+    else
+      dma_rows16(lds + 16 * kb, p.w2s + rbase * kb, NB * 16 * kb, lane);
+  }, [&]() { __syncthreads(); }, c16 < nrows, kw * NSTH);
+  v4f* red = reinterpret_cast<v4f*>(lds + (1 + NBW) * 16 * kb);
+  if (kw == 1) {
+#pragma unroll
+    for (int n = 0; n < NB; ++n) red[n * 64 + lane] = acc[n];
+  }
+  __syncthreads();
+  if (kw == 1) return;
+#pragma unroll
+  for (int n = 0; n < NB; ++n) acc[n] = acc[n] + red[n * 64 + lane];
+  s2_epilogue<NBW>(acc, p, row0, nrows, nc0, g, c16);
+}
+
+// The streaming stages split K over two waves for K/32 = 32, 64, 128 or 256
+// (4 .. 32 steps of 8 blocks); the fused down + combine kernel follows the
+// same rule so that both paths add the same two halves.
+inline bool split_k(int kb) { return kb == 32 || kb == 64 || kb == 128 || kb == 256; }
+
 // Stage 2 fused with the fixed-order combine, for few rows (decode): the
 // paper's small down consumer joined to the reducer (Historical down-consumer
 // pilot; Current TP8 native-AR results). A workgroup owns 16 output columns
 // and every row: its waves take the row tiles round-robin, stream those 16
 // W2 rows of the tile's expert once over the whole K extent with the same
-// products in the same order as s2_stream_kernel (so the same fp32 values),
-// and put each row's result into LDS at the row's assignment index. After
+// products in the same order as the unfused stage 2 (so the same fp32
+// values; where that splits K over two waves, so do these: waves 2i and
+// 2i + 1 take the same tiles, one K half each, and the halves are added in
+// the same order), and put each row's result into LDS at the row's
+// assignment index. After
 // one barrier the workgroup forms out[t, columns] = bf16(acc), acc =
 // fmaf(topk_w[t, j], P[t*k_total + j], acc) for j = 0, 1, ... -- the combine
 // kernel's arithmetic -- so the output has the bits of s2_stream_kernel +
@@ -453,8 +511,8 @@ __global__ __launch_bounds__(64) void s2_stream_kernel(S2Args p) {
 // explicit wait at each tile's first step covers it (see s2c_tiles).
 //
 // LDS: P [A][16] fp32 (zeroed first, so an assignment whose expert id was
-// invalid contributes 0), then two slots per wave of 16 activation and 16
-// weight scale rows.
+// invalid contributes 0; with the K split, one such array per K half), then
+// two slots per wave of 16 activation and 16 weight scale rows.
 #ifndef MOE_FUSED_WAVES
 #define MOE_FUSED_WAVES 16
 #endif
@@ -503,7 +561,7 @@ __device__ __forceinline__ void s2c_scales(uint8_t* lds, uint32_t slot, const S2
 // step-1 loads are kStepLoads unconditional instructions issued after it,
 // so the DMA is complete when at most kStepLoads loads are outstanding
 // (loads complete in order).
-template <int FA, int J>
+template <int FA, int J, bool SPLIT>
 __device__ __forceinline__ void s2c_tiles(const S2CArgs& c, uint8_t* lds, float* P, int wave,
                                           int lane, int nc0) {
   const S2Args& p = c.s;
@@ -515,10 +573,14 @@ __device__ __forceinline__ void s2c_tiles(const S2CArgs& c, uint8_t* lds, float*
   const int kb = p.I / 32, nst = kb / kc;
   wave = __builtin_amdgcn_readfirstlane(wave);
   const int ntl = *p.t.ntiles;
-  const int W = kFusedWaves;
-  int tj = wave;
+  // with the K split: wave pairs take the tiles, wave 2i + h steps K half h
+  const int W = SPLIT ? kFusedWaves / 2 : kFusedWaves;
+  const int kh = SPLIT ? (wave & 1) : 0;
+  const int ns = SPLIT ? nst / 2 : nst, s0 = kh * ns;  // this wave's steps s0 .. s0 + ns - 1
+  float* const Pw = P + (size_t)kh * c.T * c.k_total * 16;
+  int tj = SPLIT ? wave >> 1 : wave;
   if (tj >= ntl) return;
-  const uint32_t slot0 = (uint32_t)(c.T * c.k_total * 64 + wave * 64 * kb);
+  const uint32_t slot0 = (uint32_t)((SPLIT ? 2 : 1) * c.T * c.k_total * 64 + wave * 64 * kb);
   const uint32_t wo[1] = {(uint32_t)(c16 * kb)};
   auto a_row = [&](const S2CTile& t) {
     return p.hq + ((size_t)t.row0 + (c16 < t.nrows ? c16 : 0)) * (p.I / 32) * kAB;
@@ -531,7 +593,7 @@ __device__ __forceinline__ void s2c_tiles(const S2CArgs& c, uint8_t* lds, float*
   F fa, fb;
   {
     const uint8_t* br = b_row(tc);
-    frag_codes<FA, J, 1>(fa, a_row(tc), &br, 0, 0, g);
+    frag_codes<FA, J, 1>(fa, a_row(tc), &br, 0, s0 * kc, g);
   }
   s2c_scales(lds, slot, p, tc, kb, lane);
   wait_all_vmem();
@@ -548,34 +610,34 @@ __device__ __forceinline__ void s2c_tiles(const S2CArgs& c, uint8_t* lds, float*
     }
     const uint8_t* ar = a_row(tc);
     const uint8_t* br = b_row(tc);
-    // codes of the step after s + 1: step s + 2 of this tile, else step 0 of
-    // the next tile (of this tile again when there is none: every step issues
-    // the same loads, so the compiler's waits count exactly)
+    // codes of the step after s + 1: step s + 2 of this tile, else the first
+    // step (s0) of the next tile (of this tile again when there is none:
+    // every step issues the same loads, so the compiler's waits count exactly)
     const uint8_t* arn = has_next ? a_row(tn) : ar;
     const uint8_t* brn = has_next ? b_row(tn) : br;
     const uint32_t xa = slot + c16 * kb, wb = slot + 16 * kb;
     const uint32_t nslot = slot ^ (slot0 ^ (slot0 + 32 * kb));
     v4f acc[1] = {v4f{0.f, 0.f, 0.f, 0.f}};
-    auto pair = [&](int s, bool first) {
-      frag_codes<FA, J, 1>(fb, ar, &br, 0, (s + 1) * kc, g);
+    auto pair = [&](int s, bool first) {  // steps s0 + s, s0 + s + 1
+      frag_codes<FA, J, 1>(fb, ar, &br, 0, (s0 + s + 1) * kc, g);
       if (first) {
         tvmcnt_s<kStepLoads>();
         if (has_next) s2c_scales(lds, nslot, p, tn, kb, lane);
       }
-      frag_scales<FA, J, 1>(fa, xa, wb, wo, s * kc, g);
+      frag_scales<FA, J, 1>(fa, xa, wb, wo, (s0 + s) * kc, g);
       frag_mma<FA, J, 1>(fa, acc);
-      const bool last = s + 2 >= nst;
+      const bool last = s + 2 >= ns;
       const uint8_t* a2 = last ? arn : ar;
       const uint8_t* b2 = last ? brn : br;
-      frag_codes<FA, J, 1>(fa, a2, &b2, 0, last ? 0 : (s + 2) * kc, g);
-      frag_scales<FA, J, 1>(fb, xa, wb, wo, (s + 1) * kc, g);
+      frag_codes<FA, J, 1>(fa, a2, &b2, 0, (last ? s0 : s0 + s + 2) * kc, g);
+      frag_scales<FA, J, 1>(fb, xa, wb, wo, (s0 + s + 1) * kc, g);
       frag_mma<FA, J, 1>(fb, acc);
     };
     pair(0, true);
-    for (int s = 2; s < nst; s += 2) pair(s, false);
+    for (int s = 2; s < ns; s += 2) pair(s, false);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      if (arow[i] >= 0) P[arow[i] * 16 + c16] = acc[0][i];
+      if (arow[i] >= 0) Pw[arow[i] * 16 + c16] = acc[0][i];
     if (!has_next) break;
     tj += W;
     tc = tn;
@@ -584,7 +646,7 @@ __device__ __forceinline__ void s2c_tiles(const S2CArgs& c, uint8_t* lds, float*
   }
 }
 
-template <int FA, int J, bool EVEN>
+template <int FA, int J, bool EVEN, bool SPLIT>
 __global__ __launch_bounds__(64 * kFusedWaves) void s2c_stream_kernel(S2CArgs c) {
   const S2Args& p = c.s;
   constexpr int kAB = ActBytes<FA>::kBlock;
@@ -595,12 +657,13 @@ __global__ __launch_bounds__(64 * kFusedWaves) void s2c_stream_kernel(S2CArgs c)
   const int A = c.T * kt;
   const int nc0 = blockIdx.x * 16;  // first output column of the workgroup
 
-  for (int i = threadIdx.x; i < A * 4; i += blockDim.x)
+  constexpr int kNP = SPLIT ? 2 : 1;  // result arrays (one per K half)
+  for (int i = threadIdx.x; i < kNP * A * 4; i += blockDim.x)
     reinterpret_cast<v4f*>(P)[i] = v4f{0.f, 0.f, 0.f, 0.f};
   __syncthreads();
 
   if constexpr (EVEN) {
-    s2c_tiles<FA, J>(c, lds, P, wave, lane, nc0);
+    s2c_tiles<FA, J, SPLIT>(c, lds, P, wave, lane, nc0);
   } else {  // odd step counts: one tile at a time
     const uint32_t sb = (uint32_t)(A * 64 + wave * 64 * kb);  // this wave's scale rows
     const int ntl = *p.t.ntiles;
@@ -636,11 +699,14 @@ __global__ __launch_bounds__(64 * kFusedWaves) void s2c_stream_kernel(S2CArgs c)
     const int t = o >> 3, cp = 2 * (o & 7);
     const float* wrow = c.topk_w + (size_t)t * kt;
     const float* prow = P + (size_t)t * kt * 16 + cp;
+    const float* qrow = prow + (size_t)A * 16;  // second K half (with the split)
     float a0 = 0.f, a1 = 0.f;
     for (int j = 0; j < kt; ++j) {
       const float wj = wrow[j];
-      a0 = fmaf(wj, prow[16 * j], a0);
-      a1 = fmaf(wj, prow[16 * j + 1], a1);
+      const float p0 = SPLIT ? prow[16 * j] + qrow[16 * j] : prow[16 * j];
+      const float p1 = SPLIT ? prow[16 * j + 1] + qrow[16 * j + 1] : prow[16 * j + 1];
+      a0 = fmaf(wj, p0, a0);
+      a1 = fmaf(wj, p1, a1);
     }
     *reinterpret_cast<uint32_t*>(c.out + (size_t)t * p.H + nc0 + cp) =
         f32_to_bf16_rne(a0) | (f32_to_bf16_rne(a1) << 16);
@@ -648,7 +714,9 @@ __global__ __launch_bounds__(64 * kFusedWaves) void s2c_stream_kernel(S2CArgs c)
 }
 
 size_t fused_lds_bytes(int T, int k_total, int I) {
-  return (size_t)T * k_total * 64 + (size_t)kFusedWaves * 64 * (I / 32);
+  const int kb = I / 32;
+  const size_t np = kb % 16 == 0 && split_k(kb) ? 2 : 1;
+  return np * T * k_total * 64 + (size_t)kFusedWaves * 64 * kb;
 }
 
 template <int FA>
@@ -656,9 +724,13 @@ static void launch_s2c(const S2CArgs& p, hipStream_t s) {
   const int kb = p.s.I / 32;
   const size_t lds = fused_lds_bytes(p.T, p.k_total, p.s.I);
   const dim3 grid(p.s.H / 16), block(64 * kFusedWaves);
-  if (kb % 16 == 0) hipLaunchKernelGGL((s2c_stream_kernel<FA, 2, true>), grid, block, lds, s, p);
-  else if (kb % 8 == 0) hipLaunchKernelGGL((s2c_stream_kernel<FA, 1, true>), grid, block, lds, s, p);
-  else hipLaunchKernelGGL((s2c_stream_kernel<FA, 1, false>), grid, block, lds, s, p);
+  if (kb % 16 == 0 && split_k(kb))
+    hipLaunchKernelGGL((s2c_stream_kernel<FA, 2, true, true>), grid, block, lds, s, p);
+  else if (kb % 16 == 0)
+    hipLaunchKernelGGL((s2c_stream_kernel<FA, 2, true, false>), grid, block, lds, s, p);
+  else if (kb % 8 == 0)
+    hipLaunchKernelGGL((s2c_stream_kernel<FA, 1, true, false>), grid, block, lds, s, p);
+  else hipLaunchKernelGGL((s2c_stream_kernel<FA, 1, false, false>), grid, block, lds, s, p);
 }
 
 void launch_s2c_stream(const S2CArgs& p, int fa, hipStream_t s) {
@@ -684,8 +756,7 @@ static void launch_stream(int kb, K2 k2, K1 k1, K0 k0, long mt, int ntl, const P
 template <int FA, int NBW1>
 static void launch_s1(const S1Args& p, long mt, hipStream_t s) {
   const int kb = p.H / 32;
-  // K = 1024 .. 8192: the two-wave split (4 .. 32 steps of 8 blocks)
-  if (kb == 32 || kb == 64 || kb == 128 || kb == 256) {
+  if (split_k(kb)) {  // K = 1024 .. 8192: the two-wave split
     S1Args q = p;
     const int ntl = p.I / (NBW1 * 16);
     q.t.n_ntiles = ntl;
@@ -707,6 +778,20 @@ static void launch_s1(const S1Args& p, long mt, hipStream_t s) {
 template <int FA, int NBW2>
 static void launch_s2(const S2Args& p, long mt, hipStream_t s) {
   const int kb = p.I / 32;
+  if (split_k(kb)) {
+    S2Args q = p;
+    const int ntl = p.H / (NBW2 * 16);
+    q.t.n_ntiles = ntl;
+    q.t.ngroup = n_group_of(ntl);
+    const long n = mt * ntl;
+    const dim3 grid((int)((n + 7) / 8 * 8)), block(128);
+    const size_t lds = (size_t)(1 + NBW2) * 16 * kb + (size_t)NBW2 * 64 * 16;
+    if (kb == 32) hipLaunchKernelGGL((s2_stream2_kernel<FA, NBW2, 2>), grid, block, lds, s, q);
+    else if (kb == 64) hipLaunchKernelGGL((s2_stream2_kernel<FA, NBW2, 4>), grid, block, lds, s, q);
+    else if (kb == 128) hipLaunchKernelGGL((s2_stream2_kernel<FA, NBW2, 8>), grid, block, lds, s, q);
+    else hipLaunchKernelGGL((s2_stream2_kernel<FA, NBW2, 16>), grid, block, lds, s, q);
+    return;
+  }
   launch_stream(kb, s2_stream_kernel<FA, 2, NBW2, true>, s2_stream_kernel<FA, 1, NBW2, true>,
                 s2_stream_kernel<FA, 1, NBW2, false>, mt, p.H / (NBW2 * 16), p, s,
                 (size_t)(1 + NBW2) * 16 * kb);

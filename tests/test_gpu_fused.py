@@ -58,16 +58,16 @@ def test_fused_matches_unfused_and_oracle(m, shape, fmt):
 
 def test_fused_row_limit(m):
     """The largest batch whose rows fit the workgroup's LDS, I = 2048: every
-    row's result for 16 columns (64 bytes a row) plus two slots of scale rows
-    for each of 16 waves (64 KiB), within 160 KiB."""
-    cfg = synth.LayerConfig("fused_max", 170, 512, 256, 8, 2048, 1, "normal", 11)
-    assert cfg.A == 1530
+    row's result for 16 columns per K half (2 x 64 bytes a row) plus two
+    slots of scale rows for each of 16 waves (64 KiB), within 160 KiB."""
+    cfg = synth.LayerConfig("fused_max", 85, 512, 256, 8, 2048, 1, "normal", 11)
+    assert cfg.A == 765
     inp = synth.make_inputs(cfg)
     log(f"fused row limit A={cfg.A}")
     lf, of, lu, ou = both_paths(m, cfg, inp)
     assert np.array_equal(gc.bf16_bits(of), gc.bf16_bits(ou))
     check_against_oracle(cfg, inp, lf, of, np.arange(0, cfg.T, 7))
-    assert not m.moe_fp4_grouped_gemm_combine_supported(171, 512, 2048, 257, 9, "e4m3")
+    assert not m.moe_fp4_grouped_gemm_combine_supported(86, 512, 2048, 257, 9, "e4m3")
 
 
 def test_fused_decode_full_size(m):
