@@ -274,10 +274,14 @@ __global__ __launch_bounds__(64 * kWaves) void bf16_gemm_kernel(BfArgs p) {
 
 // ---------------------------------------------------------------------------
 // Weight-streaming geometry of the BF16 contract, for few rows per expert
-// (decode): one wave per workgroup takes a tile of up to 16 sorted rows and
-// NBW blocks of 16 weight rows (stage 1: NBW gate blocks and the matching up
-// blocks), so every weight byte is read once, straight into registers, and
-// expanded there. 16x16x32 bf16 products with the weights as the row
+// (decode): a workgroup takes a tile of up to 16 sorted rows and NBW blocks
+// of 16 weight rows (stage 1: NBW gate blocks and the matching up blocks),
+// so every weight byte is read once, straight into registers, and expanded
+// there. With KW = 2 its two waves each stream half of the K steps and wave
+// 0 adds wave 1's fp32 sums (first half + second half, through LDS) before
+// the epilogue: the last, partly filled round of a streaming launch is
+// bound by each wave's own loads in flight, and half the K extent per wave
+// halves it. 16x16x32 bf16 products with the weights as the row
 // operand: lane l supplies weight row l % 16 and activation row l % 16, and
 // its accumulator holds weight rows 4 (l / 16) .. +3 of activation row l % 16.
 // K order: in each K step of 128, lane group g = l / 16 takes the physical
@@ -295,16 +299,18 @@ struct BfStep {
   v4u b[NB];  // 32 FP4 codes of each weight row, same K
 };
 
-template <int ST, int NBW>
-__global__ __launch_bounds__(64) void bf16_stream_kernel(BfArgs p) {
+template <int ST, int NBW, int KW>
+__global__ __launch_bounds__(64 * KW) void bf16_stream_kernel(BfArgs p) {
   constexpr int NB = ST == 1 ? 2 * NBW : NBW;
   int4 tile;
   int nt;
   if (!tile_of_block(p.t, &tile, &nt)) return;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int e = tile.x, row0 = tile.y, nrows = tile.z;
-  const int lane = threadIdx.x, g = lane >> 4, c16 = lane & 15;
+  const int kw = KW == 2 ? __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) : 0;
+  const int lane = threadIdx.x & 63, g = lane >> 4, c16 = lane & 15;
   const int kb = p.K / 32, nst = p.K / 128;
+  const int s_lo = kw * (nst / KW), s_hi = s_lo + nst / KW;  // this wave's K steps
   const int c0 = nt * NBW * 16;  // first h column (stage 1) or output column (stage 2)
 
   // this lane's activation row (rows past the tile's end read its first
@@ -335,10 +341,10 @@ __global__ __launch_bounds__(64) void bf16_stream_kernel(BfArgs p) {
   // they would have only a few instructions of lead)
   // running lane offsets of the next step to load (advanced in place, so
   // no address register is also a load target)
-  uint32_t ao = aoff;
+  uint32_t ao = aoff + 256 * (uint32_t)s_lo;
   uint32_t bo[NB];
 #pragma unroll
-  for (int n = 0; n < NB; ++n) bo[n] = boff[n];
+  for (int n = 0; n < NB; ++n) bo[n] = boff[n] + 64 * (uint32_t)s_lo;
   auto load = [&](BfStep<NB>& f) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -354,14 +360,20 @@ __global__ __launch_bounds__(64) void bf16_stream_kernel(BfArgs p) {
   load(f0);
   // weight scale rows of the tile: [NB * 16 rows][kb bytes] (stage 1: the gate
   // rows, then the up rows)
+  // (with KW = 2: wave 0 the first half of them, wave 1 the second)
   const uint8_t* sbase = p.ws + (size_t)e * p.N * kb;
   if constexpr (ST == 1) {
-    dma_rows16(lds, sbase + (size_t)wrow(0) * kb, NBW * 16 * kb, lane);
-    dma_rows16(lds + NBW * 16 * kb, sbase + (size_t)wrow(NBW) * kb, NBW * 16 * kb, lane);
-  } else {
+    if (KW == 1 || kw == 0) dma_rows16(lds, sbase + (size_t)wrow(0) * kb, NBW * 16 * kb, lane);
+    if (KW == 1 || kw == 1)
+      dma_rows16(lds + NBW * 16 * kb, sbase + (size_t)wrow(NBW) * kb, NBW * 16 * kb, lane);
+  } else if constexpr (KW == 1) {
     dma_rows16(lds, sbase + (size_t)wrow(0) * kb, NB * 16 * kb, lane);
+  } else {
+    const int hb = NB * 8 * kb;  // bytes of half the rows
+    dma_rows16(lds + kw * hb, sbase + (size_t)wrow(0) * kb + kw * hb, hb, lane);
   }
   wait_all_vmem();
+  if constexpr (KW == 2) __syncthreads();  // the other wave's scale rows landed
 
   v4f acc[NB];
 #pragma unroll
@@ -380,19 +392,30 @@ __global__ __launch_bounds__(64) void bf16_stream_kernel(BfArgs p) {
     }
   };
   // f0 holds step s on entry; steps s + 1 and s + 2 exist inside the loop
-  int s = 0;
-  for (; s + 2 < nst; s += 2) {
+  int s = s_lo;
+  for (; s + 2 < s_hi; s += 2) {
     load(f1);
     mma(f0, s);
     load(f0);
     mma(f1, s + 1);
   }
-  if (s + 1 < nst) {
+  if (s + 1 < s_hi) {
     load(f1);
     mma(f0, s);
     mma(f1, s + 1);
   } else {
     mma(f0, s);
+  }
+  if constexpr (KW == 2) {  // first half + second half, in wave 0
+    v4f* red = reinterpret_cast<v4f*>(lds + NB * 16 * kb);
+    if (kw == 1) {
+#pragma unroll
+      for (int n = 0; n < NB; ++n) red[n * 64 + lane] = acc[n];
+    }
+    __syncthreads();
+    if (kw == 1) return;
+#pragma unroll
+    for (int n = 0; n < NB; ++n) acc[n] = acc[n] + red[n * 64 + lane];
   }
 
   if (c16 >= nrows) return;
@@ -445,14 +468,23 @@ constexpr int kBfS1 = 2, kBfS2 = 4;
 
 int bf16_stream_rows() { return 16; }
 
+// K split over two waves when each gets at least two steps of 128 and the
+// same number of them.
+static bool bf_split(int K) { return K % 256 == 0 && K >= 512; }
+
 void launch_s1_bf16_stream(const S1Args& a, long mt, hipStream_t s) {
   BfArgs p{a.xq, a.sorted, a.w13, a.w13s, a.hq, nullptr, a.H, 2 * a.I, a.I, a.H, a.k_total, a.t};
   const int ntl = a.I / (kBfS1 * 16);
   p.t.n_ntiles = ntl;
   p.t.ngroup = n_group_of(ntl);
   const long n = mt * ntl;
-  hipLaunchKernelGGL((bf16_stream_kernel<1, kBfS1>), dim3((int)((n + 7) / 8 * 8)), dim3(64),
-                     (size_t)2 * kBfS1 * 16 * (a.H / 32), s, p);
+  const dim3 grid((int)((n + 7) / 8 * 8));
+  const size_t lds = (size_t)2 * kBfS1 * 16 * (a.H / 32);
+  if (bf_split(a.H))
+    hipLaunchKernelGGL((bf16_stream_kernel<1, kBfS1, 2>), grid, dim3(128),
+                       lds + (size_t)2 * kBfS1 * 64 * 16, s, p);
+  else
+    hipLaunchKernelGGL((bf16_stream_kernel<1, kBfS1, 1>), grid, dim3(64), lds, s, p);
 }
 
 void launch_s2_bf16_stream(const S2Args& a, long mt, hipStream_t s) {
@@ -461,8 +493,13 @@ void launch_s2_bf16_stream(const S2Args& a, long mt, hipStream_t s) {
   p.t.n_ntiles = ntl;
   p.t.ngroup = n_group_of(ntl);
   const long n = mt * ntl;
-  hipLaunchKernelGGL((bf16_stream_kernel<2, kBfS2>), dim3((int)((n + 7) / 8 * 8)), dim3(64),
-                     (size_t)kBfS2 * 16 * (a.I / 32), s, p);
+  const dim3 grid((int)((n + 7) / 8 * 8));
+  const size_t lds = (size_t)kBfS2 * 16 * (a.I / 32);
+  if (bf_split(a.I))
+    hipLaunchKernelGGL((bf16_stream_kernel<2, kBfS2, 2>), grid, dim3(128),
+                       lds + (size_t)kBfS2 * 64 * 16, s, p);
+  else
+    hipLaunchKernelGGL((bf16_stream_kernel<2, kBfS2, 1>), grid, dim3(64), lds, s, p);
 }
 
 }  // namespace moe
