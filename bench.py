@@ -54,11 +54,14 @@ def sources_hash(kernel):
     return h.hexdigest()[:16]
 
 
-def stored_traffic(kernel, workload):
+def stored_traffic(kernel, workload, fmt="e4m3"):
     """HBM bytes per launch of `kernel` on `workload` from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE summaries (lines
-    'traffic_bytes kernel=... workload=... bytes=... sources=...'), or None
-    when there is none or the kernel's sources changed since it was taken."""
+    'traffic_bytes kernel=... workload=... bytes=... sources=...', taken with
+    MXFP8 activations), or None when there is none, the activation format
+    differs or the kernel's sources changed since it was taken."""
+    if fmt != "e4m3":
+        return None
     want = sources_hash(kernel)
     if not os.path.isdir(PROFILES):
         return None
@@ -201,7 +204,7 @@ def measure_workload(name, steps, fmt, use_graph, weights_np=None):
             "layer_GBps": gb, "layer_hbm_frac": gb / HBM_PEAK_GBS,
             "layer_TFLOPs": tf, "layer_frac_of_fp8_peak": tf / MFMA_PEAK_FP8_TFLOPS,
             "layer_frac_of_fp4_peak": tf / MFMA_PEAK_FP4_TFLOPS,
-            "gate_up_traffic": stored_traffic("s1_tiled_kernel", name),
+            "gate_up_traffic": stored_traffic("s1_tiled_kernel", name, fmt),
             "gate_up_algorithmic_bytes": r["gate_up_bytes"]}
 
 
@@ -456,7 +459,7 @@ def main():
         "graph_ms_per_step": r["graph_ms_per_step"],
         "roofline": {"kernel": "gate_up (stage 1)", "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": stored_traffic("s1_stream2_kernel", cfg.name),
+                     "traffic": stored_traffic("s1_stream2_kernel", cfg.name, args.fmt),
                      "algorithmic_bytes": r["gate_up_bytes"]},
         "stage_ms": r["stage_ms"],
         "step_ms_median": r["step_ms_median"],
@@ -502,7 +505,7 @@ def main():
                          "peak": MFMA_PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
                          "frac": tf / MFMA_PEAK_FP8_TFLOPS,
                          "frac_of_fp4_peak": tf / MFMA_PEAK_FP4_TFLOPS,
-                         "traffic": stored_traffic("s1_tiled_kernel", pcfg.name),
+                         "traffic": stored_traffic("s1_tiled_kernel", pcfg.name, args.fmt),
                          "algorithmic_bytes": p["gate_up_bytes"]},
             "layer_mfma_frac_of_fp4_peak": p["layer_flops"] / (p["ms_per_step"] * 1e-3) / 1e12
             / MFMA_PEAK_FP4_TFLOPS,
