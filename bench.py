@@ -98,7 +98,8 @@ def measure(cfg, weights_np, steps, warmup, fmt, use_graph=True, fused=False):
     else:                        # the step starts from the workload's logits
         logits = torch.from_numpy(synth.gen_logits(cfg)).to(dev)
         wr = None
-    w = tuple(torch.from_numpy(a[: cfg.NE]).to(dev) for a in weights_np)
+    # codes in the grouped GEMM's block layout, packed once at load time
+    w = moe.pack_expert_weights(tuple(torch.from_numpy(a[: cfg.NE]).to(dev) for a in weights_np))
     layer = moe.MoELayer(cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.n_shared, fmt, device=dev,
                          fused=fused)
     stream = torch.cuda.current_stream()

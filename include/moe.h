@@ -203,6 +203,24 @@ moe_status moe_permute(const int32_t* topk_ids, int T, int n_experts_total, int 
                        int32_t* counts, int32_t* offsets, int32_t* sorted, int32_t* pos, void* ws,
                        size_t ws_bytes, void* stream);
 
+/* ---- expert weight layout -------------------------------------------------
+ * The grouped GEMM reads FP4 e2m1 expert weights (two codes per byte, low
+ * nibble first, as the paper packs them: Prefill optimization / From
+ * per-assignment scalar work to CDNA2 MFMA) in a block layout of its own:
+ * rows in groups of 16, each group's bytes ordered by 64-byte K piece, then
+ * by row, so that byte c of K piece q of row 16 g + r of a [rows, K/2] code
+ * matrix sits at 16 g * K/2 + 1024 q + 64 r + c (one K piece of 16 rows is
+ * 1 KiB of contiguous memory). A group covers the same bytes in both
+ * layouts, so expert and row offsets are unchanged; only the bytes inside a
+ * group move. The E8M0 scales stay row-major. Weights are packed once, when
+ * they are loaded; the values are unchanged.
+ *   w    uint8 [rows, K/2] row-major codes (e.g. W13 viewed as [NE * 2I, H/2],
+ *        W2 as [NE * H, I/2]); read
+ *   out  uint8 [rows, K/2] in the block layout (written); must not overlap w
+ * Requires rows >= 0, rows % 16 == 0, K > 0, K % 128 == 0, both pointers
+ * 16-byte aligned (else MOE_ERR_INVALID_ARG, nothing enqueued). */
+moe_status moe_pack_fp4_weights(const uint8_t* w, uint8_t* out, long rows, int K, void* stream);
+
 /* ---- a4: activation quantisation (standalone) -----------------------------
  * Per block of 32 consecutive elements of each row: X = the smallest integer
  * in [-127, 127] with max|v| <= maxval(format) * 2^X (X = 0 for an all-zero
@@ -241,11 +259,15 @@ moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f
  *   partials[a, :] = hq . W2[e]^T                   (fp32, one unique row per
  *                                                   assignment: no atomics)
  * Products of codes and power-of-two scales are exact; sums are fp32 on the
- * matrix cores in a fixed order (no split-K).
+ * matrix cores in a fixed order (the weight-streaming geometry adds two
+ * halves of the K extent, first + second; no atomics, no run-to-run
+ * variation).
  *   x         bf16 [T, H]
  *   offsets   int32 [NE + 1], sorted int32 [T * k_total]   (from moe_permute)
  *   w13       uint8 [NE, 2I, H/2]   w13_s uint8 [NE, 2I, H/32]
  *   w2        uint8 [NE, H, I/2]    w2_s  uint8 [NE, H, I/32]
+ *             (w13 and w2 in the block layout of moe_pack_fp4_weights; the
+ *             scales row-major)
  *   partials  fp32 [T * k_total, H]; row a = t*k_total + j (written for every
  *             assignment with a valid expert id)
  * ws: device workspace of at least moe_fp4_grouped_gemm_workspace_bytes(...)

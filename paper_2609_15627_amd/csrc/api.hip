@@ -183,6 +183,16 @@ moe_status moe_quantize_act(const uint16_t* x, int rows, int K, moe_act_format f
   return launched(moe::launch_quantize_act(x, rows, K, fc, codes, scales, as_stream(stream)));
 }
 
+moe_status moe_pack_fp4_weights(const uint8_t* w, uint8_t* out, long rows, int K, void* stream) {
+  if (rows < 0 || rows % 16 || K <= 0 || K % 128) return MOE_ERR_INVALID_ARG;
+  if (rows == 0) return MOE_OK;
+  if (!w || !out || !aligned(w, 16) || !aligned(out, 16)) return MOE_ERR_INVALID_ARG;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(w), b = reinterpret_cast<uintptr_t>(out);
+  const uintptr_t n = (uintptr_t)rows * (uintptr_t)(K / 2);
+  if (a < b + n && b < a + n) return MOE_ERR_INVALID_ARG;  // overlapping buffers
+  return launched(moe::launch_pack_fp4(w, out, rows, K, as_stream(stream)));
+}
+
 // The GEMM kernels address activation rows (x, h) and one expert's weights
 // with 32-bit byte offsets from a base: each must stay below 4 GiB.
 static bool offsets_fit(int T, int H, int I, int k_total, int fc) {

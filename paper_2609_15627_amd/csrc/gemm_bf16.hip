@@ -171,13 +171,18 @@ __global__ __launch_bounds__(64 * kWaves) void bf16_gemm_kernel(BfArgs p) {
     const int c = (lane & 3) ^ ((r >> 2) & 3);
     aoff = (uint32_t)src * (uint32_t)(p.K * 2) + 16 * c;
   }
-  const uint32_t boff = (uint32_t)wrow(32 * w + l32) * (uint32_t)(p.K / 2);
+  // weights in the block layout: step s (16 bytes of a row) is bytes
+  // 16 (s % 4) of K piece s / 4 of the row's 16-row group
+  const int wr = wrow(32 * w + l32);
+  const uint32_t boff = (uint32_t)(wr & ~15) * (uint32_t)(p.K / 2) + 64 * (uint32_t)(wr & 15);
   // step s's slot; past the last step the slot gets the last step again
   auto issue = [&](int s) {
     const uint32_t slot = ring + (uint32_t)((s % kRingN) * kSlot);
     const int step = s < nk ? s : nk - 1;
     sdma16(p.act, aoff + (uint32_t)step * 64, slot + 16 * w * 64);
-    if (lane < 32) sdma16(wbase, boff + (uint32_t)step * 16, slot + kAS + 32 * w * 16);
+    if (lane < 32)
+      sdma16(wbase, boff + (uint32_t)(step >> 2) * 1024 + 16 * (uint32_t)(step & 3),
+             slot + kAS + 32 * w * 16);
   };
 
   // weight scale rows of the tile (stage 1: the 128 gate rows, then the 128
@@ -326,11 +331,11 @@ __global__ __launch_bounds__(64 * KW) void bf16_stream_kernel(BfArgs p) {
     return ST == 1 ? (n < NBW ? c0 + 16 * n : p.I + c0 + 16 * (n - NBW)) : c0 + 16 * n;
   };
   const uint8_t* wbase = p.w + (size_t)e * p.N * (p.K / 2);
-  uint32_t boff[NB];  // this lane's byte of step 0 in weight row wrow(n) + c16
+  uint32_t boff[NB];  // this lane's 16 bytes of step 0 (row wrow(n) + c16, block layout)
   uint32_t so[NB];    // LDS byte of this lane's scale of step 0
 #pragma unroll
   for (int n = 0; n < NB; ++n) {
-    boff[n] = (uint32_t)(wrow(n) + c16) * (uint32_t)(p.K / 2) + 16 * g;
+    boff[n] = (uint32_t)wrow(n) * (uint32_t)(p.K / 2) + 64 * c16 + 16 * g;  // block layout
     so[n] = (uint32_t)((16 * n + c16) * kb + g);
   }
 
@@ -344,16 +349,16 @@ __global__ __launch_bounds__(64 * KW) void bf16_stream_kernel(BfArgs p) {
   uint32_t ao = aoff + 256 * (uint32_t)s_lo;
   uint32_t bo[NB];
 #pragma unroll
-  for (int n = 0; n < NB; ++n) bo[n] = boff[n] + 64 * (uint32_t)s_lo;
+  for (int n = 0; n < NB; ++n) bo[n] = boff[n] + 1024 * (uint32_t)s_lo;
   auto load = [&](BfStep<NB>& f) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < 4; ++i) f.a[i] = ld16<false>(abase + ao + 16 * i);
 #pragma unroll
-    for (int n = 0; n < NB; ++n) f.b[n] = ld16<false>(wbase + bo[n]);
+    for (int n = 0; n < NB; ++n) f.b[n] = ld16<true>(wbase + bo[n]);  // streamed once
     ao += 256;
 #pragma unroll
-    for (int n = 0; n < NB; ++n) bo[n] += 64;
+    for (int n = 0; n < NB; ++n) bo[n] += 1024;  // next K piece of the 16-row group
     __builtin_amdgcn_sched_barrier(0);
   };
   BfStep<NB> f0, f1;

@@ -97,10 +97,12 @@ __global__ __launch_bounds__(256, 2) void s2_short_kernel(S2Args p) {
       const int rr = r < nrows ? r : 0;  // rows past the tile's end repeat row 0
       s_dma16(abase + (size_t)rr * L::kARow + 16 * c, lds + L::kA + 16 * (q - lane));
     }
+    // W2 in the block layout: chunk c of row r is K piece c / 4 of r's group
     const uint8_t* bbase = p.w2 + wr0 * L::kBRow;
     for (int q = tid; q < SBN * L::kBCh; q += 256) {
       const int r = q / L::kBCh, c = (q % L::kBCh) ^ s_key<L::kBCh>(q / L::kBCh);
-      s_dma16(bbase + (size_t)r * L::kBRow + 16 * c, lds + L::kB + 16 * (q - lane));
+      s_dma16(bbase + (size_t)(r & ~15) * L::kBRow + 1024 * (c >> 2) + 64 * (r & 15) + 16 * (c & 3),
+              lds + L::kB + 16 * (q - lane));
     }
     const uint8_t* asb = p.hs + (size_t)row0 * L::kSRow;
     for (int q = tid; q < SBM * L::kSRow / 4; q += 256) {

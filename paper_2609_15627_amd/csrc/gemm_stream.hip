@@ -71,8 +71,8 @@ struct Frag {
 // Code loads of one K step starting at 32-element block `step` (a multiple
 // of 4). Product j of the step covers the 128 elements [step*32 + 128j, +128):
 //  - a weight lane (column c16, lane group g) supplies block step + 4j + g,
-//    16 contiguous bytes; one load instruction reads 64 contiguous bytes of
-//    each of the wave's 16 rows;
+//    16 contiguous bytes; one load instruction reads the 16 rows' 64-byte
+//    pieces of one K piece, a contiguous KiB in the block layout;
 //  - an FP4 activation lane does the same on its row;
 //  - an FP8 activation lane supplies 16-element halves: the matrix core reads
 //    an FP8 lane's bytes 0-15 as K = 16g.. and bytes 16-31 as K = 64 + 16g..
@@ -105,11 +105,16 @@ __device__ __forceinline__ void frag_codes(Frag<FA, J, NB>& f, const uint8_t* a_
       }
     }
   }
+  // weights in the block layout (moe_pack_fp4_weights): b_rows[n] is this
+  // lane's 64-byte row piece of K piece 0 of its 16-row group; product j of
+  // the step is K piece step / 4 + j, one contiguous KiB for the 64 lanes,
+  // read with the streaming (non-temporal) policy, which pays for whole
+  // contiguous KiB reads
 #pragma unroll
   for (int n = 0; n < NB; ++n)
 #pragma unroll
     for (int j = 0; j < J; ++j)
-      f.b[n][j] = ld16<false>(b_rows[n] + b_off + (size_t)(step + 4 * j + g) * 16);
+      f.b[n][j] = ld16<true>(b_rows[n] + b_off + (size_t)(step / 4 + j) * 1024 + 16 * g);
   __builtin_amdgcn_sched_barrier(0);
 }
 
@@ -314,9 +319,9 @@ __global__ __launch_bounds__(128) void s1_stream2_kernel(S1Args p) {
   uint32_t wo[NB];
 #pragma unroll
   for (int b = 0; b < NBW; ++b) {
-    const size_t gr = ebase + hc0 + 16 * b + c16;  // gate row
-    b_rows[b] = p.w13 + gr * (p.H / 2);
-    b_rows[NBW + b] = p.w13 + (gr + p.I) * (p.H / 2);
+    const size_t gr = ebase + hc0 + 16 * b;  // first gate row of the group
+    b_rows[b] = p.w13 + gr * (p.H / 2) + 64 * c16;
+    b_rows[NBW + b] = p.w13 + (gr + p.I) * (p.H / 2) + 64 * c16;
     wo[b] = (16 * b + c16) * kb;
     wo[NBW + b] = (NBW * 16 + 16 * b + c16) * kb;
   }
@@ -374,9 +379,9 @@ __global__ __launch_bounds__(64) void s1_stream_kernel(S1Args p) {
   uint32_t wo[NB];
 #pragma unroll
   for (int b = 0; b < NBW; ++b) {
-    const size_t gr = ebase + hc0 + 16 * b + c16;  // gate row
-    b_rows[b] = p.w13 + gr * (p.H / 2);
-    b_rows[NBW + b] = p.w13 + (gr + p.I) * (p.H / 2);
+    const size_t gr = ebase + hc0 + 16 * b;  // first gate row of the group
+    b_rows[b] = p.w13 + gr * (p.H / 2) + 64 * c16;
+    b_rows[NBW + b] = p.w13 + (gr + p.I) * (p.H / 2) + 64 * c16;
     wo[b] = (16 * b + c16) * kb;
     wo[NBW + b] = (NBW * 16 + 16 * b + c16) * kb;
   }
@@ -417,7 +422,7 @@ __global__ __launch_bounds__(64) void s2_stream_kernel(S2Args p) {
   uint32_t wo[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    b_rows[b] = p.w2 + (rbase + 16 * b + c16) * (p.I / 2);
+    b_rows[b] = p.w2 + (rbase + 16 * b) * (p.I / 2) + 64 * c16;
     wo[b] = (16 * b + c16) * kb;
   }
   v4f acc[NB];
@@ -456,7 +461,7 @@ __global__ __launch_bounds__(128) void s2_stream2_kernel(S2Args p) {
   uint32_t wo[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    b_rows[b] = p.w2 + (rbase + 16 * b + c16) * (p.I / 2);
+    b_rows[b] = p.w2 + (rbase + 16 * b) * (p.I / 2) + 64 * c16;
     wo[b] = (16 * b + c16) * kb;
   }
   v4f acc[NB];
@@ -585,7 +590,7 @@ __device__ __forceinline__ void s2c_tiles(const S2CArgs& c, uint8_t* lds, float*
   auto a_row = [&](const S2CTile& t) {
     return p.hq + ((size_t)t.row0 + (c16 < t.nrows ? c16 : 0)) * (p.I / 32) * kAB;
   };
-  auto b_row = [&](const S2CTile& t) { return p.w2 + (t.rbase + c16) * (p.I / 2); };
+  auto b_row = [&](const S2CTile& t) { return p.w2 + t.rbase * (p.I / 2) + 64 * c16; };
 
   S2CTile tc = s2c_tile(p.t.tiles[tj], p.H, nc0);
   int4 tn4 = p.t.tiles[tj + W < ntl ? tj + W : tj];
@@ -676,7 +681,7 @@ __global__ __launch_bounds__(64 * kFusedWaves) void s2c_stream_kernel(S2CArgs c)
       for (int i = 0; i < 4; ++i) arow[i] = 4 * g + i < nrows ? p.sorted[row0 + 4 * g + i] : -1;
       const size_t ar = (size_t)row0 + (c16 < nrows ? c16 : 0);
       const uint8_t* a_row = p.hq + ar * (p.I / 32) * kAB;
-      const uint8_t* b_rows[1] = {p.w2 + (rbase + c16) * (p.I / 2)};
+      const uint8_t* b_rows[1] = {p.w2 + rbase * (p.I / 2) + 64 * c16};
       const uint32_t wo[1] = {(uint32_t)(c16 * kb)};
       v4f acc[1] = {v4f{0.f, 0.f, 0.f, 0.f}};
       stream_k<FA, J, 1, false>(

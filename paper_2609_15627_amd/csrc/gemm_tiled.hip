@@ -11,7 +11,9 @@
 //  - operands travel global -> LDS by DMA (global_load_lds, 16 bytes a lane,
 //    1 KiB of contiguous LDS per instruction) through a ring of NS K-step
 //    stages (3 with FP8 activations, 4 with FP4 ones, whose stages are
-//    smaller); every instruction reads whole 64- or 128-byte row segments;
+//    smaller); an activation instruction reads whole 64- or 128-byte row
+//    segments, a weight instruction one contiguous KiB (16 rows x 64 bytes of
+//    the block layout of moe_pack_fp4_weights);
 //  - E8M0 scales move in 16-byte row pieces covering four K steps (a
 //    separate ring of two scale groups), not one word per row per step: a
 //    4-byte gather costs a cache line per lane;
@@ -149,7 +151,7 @@ template <int FA, bool AON>
 __device__ __forceinline__ void t_issue_stage(uint8_t* lds, const TSrc<FA>& S, int w, int k) {
   using L = TL<FA>;
   uint8_t* st = lds + (k % L::kNS) * L::kStage;
-  const size_t ka = (size_t)k * L::kARow, kb = (size_t)k * 64;
+  const size_t ka = (size_t)k * L::kARow, kb = (size_t)k * 1024;  // K piece k of the weight groups
   if constexpr (AON) {
 #pragma unroll
     for (int i = 0; i < L::kAInstr; ++i)
@@ -351,7 +353,7 @@ __device__ __forceinline__ void t_step(uint8_t* lds, const TSrc<FA>& src, const 
   const uint8_t* sbuf1 = lds + Lo::kS + ((k1 / kSG) & 1) * Lo::kSBuf;
   const uint8_t* st1 = lds + (NS == 4 ? (J + 1) % 4 : k1 % NS) * Lo::kStage;
   uint8_t* dst = lds + slot * Lo::kStage;  // stage k + NS reuses the slot of step k
-  const size_t ka = (size_t)(k + NS) * Lo::kARow, kb = (size_t)(k + NS) * 64;
+  const size_t ka = (size_t)(k + NS) * Lo::kARow, kb = (size_t)(k + NS) * 1024;
   uint8_t* sdst = lds + Lo::kS + ((k / kSG + 1) & 1) * Lo::kSBuf;
   constexpr int kR = kNext ? kOpReads + kScaleReads : 0;
   constexpr int kDS = kScales ? kScaleLoads : 0;
@@ -627,7 +629,8 @@ __device__ __forceinline__ S1Tile<FA> s1_setup(const S1Args& p, int4 tile, int n
   for (int i = 0; i < Lo::kBInstr; ++i) {
     int r, ch;
     t_bslot(Lo::kBInstr * w + i, lane, &r, &ch);
-    c.S.b[i] = (uint32_t)(wrow(r) * (p.H / 2) + 16 * ch);
+    const int wr = wrow(r);  // its 16-row group in the block layout, K piece 0
+    c.S.b[i] = (uint32_t)((wr & ~15) * (p.H / 2) + 64 * (wr & 15) + 16 * ch);
   }
   const int ra = t_arow0(w) + lane;
   const int tok = p.sorted[row0 + (ra < nrows ? ra : 0)] / p.k_total;
@@ -762,7 +765,7 @@ __device__ __forceinline__ S2Tile<FA> s2_setup(const S2Args& p, int4 tile, int n
   for (int i = 0; i < Lo::kBInstr; ++i) {
     int r, ch;
     t_bslot(Lo::kBInstr * w + i, lane, &r, &ch);
-    c.S.b[i] = (uint32_t)(r * (p.I / 2) + 16 * ch);
+    c.S.b[i] = (uint32_t)((r & ~15) * (p.I / 2) + 64 * (r & 15) + 16 * ch);  // block layout
   }
   const int ra = t_arow0(w) + lane;
   c.S.as = (uint32_t)((ra < nrows ? ra : 0) * (p.I / 32));

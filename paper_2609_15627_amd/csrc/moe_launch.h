@@ -70,6 +70,9 @@ bool fused_combine_ok(const GemmArgs& a);
 hipError_t launch_combine(const float* partials, const float* w, int T, int H, int k_total,
                           uint16_t* out, hipStream_t s);
 
+// Expert weights [rows, K/2] FP4 codes -> the GEMM's layout (pack.hip).
+hipError_t launch_pack_fp4(const uint8_t* w, uint8_t* out, long rows, int K, hipStream_t s);
+
 hipError_t launch_probe(const uint8_t* a, const uint8_t* sa, int fmt, const uint8_t* b,
                         const uint8_t* sb, float* d, hipStream_t s);
 

@@ -35,6 +35,7 @@ _SIGNATURES = {
     "moe_permute_workspace_bytes": (_SZ, [_I, _I, _I]),
     "moe_permute": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _P, _SZ, _P]),
     "moe_quantize_act": (_I, [_P, _I, _I, _I, _P, _P, _P]),
+    "moe_pack_fp4_weights": (_I, [_P, _P, ctypes.c_long, _I, _P]),
     "moe_fp4_grouped_gemm_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I]),
     "moe_fp4_grouped_gemm_workspace_layout": (_I, [_I, _I, _I, _I, _I, _I, ctypes.POINTER(_SZ)]),
     "moe_fp4_grouped_gemm": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P,
@@ -229,6 +230,32 @@ def moe_quantize_act(x, fmt="e4m3", codes=None, scales=None, stream=None):
     return codes, scales
 
 
+def moe_pack_fp4_weights(w, out=None, stream=None):
+    """FP4 code matrix (uint8, last dimension K/2, any leading dimensions:
+    e.g. W13 [NE, 2I, H/2]) into the grouped GEMM's block layout; returns a
+    tensor of the same shape."""
+    if w.dtype != torch.uint8 or not w.is_cuda or not w.is_contiguous():
+        raise ValueError("w: contiguous uint8 tensor on the GPU expected")
+    kbytes = w.shape[-1]
+    rows = w.numel() // kbytes if kbytes else 0
+    if out is None:
+        out = torch.empty_like(w)
+    elif out.shape != w.shape or out.dtype != torch.uint8 or not out.is_contiguous():
+        raise ValueError("out: contiguous uint8 tensor of w's shape expected")
+    _check(lib.moe_pack_fp4_weights(_ptr(w), _ptr(out), rows, 2 * kbytes, _stream(stream)),
+           "moe_pack_fp4_weights")
+    return out
+
+
+def pack_expert_weights(weights, stream=None):
+    """(w13, w13_s, w2, w2_s) with row-major codes -> the same tuple with both
+    code tensors in the block layout the grouped GEMM reads (the scales are
+    unchanged). Done once, when the weights are loaded."""
+    w13, w13_s, w2, w2_s = weights
+    return (moe_pack_fp4_weights(w13, stream=stream), w13_s,
+            moe_pack_fp4_weights(w2, stream=stream), w2_s)
+
+
 def moe_fp4_grouped_gemm_workspace_bytes(T, H, I, n_experts_total, k_total, fmt="e4m3"):
     return lib.moe_fp4_grouped_gemm_workspace_bytes(T, H, I, n_experts_total, k_total,
                                                     ACT_FORMATS[fmt])
@@ -400,7 +427,8 @@ class MoELayer:
         return self.gemm_ws[off[region]:off[region + 1]]
 
     def forward(self, x, weights, logits=None, w_router=None, stream=None, events=None):
-        """Enqueue the layer. ``events``: optional list of 7 torch.cuda.Event
+        """Enqueue the layer. ``weights``: (w13, w13_s, w2, w2_s) with the codes in
+        the block layout (``pack_expert_weights``). ``events``: optional list of 7 torch.cuda.Event
         recorded between the steps (route, permute, quantise, gate/up, down,
         combine) for per-step timing; with the fused path "down" is the fused
         down projection + combine and "combine" is empty."""

@@ -33,6 +33,23 @@ def bf16_to_f64(bits):
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
+def pack_fp4_ref(w):
+    """The block layout of moe_pack_fp4_weights written out in numpy: a
+    [rows, K/2] code matrix as groups of 16 rows, each group's bytes ordered
+    by 64-byte K piece, then row, then byte."""
+    w = np.ascontiguousarray(w, np.uint8)
+    rows, kb = w.shape
+    return w.reshape(rows // 16, 16, kb // 64, 64).transpose(0, 2, 1, 3).reshape(rows, kb)
+
+
+def dev_expert_weights(ws):
+    """Row-major numpy (w13, w13_s, w2, w2_s) -> device tensors with the codes
+    in the grouped GEMM's block layout (moe_pack_fp4_weights; scales as they
+    are)."""
+    from paper_2609_15627_amd import moe
+    return moe.pack_expert_weights(tuple(to_dev_u8(a) for a in ws))
+
+
 @functools.lru_cache(maxsize=2)
 def _stacked_weights(H, I, NE, seed):
     cfg = synth.LayerConfig("w", 1, H, NE, 1, I, 0, "normal", seed)
@@ -41,7 +58,7 @@ def _stacked_weights(H, I, NE, seed):
 
 @functools.lru_cache(maxsize=1)
 def _dev_weights(H, I, NE, seed):
-    return tuple(to_dev_u8(a) for a in _stacked_weights(H, I, NE, seed))
+    return dev_expert_weights(_stacked_weights(H, I, NE, seed))
 
 
 def drop_caches():
@@ -51,10 +68,12 @@ def drop_caches():
 
 
 def dev_weights(cfg, share=True):
-    """Device weights of a config. Routed experts depend only on (H, I, e, seed),
-    so configs with equal dims share one upload (the shared expert is index E)."""
+    """Device weights of a config (codes in the block layout). Routed experts
+    depend only on (H, I, e, seed), so configs with equal dims share one
+    upload (the shared expert is index E); a block-layout tensor sliced to
+    its first NE experts is the block layout of those experts."""
     if not share:
-        return tuple(to_dev_u8(a) for a in synth.gen_all_experts(cfg))
+        return dev_expert_weights(synth.gen_all_experts(cfg))
     ne_max = 257 if (cfg.H, cfg.I) == (4096, 2048) else cfg.NE
     full = _dev_weights(cfg.H, cfg.I, ne_max, cfg.seed)
     if cfg.NE == ne_max:

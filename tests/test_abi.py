@@ -204,3 +204,20 @@ def test_noalloc_gemm_rejects_before_touching_the_gpu(m):
     assert call(64, f=9) == m.MOE_ERR_INVALID_ARG                    # format
     assert call(64, x=NUL) == m.MOE_ERR_INVALID_ARG                  # null pointer
     assert call(0) == m.MOE_OK                                       # empty batch: nothing enqueued
+
+
+def test_pack_fp4_weights_validation(m):
+    """The weight packing call rejects shapes outside its layout and
+    overlapping or misaligned buffers on the host."""
+    L = m.lib
+    buf = ctypes.create_string_buffer(64 * 1024 + 16)
+    base = (ctypes.addressof(buf) + 15) // 16 * 16
+    src, dst = ctypes.c_void_p(base), ctypes.c_void_p(base + 32 * 1024)
+    assert L.moe_pack_fp4_weights(src, dst, 0, 128, NUL) == 0        # nothing to do
+    assert L.moe_pack_fp4_weights(src, dst, 15, 128, NUL) == 1       # rows % 16
+    assert L.moe_pack_fp4_weights(src, dst, 16, 96, NUL) == 1        # K % 128
+    assert L.moe_pack_fp4_weights(src, dst, -16, 128, NUL) == 1
+    assert L.moe_pack_fp4_weights(src, src, 16, 128, NUL) == 1       # in place
+    assert L.moe_pack_fp4_weights(src, ctypes.c_void_p(base + 512), 16, 128, NUL) == 1  # overlap
+    assert L.moe_pack_fp4_weights(ctypes.c_void_p(base + 4), dst, 16, 128, NUL) == 1    # alignment
+    assert L.moe_pack_fp4_weights(None, dst, 16, 128, NUL) == 1

@@ -38,7 +38,7 @@ def m():
 
 
 def run(m, cfg, inp, weights=None, fmt="bf16"):
-    w = weights if weights is not None else tuple(gc.to_dev_u8(a) for a in inp.weights)
+    w = weights if weights is not None else gc.dev_expert_weights(inp.weights)
     layer = m.MoELayer(cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.n_shared, fmt)
     out = layer.forward(gc.to_dev_bf16(inp.x), w, logits=torch.from_numpy(inp.logits).cuda())
     torch.cuda.synchronize()
@@ -108,7 +108,7 @@ def test_bf16_small_layers(m, shape):
     assert np.array_equal(layer.ids.cpu().numpy(), ref["ids"])
     assert np.array_equal(layer.perm[2].cpu().numpy(), ref["sorted"])
     first = gc.bf16_bits(out).copy()
-    w = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    w = gc.dev_expert_weights(inp.weights)
     for _ in range(3):
         o2 = layer.forward(gc.to_dev_bf16(inp.x), w, logits=torch.from_numpy(inp.logits).cuda())
         torch.cuda.synchronize()
@@ -169,7 +169,7 @@ def test_bf16_streaming_skewed(m):
     counts = np.bincount(ref["ids"].ravel(), minlength=cfg.NE)
     assert (counts == 0).any() and counts.max() > 16, counts
     first = gc.bf16_bits(out).copy()
-    o2 = layer.forward(gc.to_dev_bf16(inp.x), tuple(gc.to_dev_u8(a) for a in inp.weights),
+    o2 = layer.forward(gc.to_dev_bf16(inp.x), gc.dev_expert_weights(inp.weights),
                        logits=torch.from_numpy(inp.logits).cuda())
     torch.cuda.synchronize()
     assert np.array_equal(gc.bf16_bits(o2), first)

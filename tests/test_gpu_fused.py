@@ -26,7 +26,7 @@ def m():
 
 
 def both_paths(m, cfg, inp, fmt="e4m3", weights=None):
-    w = weights if weights is not None else tuple(gc.to_dev_u8(a) for a in inp.weights)
+    w = weights if weights is not None else gc.dev_expert_weights(inp.weights)
     x = gc.to_dev_bf16(inp.x)
     assert m.moe_fp4_grouped_gemm_combine_supported(cfg.T, cfg.H, cfg.I, cfg.NE, cfg.k_total, fmt)
     lf, of = run_layer(m, cfg, x, w, logits=inp.logits, fmt=fmt, fused=True)
@@ -96,7 +96,7 @@ def test_fused_stages_and_graph(m):
     captured graph of the fused layer, replayed several times."""
     cfg = synth.LayerConfig("fused_st", 48, 1024, 64, 8, 512, 1, "normal", 5)
     inp = synth.make_inputs(cfg)
-    w = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    w = gc.dev_expert_weights(inp.weights)
     x = gc.to_dev_bf16(inp.x)
     lg = torch.from_numpy(inp.logits).cuda()
     log("fused stages")
@@ -127,7 +127,7 @@ def test_fused_rejects(m):
     cfg = synth.LayerConfig("rej", 600, 512, 2, 1, 1024, 0, "normal", 3)
     inp = synth.make_inputs(cfg)
     x = gc.to_dev_bf16(inp.x)
-    w = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    w = gc.dev_expert_weights(inp.weights)
     ids = torch.from_numpy(np.argmax(inp.logits, 1).astype(np.int32)[:, None]).cuda()
     tw = torch.ones((cfg.T, 1), dtype=torch.float32, device="cuda")
     _, offsets, srt, _ = m.moe_permute(ids, cfg.NE)

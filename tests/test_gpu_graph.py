@@ -36,7 +36,7 @@ def test_graph_replays_match_eager(m, shape, variant):
     inp = synth.make_inputs(cfg)
     log(f"graph: shape={shape}")
     x = gc.to_dev_bf16(inp.x)
-    w = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    w = gc.dev_expert_weights(inp.weights)
     lg = torch.from_numpy(inp.logits).cuda()
     eager = m.MoELayer(T, H, E, k, I, S, "e4m3")
     ref = eager.forward(x, w, logits=lg).clone()

@@ -11,6 +11,7 @@ import torch
 import synth
 from oracle import moe as omoe
 from oracle import mx
+from tests import gpu_common as gc
 from tests.gpu_common import bf16_bits, log, to_dev_bf16, to_dev_u8
 
 pytestmark = pytest.mark.gpu
@@ -256,7 +257,7 @@ def test_layer_empty_batch(m, fmt):
     H, I, E, k, S = 256, 128, 8, 2, 1
     cfg = synth.LayerConfig("empty", 4, H, E, k, I, S, "normal", 1)
     inp = synth.make_inputs(cfg)
-    w = tuple(torch.from_numpy(a).cuda() for a in inp.weights)
+    w = gc.dev_expert_weights(inp.weights)
     lg = torch.empty((0, E), dtype=torch.float32, device="cuda")
     ids, tw = m.moe_route_topk(lg, k, S)
     counts, offsets, sorted_, pos = m.moe_permute(ids, cfg.NE)
@@ -267,3 +268,26 @@ def test_layer_empty_batch(m, fmt):
     assert ids.shape == (0, k + S) and sorted_.numel() == 0
     assert int(counts.sum().item()) == 0 and int(offsets[-1].item()) == 0
     assert partials.shape == (0, H) and out.shape == (0, H)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("rows,K", [(16, 128), (48, 512), (4096, 2048), (257 * 32, 4096)])
+def test_pack_fp4_weights(m, rows, K):
+    """The weight block layout: byte c of K piece q of row 16 g + r at
+    16 g * K/2 + 1024 q + 64 r + c, bit-exact against the numpy permutation
+    and against that formula on sampled bytes."""
+    log(f"pack fp4 weights rows={rows} K={K}")
+    w = np.random.default_rng(rows + K).integers(0, 256, size=(rows, K // 2), dtype=np.uint8)
+    got = m.moe_pack_fp4_weights(to_dev_u8(w)).cpu().numpy()
+    ref = gc.pack_fp4_ref(w)
+    assert np.array_equal(got, ref)
+    flat = got.reshape(-1)
+    rng = np.random.default_rng(1)
+    for _ in range(64):
+        row, byte = int(rng.integers(rows)), int(rng.integers(K // 2))
+        g, r, q, c = row // 16, row % 16, byte // 64, byte % 64
+        assert flat[16 * g * (K // 2) + 1024 * q + 64 * r + c] == w[row, byte]
+    # a 3-D view (experts x rows) packs the same bytes
+    if rows % 32 == 0:
+        got3 = m.moe_pack_fp4_weights(to_dev_u8(w.reshape(2, rows // 2, K // 2))).cpu().numpy()
+        assert np.array_equal(got3.reshape(rows, K // 2), ref)

@@ -252,7 +252,7 @@ def small_case(T, H, I, E, k, S, seed, routing="normal"):
 def test_small_layers(m, shape, fmt):
     cfg, inp = small_case(*shape, seed=sum(shape))
     log(f"small layer {shape} {fmt}")
-    weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    weights = gc.dev_expert_weights(inp.weights)
     # the unfused path, so its partials are checked too (the fused path's
     # output is compared with this path's bit for bit in test_gpu_fused.py)
     layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, logits=inp.logits, fmt=fmt)
@@ -273,7 +273,7 @@ def test_tiled_geometry_skewed(m):
     cfg = synth.LayerConfig("skew", 600, 512, 16, 4, 512, 0, "zipf", 5, zipf_empty=3)
     inp = synth.make_inputs(cfg)
     log("tiled skewed")
-    weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    weights = gc.dev_expert_weights(inp.weights)
     layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, logits=inp.logits)
     assert m.moe_last_variant() == m.VARIANT_TILED
     check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T))
@@ -284,7 +284,7 @@ def test_tiny_config_with_router(m):
     cfg = synth.CONFIGS["tiny"]
     inp = synth.make_inputs(cfg)
     log("tiny config")
-    weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    weights = gc.dev_expert_weights(inp.weights)
     wr = gc.to_dev_bf16(inp.wr)
     layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, wr=wr)
     lg64 = omoe.router_logits(inp.x, inp.wr)
@@ -332,7 +332,7 @@ def test_hand_cases_exact(m):
 def test_empty_tokens(m):
     log("T = 0")
     cfg = synth.LayerConfig("empty", 0, 256, 8, 2, 128, 1)
-    w = tuple(gc.to_dev_u8(a) for a in synth.gen_all_experts(cfg))
+    w = gc.dev_expert_weights(synth.gen_all_experts(cfg))
     layer = m.MoELayer(0, 256, 8, 2, 128, 1)
     out = layer.forward(torch.empty((0, 256), dtype=torch.bfloat16, device="cuda"), w,
                         logits=torch.empty((0, 8), dtype=torch.float32, device="cuda"))
@@ -411,7 +411,7 @@ def test_metamorphic_w2_scale_doubles_output(m):
     cfg = synth.LayerConfig("mm", 96, 512, 16, 4, 256, 1, "normal", 3)
     inp = synth.make_inputs(cfg)
     log("metamorphic w2 scale")
-    w = [gc.to_dev_u8(a) for a in inp.weights]
+    w = list(gc.dev_expert_weights(inp.weights))
     x = gc.to_dev_bf16(inp.x)
     _, out = run_layer(m, cfg, x, tuple(w), logits=inp.logits)
     base = gc.bf16_to_f64(gc.bf16_bits(out))
@@ -452,7 +452,7 @@ def test_layer_at_expert_and_k_limits(m):
     cfg = synth.LayerConfig("limits", 8, 256, 1024, 31, 128, 1, "normal", 11)
     inp = synth.make_inputs(cfg)
     log("layer at the expert and k limits")
-    weights = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    weights = gc.dev_expert_weights(inp.weights)
     layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, logits=inp.logits)
     ref, _ = check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T))
     assert np.array_equal(layer.ids.cpu().numpy(), ref["ids"])

@@ -37,7 +37,7 @@ def m():
 def test_partials_decode_to_identity(m, T, H, I, variants, fmt):
     log(f"layout fingerprint T={T} H={H} I={I} {fmt}")
     w_np = fp.weights(H, I)
-    w = tuple(gc.to_dev_u8(a) for a in w_np)
+    w = gc.dev_expert_weights(w_np)
     x = gc.to_dev_bf16(fp.x_bits(T, H))
     layer = m.MoELayer(T, H, 1, 1, I, 0, fmt)
     layer.forward(x, w, logits=torch.zeros((T, 1), dtype=torch.float32, device="cuda"))

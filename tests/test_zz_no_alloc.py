@@ -30,7 +30,7 @@ def _inputs(m, shape, seed, fmt):
     cfg = synth.LayerConfig("noalloc", T, H, E, k, I, S, "normal", seed)
     inp = synth.make_inputs(cfg)
     x = gc.to_dev_bf16(inp.x)
-    w = tuple(gc.to_dev_u8(a) for a in inp.weights)
+    w = gc.dev_expert_weights(inp.weights)
     ids, _ = m.moe_route_topk(torch.from_numpy(inp.logits).cuda(), k, S)
     _, offsets, srt, _ = m.moe_permute(ids, cfg.NE)
     return cfg, x, w, offsets, srt
