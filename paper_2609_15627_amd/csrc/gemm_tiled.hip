@@ -4,8 +4,13 @@
 // Workgroup tile: 256 sorted rows of one expert x 256 weight rows (stage 1:
 // 128 gate rows and the 128 matching up rows; stage 2: 256 output columns),
 // K in steps of 128 = two 64-element sub-steps. Four waves in a 2 x 2
-// arrangement, one per SIMD; each owns 128 rows x 128 weight rows = 4 x 4
-// products of 32x32 per sub-step, accumulated in fp32.
+// arrangement, one per SIMD; each owns four 32-row blocks x 128 weight rows
+// = 4 x 4 products of 32x32 per sub-step, accumulated in fp32. The wave
+// halves take alternate row blocks (wave half wm: blocks wm, wm + 2, wm + 4,
+// wm + 6), so a tile of fewer rows (an expert's overflow past 256 rows, or
+// the ~128-row tiles of the TP-shard shape) still keeps both halves' matrix
+// cores busy; in LDS the rows sit in owner order (t_row), so each wave's
+// operand reads and DMA stay within one contiguous half.
 //
 // Data movement, chosen from measurements on gfx950:
 //  - operands travel global -> LDS by DMA (global_load_lds, 16 bytes a lane,
@@ -136,10 +141,11 @@ __device__ __forceinline__ void t_bslot(int ci, int lane, int* row, int* chunk) 
   *chunk = (lane % 4) ^ ((*row >> 2) & 3);
 }
 
-// Activation rows a wave moves by DMA: the 64 rows from t_arow0(w), inside
-// the 128 rows the wave multiplies (rows 128 (w & 1) ..), so a wave without
-// rows to multiply (a tile of at most 128 rows, w odd) moves no activation
-// data either. Its DMA instruction i fills activation tile chunk t_aci.
+// Activation rows a wave moves by DMA: LDS positions t_arow0(w) .. + 63,
+// inside the 128 positions the wave multiplies (128 (w & 1) ..), which hold
+// two of its wave half's row blocks, so a wave without rows to multiply (a
+// tile of at most 32 rows, w odd) moves no activation data either. Its DMA
+// instruction i fills activation tile chunk t_aci.
 __device__ __forceinline__ int t_arow0(int w) { return 128 * (w & 1) + 64 * (w >> 1); }
 template <int FA>
 __device__ __forceinline__ int t_aci(int w, int i) {
@@ -559,10 +565,17 @@ __device__ __forceinline__ bool t_next(const TileArgs& t, int* slot, int nch, in
   }
 }
 
-// Row blocks of 32 that wave half wm (rows 128 wm ..) multiplies in a tile of
-// nrows rows (wave-uniform).
+// Tile row held at LDS row position pos: positions 128 wm + 32 mb + r hold
+// row 32 (2 mb + wm) + r, wave half wm's block mb (row blocks alternate
+// between the wave halves).
+__device__ __forceinline__ int t_row(int pos) {
+  return 64 * ((pos >> 5) & 3) + 32 * (pos >> 7) + (pos & 31);
+}
+// Row blocks of 32 that wave half wm multiplies in a tile of nrows rows
+// (blocks wm, wm + 2, .. that hold rows; wave-uniform).
 __device__ __forceinline__ int t_nmb(int nrows, int wm) {
-  return __builtin_amdgcn_readfirstlane(min(4, max(0, (nrows - 128 * wm + 31) / 32)));
+  const int nb = (nrows + 31) / 32;  // 32-row blocks holding rows
+  return __builtin_amdgcn_readfirstlane(min(4, max(0, (nb + 1 - wm) / 2)));
 }
 
 template <int FA, int ST>
@@ -618,7 +631,8 @@ __device__ __forceinline__ S1Tile<FA> s1_setup(const S1Args& p, int4 tile, int n
   for (int i = 0; i < Lo::kAInstr; ++i) {
     int r, ch;
     t_aslot<FA>(t_aci<FA>(w, i), lane, &r, &ch);
-    const int tok = p.sorted[row0 + (r < nrows ? r : 0)] / p.k_total;
+    const int R = t_row(r);
+    const int tok = p.sorted[row0 + (R < nrows ? R : 0)] / p.k_total;
     c.S.a[i] = (uint32_t)(tok * xrow + 16 * ch);
   }
   // weight row (within the expert) of tile row r: 128 gate rows, then the 128 up rows
@@ -632,7 +646,7 @@ __device__ __forceinline__ S1Tile<FA> s1_setup(const S1Args& p, int4 tile, int n
     const int wr = wrow(r);  // its 16-row group in the block layout, K piece 0
     c.S.b[i] = (uint32_t)((wr & ~15) * (p.H / 2) + 64 * (wr & 15) + 16 * ch);
   }
-  const int ra = t_arow0(w) + lane;
+  const int ra = t_row(t_arow0(w) + lane);
   const int tok = p.sorted[row0 + (ra < nrows ? ra : 0)] / p.k_total;
   c.S.as = (uint32_t)(tok * (p.H / 32));
   c.S.bs = (uint32_t)(wrow(64 * w + lane) * (p.H / 32));
@@ -654,7 +668,8 @@ __device__ __forceinline__ uint32_t t_xhalf(uint32_t x, int h) {
 
 // Stage-1 epilogue, in registers. The accumulators hold the transposed tile:
 // block (mb, nb), element i of lane l is weight row t_nrow(nb) + 8 (i / 4) +
-// 4 h + i % 4 (h = l / 32) of the wave, token column 32 mb + l % 32. Gate
+// 4 h + i % 4 (h = l / 32) of the wave, token column 64 mb + 32 wm + l % 32
+// of the tile (the wave half's row block mb). Gate
 // block q and up block q + 2 cover the same 32 h columns, so the 32 values
 // of one token's quantisation block are lane l's 16 and lane (l ^ 32)'s 16:
 // the block maximum takes one exchange, and two more assemble each lane's
@@ -670,7 +685,7 @@ __device__ __forceinline__ void s1_epilogue(const S1Args& p, v16f (*acc)[4], int
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) {
     if (mb < nmb) {
-      const int tr = 128 * wm + 32 * mb + r;  // token row within the tile
+      const int tr = 64 * mb + 32 * wm + r;  // token row within the tile
       uint8_t* crow_p = p.hq + ((size_t)row0 + tr) * crow;
       uint32_t sc = 0;
 #pragma unroll
@@ -756,7 +771,8 @@ __device__ __forceinline__ S2Tile<FA> s2_setup(const S2Args& p, int4 tile, int n
   for (int i = 0; i < Lo::kAInstr; ++i) {
     int r, ch;
     t_aslot<FA>(t_aci<FA>(w, i), lane, &r, &ch);
-    c.S.a[i] = (uint32_t)((r < nrows ? r : 0) * arow + 16 * ch);
+    const int R = t_row(r);
+    c.S.a[i] = (uint32_t)((R < nrows ? R : 0) * arow + 16 * ch);
   }
   const size_t wr0 = (size_t)e * p.H + c.nc0;  // first weight row of the tile
   c.S.bbase = p.w2 + wr0 * (p.I / 2);
@@ -767,7 +783,7 @@ __device__ __forceinline__ S2Tile<FA> s2_setup(const S2Args& p, int4 tile, int n
     t_bslot(Lo::kBInstr * w + i, lane, &r, &ch);
     c.S.b[i] = (uint32_t)((r & ~15) * (p.I / 2) + 64 * (r & 15) + 16 * ch);  // block layout
   }
-  const int ra = t_arow0(w) + lane;
+  const int ra = t_row(t_arow0(w) + lane);
   c.S.as = (uint32_t)((ra < nrows ? ra : 0) * (p.I / 32));
   c.S.bs = (uint32_t)((64 * w + lane) * (p.I / 32));
   return c;
@@ -830,10 +846,10 @@ __global__ __launch_bounds__(256, 1) void s2_tiled_kernel(S2Args p) {
         int slot16[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i)
-          slot16[i] = sidx[128 * wm + 32 * mb + 8 * (i / 4) + 4 * g + (i % 4)];
+          slot16[i] = sidx[64 * mb + 32 * wm + 8 * (i / 4) + 4 * g + (i % 4)];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int row = 128 * wm + 32 * mb + 8 * (i / 4) + 4 * g + (i % 4);
+          const int row = 64 * mb + 32 * wm + 8 * (i / 4) + 4 * g + (i % 4);
           if (row < nrows) {
             float* dst = col + (size_t)slot16[i] * p.H;
 #pragma unroll
