@@ -688,6 +688,11 @@ __device__ __forceinline__ void s1_epilogue(const S1Args& p, v16f (*acc)[4], int
       const int tr = 64 * mb + 32 * wm + r;  // token row within the tile
       uint8_t* crow_p = p.hq + ((size_t)row0 + tr) * crow;
       uint32_t sc = 0;
+      // both blocks' codes first, then the stores: one branch per row block,
+      // so the two blocks' arithmetic can be scheduled together
+      uint4 v8[2];
+      uint32_t v6[2][3];
+      uint2 v4[2];
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
         float hv[16];
@@ -722,29 +727,34 @@ __device__ __forceinline__ void s1_epilogue(const S1Args& p, v16f (*acc)[4], int
         // lane h = 0 keeps block positions 0-15, lane h = 1 positions 16-31
         const uint32_t s0 = h ? d[0] : d[2], s1 = h ? d[1] : d[3];
         const uint32_t r0 = t_xhalf(s0, h), r1 = t_xhalf(s1, h);
-        if (tr < nrows) {
+        if constexpr (FA == 0) {
+          v8[q] = h ? make_uint4(r0, d[2], r1, d[3]) : make_uint4(d[0], r0, d[1], r1);
+        } else if constexpr (FA == 2) {  // 16 codes at 6 bits: 12 bytes of the slot
+          const uint32_t wv[4] = {h ? r0 : d[0], h ? d[2] : r0, h ? r1 : d[1], h ? d[3] : r1};
+          pack6x16(wv, v6[q]);
+        } else {
+          v4[q] = h ? make_uint2(r0 | (d[2] << 16), r1 | (d[3] << 16))
+                    : make_uint2(d[0] | (r0 << 16), d[1] | (r1 << 16));
+        }
+      }
+      if (tr < nrows) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
           if constexpr (FA == 0) {
-            const uint4 v = h ? make_uint4(r0, d[2], r1, d[3]) : make_uint4(d[0], r0, d[1], r1);
-            *reinterpret_cast<uint4*>(crow_p + (blk0 + q) * kCB + 16 * h) = v;
-          } else if constexpr (FA == 2) {  // 16 codes at 6 bits: 12 bytes of the slot
-            const uint32_t wv[4] = {h ? r0 : d[0], h ? d[2] : r0, h ? r1 : d[1], h ? d[3] : r1};
-            uint32_t pk[3];
-            pack6x16(wv, pk);
+            *reinterpret_cast<uint4*>(crow_p + (blk0 + q) * kCB + 16 * h) = v8[q];
+          } else if constexpr (FA == 2) {
             uint32_t* dst = reinterpret_cast<uint32_t*>(crow_p + (blk0 + q) * kCB + 12 * h);
-            dst[0] = pk[0];
-            dst[1] = pk[1];
-            dst[2] = pk[2];
+            dst[0] = v6[q][0];
+            dst[1] = v6[q][1];
+            dst[2] = v6[q][2];
           } else {
-            const uint2 v = h ? make_uint2(r0 | (d[2] << 16), r1 | (d[3] << 16))
-                              : make_uint2(d[0] | (r0 << 16), d[1] | (r1 << 16));
-            *reinterpret_cast<uint2*>(crow_p + (blk0 + q) * kCB + 8 * h) = v;
+            *reinterpret_cast<uint2*>(crow_p + (blk0 + q) * kCB + 8 * h) = v4[q];
           }
         }
-        __builtin_amdgcn_sched_barrier(0);  // one block at a time: bounded live ranges
+        if (h == 0)
+          *reinterpret_cast<uint16_t*>(p.hs + ((size_t)row0 + tr) * (p.I / 32) + blk0) =
+              (uint16_t)sc;
       }
-      if (h == 0 && tr < nrows)
-        *reinterpret_cast<uint16_t*>(p.hs + ((size_t)row0 + tr) * (p.I / 32) + blk0) =
-            (uint16_t)sc;
     }
   }
 }
