@@ -15,16 +15,19 @@ namespace moe {
 // The work queue of the persistent tiled kernels starts at zero here; each
 // of their launches leaves it at zero when it ends.
 //
-// Chunk list (the tiled geometry launches two row tiles at a time, so that
-// both share their weight rows in L2): an expert's tiles pair up among
-// themselves, so its weights are never split across two chunks; the odd
-// tile left over by an expert pairs with the next expert's leftover. Chunk
-// order: all within-expert pairs (expert order), then the leftover pairs.
+// Chunk list (the tiled geometry launches C row tiles at a time, so that
+// they share their weight rows in L2). C = 2 (256-row tiles): an expert's
+// tiles pair up among themselves, so its weights are never split across two
+// chunks; the odd tile left over by an expert pairs with the next expert's
+// leftover. Chunk order: all within-expert pairs (expert order), then the
+// leftover pairs. C = 4 (128-row tiles): an expert's tiles in groups of
+// four, the last group of each expert padded with empty places (-1).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void build_tiles(const int32_t* __restrict__ offsets, int NE, int BM,
                                             int4* __restrict__ tiles, int* __restrict__ ntiles,
-                                            int2* __restrict__ chunks, int* __restrict__ nchunks,
+                                            int4* __restrict__ chunks, int* __restrict__ nchunks,
                                             int* __restrict__ queue) {
+  const int C = BM == 128 ? 4 : 2;  // row tiles per chunk
   extern __shared__ int start[];  // [NE + 1]
   int m[2], tot[3][2];
 #pragma unroll
@@ -32,11 +35,18 @@ __device__ __forceinline__ void build_tiles(const int32_t* __restrict__ offsets,
     const int e = threadIdx.x + 1024 * q;
     m[q] = e < NE ? (offsets[e + 1] - offsets[e] + BM - 1) / BM : 0;
   }
-  int p0[3], p1[3];  // exclusive prefix of: tiles, within-expert pairs, leftover singles
+  // exclusive prefix of: tiles, within-expert chunks (pairs, or groups of
+  // four with the last one padded), leftover singles (C = 2 only)
+  int p0[3], p1[3];
+  auto per_expert = [&](int k, int mv) {
+    if (k == 0) return mv;
+    if (C == 4) return k == 1 ? (mv + 3) / 4 : 0;
+    return k == 1 ? mv / 2 : mv % 2;
+  };
 #pragma unroll
   for (int k = 0; k < 3; ++k) {
-    const int v0 = k == 0 ? m[0] : (k == 1 ? m[0] / 2 : m[0] % 2);
-    const int v1 = k == 0 ? m[1] : (k == 1 ? m[1] / 2 : m[1] % 2);
+    const int v0 = per_expert(k, m[0]);
+    const int v1 = per_expert(k, m[1]);
     p0[k] = block_exclusive_scan_1024(v0, &tot[k][0]);
     p1[k] = block_exclusive_scan_1024(v1, &tot[k][1]) + tot[k][0];
   }
@@ -50,17 +60,27 @@ __device__ __forceinline__ void build_tiles(const int32_t* __restrict__ offsets,
     start[NE] = total;
     *ntiles = total;
     *nchunks = pairs + (singles + 1) / 2;
-    if (singles & 1) chunks[pairs + singles / 2].y = -1;
+    if (singles & 1) chunks[pairs + singles / 2].y = -1;  // (C = 2; C = 4 has no singles)
   }
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int e = threadIdx.x + 1024 * q;
     if (e >= NE) continue;
     const int ts = q ? p1[0] : p0[0], pr = q ? p1[1] : p0[1], sg = q ? p1[2] : p0[2];
-    for (int j = 0; j < m[q] / 2; ++j) chunks[pr + j] = make_int2(ts + 2 * j, ts + 2 * j + 1);
+    if (C == 4) {
+      const int mq = m[q];
+      for (int j = 0; j < (mq + 3) / 4; ++j) {
+        const int b = 4 * j;
+        chunks[pr + j] = make_int4(ts + b, b + 1 < mq ? ts + b + 1 : -1, b + 2 < mq ? ts + b + 2 : -1,
+                                   b + 3 < mq ? ts + b + 3 : -1);
+      }
+      continue;
+    }
+    for (int j = 0; j < m[q] / 2; ++j) chunks[pr + j] = make_int4(ts + 2 * j, ts + 2 * j + 1, -1, -1);
     if (m[q] & 1) {
       int* c = reinterpret_cast<int*>(&chunks[pairs + sg / 2]);
       c[sg & 1] = ts + m[q] - 1;
+      if ((sg & 1) == 0) c[2] = c[3] = -1;
     }
   }
   __syncthreads();
@@ -95,7 +115,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(const uint16_t* __restrict__
   const bool first = (int)blockIdx.x == nqb;
   const TileArgs& t = first ? t1 : t2;
   build_tiles(offsets, NE, first ? BM1 : BM2, const_cast<int4*>(t.tiles), const_cast<int*>(t.ntiles),
-              const_cast<int2*>(t.chunks), const_cast<int*>(t.nchunks), t.queue);
+              const_cast<int4*>(t.chunks), const_cast<int*>(t.nchunks), t.queue);
 }
 
 static int tile_bound(long A, int NE, int BM) {
@@ -106,7 +126,7 @@ static int tile_bound(long A, int NE, int BM) {
 // Bytes of one tile list (sized for the smallest row tile, 16 rows).
 static size_t tile_list_bytes(long A, int NE) {
   const size_t tb = (size_t)tile_bound(A, NE, 16) + 1;
-  return sizeof(int4) * tb + 16 + sizeof(int2) * tb + 16 + 4 * kQueueInts;
+  return sizeof(int4) * tb + 16 + sizeof(int4) * tb + 16 + 4 * kQueueInts;
 }
 
 // The tile list at `base` for row tiles of BM rows.
@@ -114,7 +134,7 @@ static TileArgs tile_list(uint8_t* base, long A, int NE, int BM) {
   const int tb = tile_bound(A, NE, 16) + 1;
   int4* tiles = reinterpret_cast<int4*>(base);
   int* ntiles = reinterpret_cast<int*>(tiles + tb);
-  int2* chunks = reinterpret_cast<int2*>(ntiles + 4);
+  int4* chunks = reinterpret_cast<int4*>(ntiles + 4);
   int* nchunks = reinterpret_cast<int*>(chunks + tb);
   return TileArgs{tiles, ntiles, tile_bound(A, NE, BM), 0, 1, chunks, nchunks, nchunks + 4};
 }
@@ -131,7 +151,7 @@ GemmWorkspace gemm_workspace(int T, int H, int I, int NE, int k_total, int fmt) 
   w.off[2] = o;  o += al(A * I * bits / 8);
   w.off[3] = o;  o += mx ? al(A * (I / 32)) : 0;
   // two tile lists (stage 1's and, when stage 2 runs another geometry,
-  // stage 2's), each: tiles (int4 x bound), count, chunks (int2 x bound),
+  // stage 2's), each: tiles (int4 x bound), count, chunks (int4 x bound),
   // count, work queue
   w.off[4] = o;  o += 2 * al(tile_list_bytes((long)A, NE));
   w.off[5] = o;
@@ -171,7 +191,8 @@ static Geometry geometry(const GemmArgs& a) {
     return Geometry{many_bf, many_bf, false};
   }
   const bool rows = A >= (long)kTiledMinRows * a.NE;
-  const bool many = rows && (size_t)max_lds_per_block() >= tiled_lds_bytes(a.fmt);
+  const bool many =
+      rows && (size_t)max_lds_per_block() >= tiled_lds_bytes(a.fmt, tiled_rows(A, a.NE));
   const bool s2_tiled = many && tiled_ok(a.H, a.I);
   const bool s2_short = rows && !s2_tiled && short_k_ok(a.I) && a.H % 256 == 0 &&
                         (size_t)max_lds_per_block() >= short_lds_bytes(a.fmt, a.I);
@@ -187,10 +208,11 @@ bool fused_combine_ok(const GemmArgs& a) {
 static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int stages,
                                   Geometry g, hipStream_t s) {
   const bool bf = a.fmt == kFmtBf16;
-  const int BM1 = g.s1_tiled ? (bf ? bf16_rows() : tiled_rows()) : (bf ? bf16_stream_rows() : 16);
-  const int BM2 = g.s2_tiled ? (bf ? bf16_rows() : tiled_rows())
-                             : (g.s2_short ? short_rows() : (bf ? bf16_stream_rows() : 16));
   const long A = (long)a.T * a.k_total;
+  const int TR = tiled_rows(A, a.NE);
+  const int BM1 = g.s1_tiled ? (bf ? bf16_rows() : TR) : (bf ? bf16_stream_rows() : 16);
+  const int BM2 = g.s2_tiled ? (bf ? bf16_rows() : TR)
+                             : (g.s2_short ? short_rows() : (bf ? bf16_stream_rows() : 16));
   uint8_t* lists = a.ws + w.off[4];
   const TileArgs t1 = tile_list(lists, A, a.NE, BM1);
   const TileArgs t2 = BM2 == BM1 ? t1 : tile_list(lists + (w.off[5] - w.off[4]) / 2, A, a.NE, BM2);
@@ -228,7 +250,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p1.k_total = a.k_total;
     p1.t = t1;
     if (bf) (g.s1_tiled ? launch_s1_bf16 : launch_s1_bf16_stream)(p1, t1.mt_bound, s);
-    else if (g.s1_tiled) launch_s1_tiled(p1, t1.mt_bound, a.fmt, s);
+    else if (g.s1_tiled) launch_s1_tiled(p1, t1.mt_bound, a.fmt, TR, s);
     else launch_s1_stream(p1, t1.mt_bound, a.fmt, s);
   }
   if (stages & 4) {
@@ -244,7 +266,7 @@ static hipError_t launch_geometry(const GemmArgs& a, const GemmWorkspace& w, int
     p2.t = t2;
     if (a.out) launch_s2c_stream(S2CArgs{p2, a.topk_w, a.out, a.T, a.k_total}, a.fmt, s);
     else if (bf) (g.s2_tiled ? launch_s2_bf16 : launch_s2_bf16_stream)(p2, t2.mt_bound, s);
-    else if (g.s2_tiled) launch_s2_tiled(p2, t2.mt_bound, a.fmt, s);
+    else if (g.s2_tiled) launch_s2_tiled(p2, t2.mt_bound, a.fmt, TR, s);
     else if (g.s2_short) launch_s2_short(p2, t2.mt_bound, a.fmt, s);
     else launch_s2_stream(p2, t2.mt_bound, a.fmt, s);
   }

@@ -105,7 +105,7 @@ struct TileArgs {
   int mt_bound;         // tiles the grid was sized for
   int n_ntiles;         // N tiles per expert
   int ngroup;           // consecutive N tiles per group (divides n_ntiles)
-  const int2* chunks;   // pairs of row tiles launched together (-1: none)
+  const int4* chunks;   // row tiles launched together: 2 (256-row tiles) or 4 (-1: none)
   const int* nchunks;   // number of valid chunks
   int* queue;           // work tickets of the persistent geometry: [8] per XCD, [8] finished
 };

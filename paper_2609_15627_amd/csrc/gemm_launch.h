@@ -30,13 +30,15 @@ int bf16_stream_rows();
 void launch_s1_bf16_stream(const S1Args& p, long mt, hipStream_t s);
 void launch_s2_bf16_stream(const S2Args& p, long mt, hipStream_t s);
 
-// LDS-tiled geometry (many rows per expert): row tiles of tiled_rows() rows.
-int tiled_rows();
-size_t tiled_lds_bytes(int fa);
+// LDS-tiled geometry (many rows per expert): row tiles of tiled_rows(A, NE)
+// rows (128 or 256, by the average rows per expert of A assignments over NE
+// experts); the launches take the same row count.
+int tiled_rows(long A, int NE);
+size_t tiled_lds_bytes(int fa, int rows);
 bool tiled_ok(int H, int I);  // both stages (K = H and K = I) fit the tiled K loop
 bool tiled_k_ok(int K);       // a K extent fits the tiled K loop
-void launch_s1_tiled(const S1Args& p, long mt, int fa, hipStream_t s);
-void launch_s2_tiled(const S2Args& p, long mt, int fa, hipStream_t s);
+void launch_s1_tiled(const S1Args& p, long mt, int fa, int rows, hipStream_t s);
+void launch_s2_tiled(const S2Args& p, long mt, int fa, int rows, hipStream_t s);
 
 // Short-K geometry of stage 2 (K = I of 128 or 256, many rows per expert):
 // row tiles of short_rows() rows, the whole K extent of a tile in LDS.
