@@ -40,8 +40,8 @@ def log(msg):
 # only reused while these are unchanged.
 KERNEL_SOURCES = {
     "s1_stream2_kernel": ["gemm_stream.hip", "gemm_common.h", "gemm_launch.h", "moe_dev.h"],
-    "s1_tiled_kernel": ["gemm_tiled.hip", "gemm_common.h", "gemm_launch.h", "quant_dev.h",
-                        "moe_dev.h"],
+    "s1_tiled_kernel": ["gemm_tiled.hip", "gemm_tiled_body.h", "gemm_common.h", "gemm_launch.h",
+                        "quant_dev.h", "moe_dev.h"],
 }
 PROFILES = os.path.join(ROOT, "profiles")
 
