@@ -237,10 +237,10 @@ def small_case(T, H, I, E, k, S, seed, routing="normal"):
     (64, 1024, 256, 64, 8, 1),    # decode-like spread
     (3, 256, 128, 8, 8, 1),       # k = E
     (1, 128, 128, 1, 1, 0),       # smallest shape
-    (300, 1024, 512, 4, 2, 1),    # tiled geometry: ~150-300 rows per expert, ragged tiles
-    (600, 512, 1024, 2, 1, 0),    # tiled geometry: a full 256-row tile plus a ragged one
+    (300, 1024, 512, 4, 2, 1),    # tiled geometry, 256-row tiles: ~150-300 rows per expert, ragged
+    (600, 512, 1024, 2, 1, 0),    # tiled geometry, 128-row tiles (2 per CU): full tiles + a ragged one
     (130, 512, 512, 2, 1, 0),     # tiled geometry: ~65 rows per expert, partial row blocks
-    (400, 512, 256, 4, 2, 0),     # tiled stage 1, short-K stage 2 (I = 256, like the TP shard)
+    (400, 512, 256, 4, 2, 0),     # tiled stage 1 (128-row tiles), short-K stage 2 (I = 256)
     (300, 1024, 384, 4, 2, 1),    # tiled stage 1, streaming stage 2 (I = 384) and a shared expert
     (700, 768, 128, 5, 2, 1),     # streaming stage 1 (H = 768), short-K stage 2 with K = 128
     (170, 1024, 256, 3, 2, 0),    # short-K stage 2: tiles of 128 rows and ragged ones under 64
@@ -342,9 +342,10 @@ def test_empty_tokens(m):
 
 
 # Sorted-row positions inside an expert that the tiled kernels treat
-# differently: first and last rows of a 256-row tile and of each 32-row
-# block, the first row of the second wave half (row 128), the first rows of a
-# ragged tail tile; the last row of the expert is added per expert.
+# differently: first and last rows of a row tile (128 or 256 rows, by the
+# shape) and of each 32-row block, the first rows of the other wave half's
+# blocks, the first rows of a ragged tail tile; the last row of the expert is
+# added per expert.
 ROW_CLASSES = (0, 31, 32, 127, 128, 129, 200, 255, 256, 257, 300, 383, 384, 511, 512)
 
 

@@ -29,7 +29,7 @@ def m():
 @pytest.mark.parametrize("fmt", ["e4m3", "e2m3", "e2m1", "bf16"])
 @pytest.mark.parametrize("T,H,I,variants", [
     (5, 256, 128, (1, 5)),       # weight-streaming geometry (MX / BF16 contract)
-    (300, 512, 512, (2, 3)),     # LDS-tiled geometry: a full 256-row tile and a ragged one
+    (300, 512, 512, (2, 3)),     # LDS-tiled geometry: full row tiles and a ragged one
     (300, 1024, 256, (6, 3)),    # tiled stage 1, short-K stage 2 (I = 256)
     (300, 512, 384, (4, 3)),     # tiled stage 1, streaming stage 2 (I = 384)
     (300, 768, 128, (6, 3)),     # streaming stage 1 (H = 768), short-K stage 2 (I = 128)
