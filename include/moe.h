@@ -392,6 +392,17 @@ const char* moe_status_string(moe_status s);
 /* MOE_VARIANT_* chosen by the calling thread's last moe_fp4_grouped_gemm. */
 int moe_last_variant(void);
 
+/* Row-tile size of the LDS-tiled geometry (MOE_VARIANT_TILED and the tiled
+ * stage 1 of MOE_VARIANT_MIXED and MOE_VARIANT_SHORT). Not an operation
+ * of the paper: a tuning and testing control. rows = 128: tiles of 128 rows,
+ * two workgroups per CU; 256: tiles of 256 rows, one workgroup per CU;
+ * 0 (the default): 128 when T * k_total / NE >= 192, else 256. Both give the
+ * same bits (every output's K reduction is the same sequence of products).
+ * Process-wide: it affects every later call on every thread and device; a
+ * call that overlaps it may use either size. Other values return
+ * MOE_ERR_INVALID_ARG and leave the setting unchanged. */
+moe_status moe_set_tiled_rows(int rows);
+
 /* One block-scaled matrix-core product, D = (A * 2^(sa-127)) . (B * 2^(sb-127))^T
  * per 32-element K block, using the same operand and scale placement as the
  * grouped GEMM. Used to check that placement against the oracle.

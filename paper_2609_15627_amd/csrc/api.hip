@@ -81,6 +81,12 @@ const char* moe_status_string(moe_status s) {
 
 int moe_last_variant(void) { return g_last_variant; }
 
+moe_status moe_set_tiled_rows(int rows) {
+  if (rows != 0 && rows != 128 && rows != 256) return MOE_ERR_INVALID_ARG;
+  moe::set_tiled_rows(rows);
+  return MOE_OK;
+}
+
 moe_status moe_router_logits(const uint16_t* x, const uint16_t* w_router, int T, int H, int E,
                              float* logits, void* stream) {
   if (T < 0 || H <= 0 || H % 8 || E < 1 || E > MOE_MAX_EXPERTS) return MOE_ERR_INVALID_ARG;

@@ -64,6 +64,9 @@
 #include "gemm_common.h"
 #include "gemm_launch.h"
 #include "quant_dev.h"
+#include "moe_launch.h"
+
+#include <atomic>
 
 namespace moe {
 
@@ -85,7 +88,16 @@ namespace t128 {
 // 256-row tiles with the row blocks split between the wave halves.
 constexpr long kRows128 = 192;
 
-int tiled_rows(long A, int NE) { return NE > 0 && A >= kRows128 * NE ? 128 : 256; }
+// 0: automatic; 128 or 256: forced (moe_set_tiled_rows).
+static std::atomic<int> g_tiled_rows{0};
+
+void set_tiled_rows(int rows) { g_tiled_rows.store(rows, std::memory_order_relaxed); }
+
+int tiled_rows(long A, int NE) {
+  const int forced = g_tiled_rows.load(std::memory_order_relaxed);
+  if (forced) return forced;
+  return NE > 0 && A >= kRows128 * NE ? 128 : 256;
+}
 
 size_t tiled_lds_bytes(int fa, int rows) {
   return rows == 128 ? t128::tiled_lds_bytes(fa) : t256::tiled_lds_bytes(fa);

@@ -62,6 +62,8 @@ struct GemmArgs {
 // stages: bit 0 = activation quantisation + tile list, bit 1 = gate/up
 // (stage 1), bit 2 = down (stage 2). Writes the geometry variant used
 // (MOE_VARIANT_*) to *variant.
+// Row-tile size of the LDS-tiled geometry: 0 (automatic), 128 or 256.
+void set_tiled_rows(int rows);
 hipError_t launch_grouped_gemm(const GemmArgs& a, int stages, hipStream_t s, int* variant);
 // Whether stage 2 can run fused with the combine for these dims (streaming
 // geometry chosen and every row's 16-column result fits one workgroup's LDS).

@@ -36,6 +36,7 @@ _SIGNATURES = {
     "moe_permute": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _P, _SZ, _P]),
     "moe_quantize_act": (_I, [_P, _I, _I, _I, _P, _P, _P]),
     "moe_pack_fp4_weights": (_I, [_P, _P, ctypes.c_long, _I, _P]),
+    "moe_set_tiled_rows": (_I, [_I]),
     "moe_fp4_grouped_gemm_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I]),
     "moe_fp4_grouped_gemm_workspace_layout": (_I, [_I, _I, _I, _I, _I, _I, ctypes.POINTER(_SZ)]),
     "moe_fp4_grouped_gemm": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P,
@@ -228,6 +229,12 @@ def moe_quantize_act(x, fmt="e4m3", codes=None, scales=None, stream=None):
     _check(lib.moe_quantize_act(_ptr(x), rows, K, ACT_FORMATS[fmt], _ptr(codes), _ptr(scales),
                                 _stream(stream)), "moe_quantize_act")
     return codes, scales
+
+
+def set_tiled_rows(rows):
+    """Row-tile size of the LDS-tiled geometry: 128, 256, or 0 for the
+    automatic choice (``moe_set_tiled_rows``; process-wide, same bits)."""
+    _check(lib.moe_set_tiled_rows(int(rows)), "moe_set_tiled_rows")
 
 
 def moe_pack_fp4_weights(w, out=None, stream=None):

@@ -206,6 +206,19 @@ def test_noalloc_gemm_rejects_before_touching_the_gpu(m):
     assert call(0) == m.MOE_OK                                       # empty batch: nothing enqueued
 
 
+def test_set_tiled_rows_validation(m):
+    """The row-tile control takes 0, 128 or 256 and rejects anything else
+    (host only)."""
+    L = m.lib
+    try:
+        for bad in (-1, 1, 64, 192, 512):
+            assert L.moe_set_tiled_rows(bad) == 1
+        for ok in (128, 256, 0):
+            assert L.moe_set_tiled_rows(ok) == 0
+    finally:
+        L.moe_set_tiled_rows(0)
+
+
 def test_pack_fp4_weights_validation(m):
     """The weight packing call rejects shapes outside its layout and
     overlapping or misaligned buffers on the host."""

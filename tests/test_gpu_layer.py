@@ -279,6 +279,31 @@ def test_tiled_geometry_skewed(m):
     check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T))
 
 
+@pytest.mark.parametrize("fmt", ["e4m3", "e2m1"])
+def test_tiled_row_tile_sizes_bit_identical(m, fmt):
+    """The two arrangements of the LDS-tiled geometry (row tiles of 128 rows,
+    two workgroups per CU, chunks of four tiles; of 256 rows, one workgroup
+    per CU, chunks of two), forced through moe_set_tiled_rows on a shape whose
+    experts hold ~360 rows (three 128-row tiles or two 256-row tiles, the last
+    one ragged): outputs and partials bit-identical, both at the oracle bar."""
+    cfg, inp = small_case(600, 512, 1024, 4, 2, 1, seed=11)
+    log(f"tiled row-tile sizes {fmt}")
+    weights = gc.dev_expert_weights(inp.weights)
+    res = {}
+    try:
+        for rows in (128, 256):
+            m.set_tiled_rows(rows)
+            layer, out = run_layer(m, cfg, gc.to_dev_bf16(inp.x), weights, logits=inp.logits,
+                                   fmt=fmt)
+            assert m.moe_last_variant() == m.VARIANT_TILED
+            check_against_oracle(cfg, inp, layer, out, np.arange(cfg.T), fmt)
+            res[rows] = (out.clone(), layer.partials.clone())
+    finally:
+        m.set_tiled_rows(0)
+    assert torch.equal(res[128][0], res[256][0])
+    assert torch.equal(res[128][1], res[256][1])
+
+
 def test_tiny_config_with_router(m):
     """The tiny workload end to end, logits from the bf16 router weights."""
     cfg = synth.CONFIGS["tiny"]
