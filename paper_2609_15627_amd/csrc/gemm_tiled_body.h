@@ -97,11 +97,12 @@ __device__ __forceinline__ void t_bslot(int ci, int lane, int* row, int* chunk) 
   *chunk = (lane % 4) ^ ((*row >> 2) & 3);
 }
 
-// Activation rows a wave moves by DMA: LDS positions t_arow0(w) .. + 63,
-// inside the 128 positions the wave multiplies (128 (w & 1) ..), which hold
-// two of its wave half's row blocks, so a wave without rows to multiply (a
-// tile of at most 32 rows, w odd) moves no activation data either. Its DMA
-// instruction i fills activation tile chunk t_aci.
+// Activation rows a wave moves by DMA: LDS positions t_arow0(w) ..
+// + TBM / 4 - 1, inside the TBM / 2 positions the wave multiplies
+// ((TBM / 2) (w & 1) ..), which hold its wave half's row blocks, so a wave
+// without rows to multiply (a tile of at most 32 rows, w odd) moves no
+// activation data either. Its DMA instruction i fills activation tile chunk
+// t_aci.
 __device__ __forceinline__ int t_arow0(int w) { return (TBM / 2) * (w & 1) + (TBM / 4) * (w >> 1); }
 
 // DMA of a wave's activation scale pieces (rows t_arow0(w) ..): one per lane,
